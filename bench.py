@@ -1,0 +1,214 @@
+"""Benchmark of the verification hot path on one MI355X.
+
+One step = one spec_verify call over a batch of B=256 rows, K=3 draft steps,
+V=151936 (bf16 logits): temperature softmax of 4 target and 3 draft rows per
+batch row, accept tests, accept length, residual / bonus resampling and the
+per-step overlap sum_v min(p, q).  Inputs are synthetic (rollout-shaped
+recipe, see paper_2606_12370_amd/workloads.py) and already resident in HBM;
+two input copies alternate so the 256 MB last-level cache cannot serve a
+step from the previous one.
+
+Prints ONE JSON line.  `value` = verified draft tokens/s = B*K / step time.
+`roofline` relates the algorithmic bytes of one launch (the logits it must
+read once) to the launch time measured with HIP events on the launch stream.
+`cpu_baseline` times the float64 CPU oracle on a bounded sample of rows of
+the same workload.  The fused TV-loss forward+backward on the training
+workload (N=16384 positions x 3 steps) is timed too and reported under
+`tv_loss` (not part of `value`).
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_12370_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(key, launches_bytes):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(key)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(d_host, K, budget_s=12.0):
+    """The float64 oracle on whole rows of the benchmark batch until about
+    budget_s of CPU time is spent."""
+    import oracle
+    from paper_2606_12370_amd import workloads as W
+    tgt, drf, ids, T = d_host
+    rows_done, t_used = 0, 0.0
+    B = tgt.shape[0]
+    while rows_done < B and t_used < budget_s:
+        sl = slice(rows_done, min(B, rows_done + 2))
+        zt = W.to_float64(tgt[sl], W.BF16)
+        zd = W.to_float64(drf[sl], W.BF16)
+        t0 = time.perf_counter()
+        oracle.verify_ref(zt, zd, ids[sl], T[sl], 0, 0, rows=np.arange(sl.start, sl.stop))
+        t_used += time.perf_counter() - t0
+        rows_done = sl.stop
+    return {
+        "value": rows_done * K / t_used,
+        "unit": "verified draft tokens/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "%d of %d rows of the B=256 K=3 V=151936 bf16 batch, float64 NumPy oracle, "
+                  "one thread, %.1f s" % (rows_done, B, t_used),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-tv", action="store_true")
+    ap.add_argument("--tv-steps", type=int, default=3)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (the verification "
+              "rows are independent and would shard over GPUs with no exchange; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_12370_amd import binding
+    from paper_2606_12370_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    binding.load_library()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    cfg = W.CONFIGS["verify_bf16_b256_k3_v151936"]
+    B, K, V = cfg["B"], cfg["K"], cfg["V"]
+    log("generating inputs B=%d K=%d V=%d bf16" % (B, K, V))
+    copies = [W.verify_inputs_torch(B, K, V, W.BF16, cfg["gen"], cfg["seed"] + 100 * c) for c in range(2)]
+    outs = [{
+        "accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+        "emitted": torch.empty((B, K + 1), dtype=torch.int32, device=dev),
+        "overlap": torch.empty((B, K), dtype=torch.float32, device=dev),
+    } for _ in copies]
+    ws = binding.workspace(binding.verify_workspace_size(B, K, V, torch.bfloat16), dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(it):
+        c = copies[it % len(copies)]
+        binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, offset=0, ws=ws,
+                       out=outs[it % len(copies)])
+
+    for it in range(args.warmup):
+        step(it)
+    torch.cuda.synchronize()
+    log("timing %d steps" % args.steps)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for it in range(args.steps):
+        step(it)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    acc = outs[0]["accept_len"].float()
+    assert float(acc.min()) >= 0
+    algo_bytes = B * (2 * K + 1) * V * 2 + B * K * 4 + B * 4 + B * (K + 1) * 4 + B * 4 + B * K * 4
+    achieved = algo_bytes / (ms_per_step * 1e-3) / 1e9
+    traffic = measured_traffic("verify_bf16_b256_k3_v151936", algo_bytes)
+    result = {
+        "metric": "verified draft tokens/sec at B=256,K=3,V=151936 bf16; % of HBM peak BW",
+        "value": B * K / (ms_per_step * 1e-3),
+        "unit": "verified draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 in, f32 math",
+        "data": "synthetic (seeded rollout-shaped logits generated on the GPU)",
+        "config": {"workload": "verify_bf16_b256_k3_v151936", "B": B, "K": K, "V": V,
+                   "temperature": "per row, 1.0", "input_copies": len(copies)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
+        "emitted_tokens_per_s": float((acc + 1).sum()) / (ms_per_step * 1e-3),
+        "mean_accept_len": float(acc.mean()),
+        "wall_s_timed_region": wall,
+    }
+    del copies
+    torch.cuda.empty_cache()
+
+    if not args.no_tv:
+        tcfg = W.CONFIGS["tv_bf16_n16384_k3_v151936"]
+        N, KT, VT = tcfg["N"], tcfg["K"], tcfg["V"]
+        log("generating TV inputs N=%d K=%d V=%d bf16" % (N, KT, VT))
+        td = W.tv_inputs_torch(N, KT, VT, W.BF16, tcfg["seed"])
+        grad = torch.empty((N, KT, VT), dtype=torch.float32, device=dev)
+        tws = binding.workspace(binding.tv_workspace_size(N, KT, VT, torch.bfloat16), dev)
+        binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.tv_steps):
+            binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        tv_ms = ev0.elapsed_time(ev1) / args.tv_steps
+        tv_bytes = N * KT * VT * (2 + 2 + 4) + N * KT * 4 + 4
+        tv_ach = tv_bytes / (tv_ms * 1e-3) / 1e9
+        result["tv_loss"] = {
+            "workload": "tv_bf16_n16384_k3_v151936", "mode": "prod", "ms_per_call": tv_ms,
+            "positions_per_s": N / (tv_ms * 1e-3),
+            "roofline": {"bound": "hbm", "achieved": tv_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": tv_ach / HBM_PEAK_GBS,
+                         "traffic": measured_traffic("tv_bf16_n16384_k3_v151936", tv_bytes)},
+        }
+        del td, grad
+
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        c0 = W.verify_inputs_torch(B, K, V, W.BF16, cfg["gen"], cfg["seed"])
+        nrow = 64
+        tgt = c0["target"][:nrow].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        drf = c0["draft"][:nrow].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        ids = c0["ids"][:nrow].cpu().numpy()
+        T = c0["temperature"][:nrow].cpu().numpy().astype(np.float64)
+        result["cpu_baseline"] = cpu_baseline((tgt, drf, ids, T), K)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,157 @@
+/*
+ * specverify.h — C ABI of the MI355X (gfx950) speculative-verification and
+ * TV-loss library (libspecverify.so).
+ *
+ * Method: "Breaking Entropy Bounds: Accelerating RL Training via MTP with
+ * Rejection Sampling".  Sec. 2.2 (Eq. reject_sample) and App. G.1 (Alg.
+ * rs_multinomial) define chain rejection-sampling verification of K draft
+ * tokens; Sec. 4.1 (Eqs. tv_loss, tv_grad), App. A and Sec. 4.2 (Eq. e2e_tv)
+ * define the TV loss, its gradient and the end-to-end multi-step TV loss.
+ *
+ * Conventions shared by every entry point
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  The
+ *    library allocates no device or host memory and keeps no mutable state
+ *    between calls other than what lives in the caller's workspace.
+ *  - The last dimension (vocabulary, length V) must be contiguous.  Other
+ *    dimensions take element strides, so shifted views of larger tensors can
+ *    be passed without copies.
+ *  - Work is only enqueued on `stream` (a hipStream_t passed as void*, NULL =
+ *    the null stream); no call synchronises with the host.
+ *  - Host-checkable argument errors are returned synchronously before any
+ *    work is enqueued.  Misaligned pointers or strides are not an error:
+ *    they select element-wise loads instead of 16-byte vector loads.
+ *  - The workspace is scratch memory: it needs no initialisation, each call
+ *    overwrites what it reads, and no state is carried from one call to the
+ *    next.  Calls that share a workspace must not run concurrently (enqueue
+ *    them on one stream).
+ *  - Each call is a short fixed sequence of kernel launches on `stream`
+ *    (spec_verify: 3, spec_tv_loss_fwd_bwd: 4); no launch waits on another
+ *    workgroup, so any number of resident workgroups is enough.
+ *  - Entry points are thread-safe; each call is independent.
+ *  - Logits are bfloat16 (raw 16-bit patterns) or float32.  Arithmetic is
+ *    float32 per element with float64 accumulation across vectors, threads
+ *    and workgroups.
+ */
+#ifndef SPECVERIFY_H
+#define SPECVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPEC_VERSION 1
+#define SPEC_MAX_K 8 /* largest number of draft steps K */
+
+typedef enum { SPEC_F32 = 0, SPEC_BF16 = 1 } spec_dtype;
+
+typedef enum {
+  SPEC_OK = 0,
+  SPEC_EINVAL = 1,       /* bad pointer, size, stride, temperature, mode */
+  SPEC_EUNSUPPORTED = 2, /* dtype or K outside what the library handles */
+  SPEC_EWORKSPACE = 4,   /* workspace NULL or smaller than *_workspace_size */
+  SPEC_EHIP = 5          /* the HIP runtime reported an error (launch, device query) */
+} spec_status;
+
+typedef enum {
+  SPEC_TV_E2E = 0,     /* Sec. 4.2 Eq. e2e_tv: L = 1 - (1/K) sum_j prod_{i<=j} alpha_i        */
+  SPEC_TV_PROD = 1,    /* L = -prod_k alpha_k (negated probability that all K drafts pass)  */
+  SPEC_TV_PER_STEP = 2 /* Sec. 4.1 Eq. tv_loss averaged over steps: (1/K) sum_k (1 - alpha_k) */
+} spec_tv_mode;
+
+/* Bytes of workspace spec_verify needs for this shape (0 on invalid sizes). */
+size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
+
+/*
+ * spec_verify — chain rejection-sampling verification of K draft tokens for B
+ * independent batch rows (Sec. 2.2 Eq. reject_sample; App. G.1 Alg.
+ * rs_multinomial).
+ *
+ * For row b, with T = temperature[b] (or temperature_scalar):
+ *   p_i = softmax(target[b, i, :] / T), i = 0..K (row K: bonus position after the last draft)
+ *   q_i = softmax(draft[b, i, :] / T),  i = 0..K-1
+ *   step i accepts x_i = draft_ids[b, i] iff u_i * q_i(x_i) < p_i(x_i)
+ *   n = first rejected step (K if none); accept_len[b] = n
+ *   emitted[b, 0..n-1] = x_0..x_{n-1}
+ *   emitted[b, n] = smallest v with C(v) > u' * Z, C = cumulative sum (vocabulary
+ *       order) of r = max(0, p_n - q_n) if n < K, else of r = p_K; Z = sum r
+ *       (if Z is exactly 0 the sample is drawn from p_n)
+ *   emitted[b, n+1..K] = -1
+ *   overlap[b, i] = sum_v min(p_i(v), q_i(v)) = 1 - d_TV(p_i, q_i) for every i < K
+ * Uniforms: block = Philox4x64-10(counter = (b, i, offset, 0), key = (seed, 0))
+ *   (Salmon et al., SC'11); u_i = (word0 >> 40) * 2^-24, the resample uniform of
+ *   the emitting step n is (word1 >> 40) * 2^-24 of the block at (b, n).
+ *
+ * target_logits  [B, K+1, V] element strides (t_stride_b, t_stride_k), dtype
+ * draft_logits   [B, K,   V] element strides (d_stride_b, d_stride_k), dtype
+ * draft_ids      [B, K] int32, contiguous; ids sampled from q_i
+ * temperature    [B] float32 device array, or NULL to use temperature_scalar
+ *                (which must then be finite and > 0)
+ * accept_len     [B] int32 out
+ * emitted_ids    [B, K+1] int32 out, contiguous
+ * overlap        [B, K] float32 out (may be NULL)
+ * p_at_draft, q_at_draft  [B, K] float32 out: p_i(x_i), q_i(x_i) (may be NULL)
+ * logz_target    [B, K+1] float32 out: natural-log partition function of z/T (may be NULL)
+ * logz_draft     [B, K]   float32 out (may be NULL)
+ * workspace      device memory of at least spec_verify_workspace_size bytes
+ *
+ * Row data errors (NaN or +inf logits, a row that is all -inf, a draft id
+ * outside [0, V), a per-row temperature that is not finite and > 0) do not
+ * fail the call: that row gets accept_len = -1, emitted = -1 and NaN in every
+ * float output.  -inf logits are legal (probability 0).
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= B, B*(K+1) < 2^31.
+ */
+spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                        const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                        spec_dtype dtype, int B, int K, int V,
+                        const int32_t* draft_ids,
+                        const float* temperature, float temperature_scalar,
+                        uint64_t seed, uint64_t offset,
+                        int32_t* accept_len, int32_t* emitted_ids,
+                        float* overlap, float* p_at_draft, float* q_at_draft,
+                        float* logz_target, float* logz_draft,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spec_tv_loss_fwd_bwd needs (0 on invalid sizes). */
+size_t spec_tv_workspace_size(int N, int K, int V, spec_dtype dtype);
+
+/*
+ * spec_tv_loss_fwd_bwd — fused TV-loss forward and gradient w.r.t. the draft
+ * logits (Sec. 4.1 Eqs. tv_loss / tv_grad, App. A, App. F; Sec. 4.2 Eq. e2e_tv).
+ *
+ * For position n and draft step k:
+ *   p = softmax(target[n, k, :] / T) (detached), q = softmax(draft[n, k, :] / T)
+ *   alpha[n, k] = sum_v min(p_v, q_v),  S[n, k] = sum_v 1[q_v <= p_v] q_v
+ *   L_n by `mode` (see spec_tv_mode); g[n, k] = d L_n / d alpha[n, k]
+ *   loss = scale * sum_n L_n
+ *   grad_draft[n, k, j] = scale * g[n, k] * (1/T) * q_j * (1[q_j <= p_j] - S[n, k])
+ *
+ * target_logits, draft_logits  [N, K, V], element strides (stride_n, stride_k)
+ * temperature    finite and > 0 (one value for all positions)
+ * loss           [1] float32 out (device)
+ * overlap        [N, K] float32 out (may be NULL)
+ * grad_draft     [N, K, V] float32 out, contiguous; NULL = forward only
+ * NaN or infinite logits propagate as NaN into that position's loss and
+ * gradient (no per-position status).
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= N, N*K < 2^31.
+ */
+spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,
+                                 const void* draft_logits, int64_t d_stride_n, int64_t d_stride_k,
+                                 spec_dtype dtype, int N, int K, int V,
+                                 float temperature, spec_tv_mode mode, float scale,
+                                 float* loss, float* overlap, float* grad_draft,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* spec_status_string(spec_status s);
+
+/* SPEC_VERSION of the built library. */
+int spec_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECVERIFY_H */

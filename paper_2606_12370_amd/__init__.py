@@ -8,7 +8,7 @@ first call of :func:`verify` or :func:`tv_loss_fwd_bwd` does.
 """
 
 __all__ = ["verify", "tv_loss_fwd_bwd", "verify_workspace_size", "tv_workspace_size",
-           "library_path", "load_library"]
+           "library_path", "load_library", "workspace", "SpecError"]
 
 
 def __getattr__(name):

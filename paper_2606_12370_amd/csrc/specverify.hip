@@ -1,0 +1,232 @@
+// specverify.hip — C ABI of libspecverify.so: argument validation, workspace
+// layout and the launch sequences behind the entry points declared in
+// include/specverify.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstddef>
+#include <cstdint>
+
+#include "specverify.h"
+#include "sv_device.h"
+#include "tv_kernel.h"
+#include "verify_kernel.h"
+
+namespace {
+
+using sv::BF16;
+using sv::F32;
+
+// Chunk geometry: a chunk is NT tiles of one 16-byte vector per thread,
+// 16384 elements for both dtypes, read S tiles per step.
+constexpr int kNtBf16 = 8;
+constexpr int kNtF32 = 16;
+constexpr int kStep = 4;
+
+int epv_of(spec_dtype dt) { return dt == SPEC_BF16 ? BF16::EPV : F32::EPV; }
+int nt_of(spec_dtype dt) { return dt == SPEC_BF16 ? kNtBf16 : kNtF32; }
+size_t esize_of(spec_dtype dt) { return dt == SPEC_BF16 ? 2 : 4; }
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Geometry {
+  int ntiles = 0;  // tiles per row
+  int C = 0;       // chunks per row
+};
+
+Geometry geometry(int V, spec_dtype dt) {
+  Geometry g;
+  const int64_t tile = static_cast<int64_t>(sv::kThreads) * epv_of(dt);
+  g.ntiles = static_cast<int>((V + tile - 1) / tile);
+  g.C = (g.ntiles + nt_of(dt) - 1) / nt_of(dt);
+  return g;
+}
+
+bool verify_sizes_ok(int B, int K, int V, spec_dtype dt) {
+  if (B < 1 || K < 1 || K > SPEC_MAX_K || V < 1) return false;
+  const int64_t rows = static_cast<int64_t>(B) * (2 * K + 1);
+  return rows * geometry(V, dt).C < (int64_t{1} << 31);
+}
+
+bool tv_sizes_ok(int N, int K, int V, spec_dtype dt) {
+  if (N < 1 || K < 1 || K > SPEC_MAX_K || V < 1) return false;
+  const int64_t rows = static_cast<int64_t>(N) * 2 * K;
+  return rows * geometry(V, dt).C < (int64_t{1} << 31);
+}
+
+struct VerifyLayout {
+  size_t stats = 0, pairs = 0, total = 0;
+};
+VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt) {
+  VerifyLayout L;
+  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  size_t off = 0;
+  L.stats = off; off = align_up(off + static_cast<size_t>(B) * (2 * K + 1) * C * sizeof(sv::RowStat), 256);
+  L.pairs = off; off = align_up(off + static_cast<size_t>(B) * K * C * sizeof(sv::PairStat), 256);
+  L.total = off;
+  return L;
+}
+
+struct TvLayout {
+  size_t stats = 0, pairs = 0, loss = 0, total = 0;
+};
+TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
+  TvLayout L;
+  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  size_t off = 0;
+  L.stats = off; off = align_up(off + static_cast<size_t>(N) * 2 * K * C * sizeof(sv::RowStat), 256);
+  L.pairs = off; off = align_up(off + static_cast<size_t>(N) * K * C * sizeof(sv::TvPair), 256);
+  L.loss = off; off = align_up(off + static_cast<size_t>(N) * sizeof(double), 256);
+  L.total = off;
+  return L;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool rows_vec_aligned(const void* base, int64_t s0, int64_t s1, size_t esize) {
+  return aligned16(base) && ((s0 * static_cast<int64_t>(esize)) % 16 == 0) &&
+         ((s1 * static_cast<int64_t>(esize)) % 16 == 0);
+}
+
+template <class E, int NT>
+spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) {
+  const int C = a.rows.C;
+  hipLaunchKernelGGL((sv::row_stats_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(rows * C)),
+                     dim3(sv::kThreads), 0, s, a.rows, const_cast<sv::RowStat*>(a.stats));
+  hipLaunchKernelGGL((sv::pair_pass_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(int64_t{a.B} * a.K * C)),
+                     dim3(sv::kThreads), 0, s, a);
+  hipLaunchKernelGGL((sv::finish_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s,
+                     a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
+spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
+  const int64_t units = int64_t{a.N} * a.K;
+  const int C = a.rows.C;
+  hipLaunchKernelGGL((sv::row_stats_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(2 * units * C)),
+                     dim3(sv::kThreads), 0, s, a.rows, const_cast<sv::RowStat*>(a.stats));
+  hipLaunchKernelGGL((sv::tv_pair_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads),
+                     0, s, a);
+  if (a.grad)
+    hipLaunchKernelGGL((sv::tv_grad_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(units * C)),
+                       dim3(sv::kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(sv::tv_forward_kernel, dim3(static_cast<unsigned>(a.N)), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(sv::tv_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int spec_version(void) { return SPEC_VERSION; }
+
+const char* spec_status_string(spec_status s) {
+  switch (s) {
+    case SPEC_OK: return "ok";
+    case SPEC_EINVAL: return "invalid argument";
+    case SPEC_EUNSUPPORTED: return "unsupported dtype or shape";
+    case SPEC_EWORKSPACE: return "workspace missing or too small";
+    case SPEC_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (!verify_sizes_ok(B, K, V, dtype)) return 0;
+  return verify_layout(B, K, V, dtype).total;
+}
+
+size_t spec_tv_workspace_size(int N, int K, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (!tv_sizes_ok(N, K, V, dtype)) return 0;
+  return tv_layout(N, K, V, dtype).total;
+}
+
+spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                        const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                        spec_dtype dtype, int B, int K, int V, const int32_t* draft_ids,
+                        const float* temperature, float temperature_scalar, uint64_t seed,
+                        uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
+                        float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  // ---- validation: synchronous, before anything touches the GPU ------------
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
+  if (!verify_sizes_ok(B, K, V, dtype)) return SPEC_EINVAL;
+  if (!target_logits || !draft_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
+  if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
+  const VerifyLayout L = verify_layout(B, K, V, dtype);
+  if (!workspace) return SPEC_EWORKSPACE;
+  if (workspace_bytes < L.total) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  const size_t es = esize_of(dtype);
+  sv::VerifyArgs a{};
+  a.rows.tgt = target_logits; a.rows.tsb = t_stride_b; a.rows.tsk = t_stride_k; a.rows.tper = K + 1;
+  a.rows.drf = draft_logits; a.rows.dsb = d_stride_b; a.rows.dsk = d_stride_k; a.rows.dper = K;
+  a.rows.nb = B;
+  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, es) ? 1 : 0;
+  a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_b, d_stride_k, es) ? 1 : 0;
+  a.B = B; a.K = K;
+  a.ids = draft_ids;
+  a.seed = seed; a.offset = offset;
+  a.accept_len = accept_len; a.emitted = emitted_ids;
+  a.overlap = overlap; a.p_at = p_at_draft; a.q_at = q_at_draft;
+  a.logz_t = logz_target; a.logz_d = logz_draft;
+  char* ws = static_cast<char*>(workspace);
+  a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
+  a.pairs = reinterpret_cast<sv::PairStat*>(ws + L.pairs);
+  const int64_t rows = int64_t{B} * (2 * K + 1);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_verify<BF16, kNtBf16>(a, rows, s) : launch_verify<F32, kNtF32>(a, rows, s);
+}
+
+spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,
+                                 const void* draft_logits, int64_t d_stride_n, int64_t d_stride_k,
+                                 spec_dtype dtype, int N, int K, int V, float temperature, spec_tv_mode mode,
+                                 float scale, float* loss, float* overlap, float* grad_draft, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
+  if (!tv_sizes_ok(N, K, V, dtype)) return SPEC_EINVAL;
+  if (!target_logits || !draft_logits || !loss) return SPEC_EINVAL;
+  if (t_stride_n < 0 || t_stride_k < 0 || d_stride_n < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!(temperature > 0.f && std::isfinite(temperature))) return SPEC_EINVAL;
+  if (mode != SPEC_TV_E2E && mode != SPEC_TV_PROD && mode != SPEC_TV_PER_STEP) return SPEC_EINVAL;
+  if (!std::isfinite(scale)) return SPEC_EINVAL;
+  const TvLayout L = tv_layout(N, K, V, dtype);
+  if (!workspace) return SPEC_EWORKSPACE;
+  if (workspace_bytes < L.total) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  const size_t es = esize_of(dtype);
+  sv::TvArgs a{};
+  a.rows.tgt = target_logits; a.rows.tsb = t_stride_n; a.rows.tsk = t_stride_k; a.rows.tper = K;
+  a.rows.drf = draft_logits; a.rows.dsb = d_stride_n; a.rows.dsk = d_stride_k; a.rows.dper = K;
+  a.rows.nb = N;
+  a.rows.temp = nullptr; a.rows.temp_scalar = temperature;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_n, t_stride_k, es) ? 1 : 0;
+  a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_n, d_stride_k, es) ? 1 : 0;
+  a.N = N; a.K = K;
+  a.mode = static_cast<int>(mode);
+  a.scale = static_cast<double>(scale);
+  a.inv_t = 1.0f / temperature;
+  a.loss = loss; a.overlap = overlap; a.grad = grad_draft;
+  char* ws = static_cast<char*>(workspace);
+  a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
+  a.pairs = reinterpret_cast<sv::TvPair*>(ws + L.pairs);
+  a.loss_pos = reinterpret_cast<double*>(ws + L.loss);
+  a.vec_g = (grad_draft && aligned16(grad_draft) && (V % 4 == 0)) ? 1 : 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_tv<BF16, kNtBf16>(a, s) : launch_tv<F32, kNtF32>(a, s);
+}
+
+}  // extern "C"

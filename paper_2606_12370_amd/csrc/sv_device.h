@@ -1,0 +1,369 @@
+// sv_device.h — device building blocks for the gfx950 verification and
+// TV-loss kernels: element types, 16-byte row loads, Philox4x64-10, wave64
+// and workgroup reductions and scans, and the per-chunk row statistics that
+// every kernel combines into a row's log2 normaliser.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sv {
+
+constexpr int kThreads = 256;          // one workgroup = 4 wave64
+constexpr int kWaves = kThreads / 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr double kLog2eD = 1.4426950408889634074;
+constexpr double kLn2D = 0.69314718055994530942;
+#define SPEC_MAX_K_DEV 8
+
+// 16-byte vector types the compiler treats as native vectors (needed by the
+// non-temporal load / store builtins).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// Element types: logits arrive as bfloat16 bit patterns or float32.  Each
+// thread owns one 16-byte vector per tile, i.e. EPV consecutive elements.
+struct BF16 {
+  using raw = uint16_t;
+  static constexpr int EPV = 8;
+  static __device__ __forceinline__ void widen(const uint4 v, float (&x)[8]) {
+    x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xffff0000u);
+    x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xffff0000u);
+    x[4] = __uint_as_float(v.z << 16); x[5] = __uint_as_float(v.z & 0xffff0000u);
+    x[6] = __uint_as_float(v.w << 16); x[7] = __uint_as_float(v.w & 0xffff0000u);
+  }
+  static __device__ __forceinline__ float one(const raw* p) {
+    return __uint_as_float(static_cast<uint32_t>(*p) << 16);
+  }
+};
+
+struct F32 {
+  using raw = float;
+  static constexpr int EPV = 4;
+  static __device__ __forceinline__ void widen(const uint4 v, float (&x)[4]) {
+    x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y);
+    x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
+  }
+  static __device__ __forceinline__ float one(const raw* p) { return *p; }
+};
+
+// Load S tiles (tile0 .. tile0+S-1) of a row: x[j][k] receives element
+// (tile0 + j) * 256 * EPV + t * EPV + k of the row, t = threadIdx.x.  Elements
+// at or beyond V are -inf (probability 0).  With `aligned` (row base 16-byte
+// aligned) every full vector is one 16-byte load, all issued back to back; a
+// vector past V is read from the row start and discarded (no branch around
+// the load); the one vector that straddles V (V not a multiple of EPV) is
+// completed element by element.  Unaligned rows are read element by element.
+template <class E, int S>
+__device__ __forceinline__ void load_tiles(const typename E::raw* __restrict__ row, int tile0, int V, bool aligned,
+                                           float (&x)[S][E::EPV]) {
+  constexpr int EPV = E::EPV;
+  constexpr int TILE = 256 * EPV;
+  const int t = threadIdx.x;
+  if (aligned) {
+    u32x4 w[S];
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const int v0 = (tile0 + j) * TILE + t * EPV;
+      const int off = (v0 + EPV <= V) ? v0 : 0;
+      w[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + off));
+    }
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const int v0 = (tile0 + j) * TILE + t * EPV;
+      E::widen(make_uint4(w[j].x, w[j].y, w[j].z, w[j].w), x[j]);
+      if (v0 + EPV > V) {
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) x[j][k] = (v0 + k < V) ? E::one(row + v0 + k) : -INFINITY;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const int v0 = (tile0 + j) * TILE + t * EPV;
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) x[j][k] = (v0 + k < V) ? E::one(row + v0 + k) : -INFINITY;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11).  Counter (c0..c3), key
+// (k0, k1); each round multiplies c0 and c2 by the two published multipliers,
+// mixes the high halves with c1 / c3 and the key, and the key is bumped by the
+// two Weyl constants between rounds.
+struct Philox4x64 {
+  uint64_t w[4];
+};
+
+__device__ inline Philox4x64 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                           uint64_t k0, uint64_t k1) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) { k0 += W0; k1 += W1; }
+    const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+    const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+  }
+  Philox4x64 out;
+  out.w[0] = c0; out.w[1] = c1; out.w[2] = c2; out.w[3] = c3;
+  return out;
+}
+
+// Top 24 bits as a uniform on the 2^-24 grid in [0, 1) (exact in float32).
+__device__ __forceinline__ double u24(uint64_t w) {
+  return static_cast<double>(w >> 40) * (1.0 / 16777216.0);
+}
+
+// ---------------------------------------------------------------------------
+// wave64 and workgroup reductions / scans.  All reductions run in a fixed
+// order so results are bitwise reproducible.
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_min_int(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// inclusive scan over the 64 lanes of a wave
+__device__ __forceinline__ double wave_incl_scan(double v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
+  return v;
+}
+
+// Scratch for workgroup-wide reductions (lives in LDS).
+template <int N>
+struct RedLds {
+  double d[kWaves][N];
+  float f[kWaves][N];
+  int i[kWaves];
+};
+
+// Workgroup max of N floats per thread; every thread receives the results.
+template <int N>
+__device__ __forceinline__ void wg_max(float (&v)[N], RedLds<N>& s) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int n = 0; n < N; ++n) v[n] = wave_max(v[n]);
+  if (lane == 0) {
+#pragma unroll
+    for (int n = 0; n < N; ++n) s.f[wave][n] = v[n];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    float m = s.f[0][n];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, s.f[w][n]);
+    v[n] = m;
+  }
+  __syncthreads();
+}
+
+// Workgroup sum of N doubles per thread; every thread receives the results.
+template <int N>
+__device__ __forceinline__ void wg_sum(double (&v)[N], RedLds<N>& s) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int n = 0; n < N; ++n) v[n] = wave_sum(v[n]);
+  if (lane == 0) {
+#pragma unroll
+    for (int n = 0; n < N; ++n) s.d[wave][n] = v[n];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    double a = s.d[0][n];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) a += s.d[w][n];
+    v[n] = a;
+  }
+  __syncthreads();
+}
+
+// Scan of one double per thread over the workgroup, in thread order.
+// Returns the exclusive prefix and sets *incl to the inclusive one; the
+// exclusive prefix of thread t is bit-identical to the inclusive prefix of
+// thread t-1, so the ranges [excl, incl) of consecutive threads tile exactly.
+__device__ __forceinline__ double wg_scan(double v, RedLds<1>& s, double* incl_out) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const double incl_w = wave_incl_scan(v);
+  double excl_w = __shfl_up(incl_w, 1, 64);
+  if (lane == 0) excl_w = 0.0;
+  if (lane == 63) s.d[wave][0] = incl_w;
+  __syncthreads();
+  double base = 0.0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w)
+    if (w < wave) base += s.d[w][0];
+  __syncthreads();
+  *incl_out = base + incl_w;
+  return base + excl_w;
+}
+
+// Workgroup minimum of an int (every thread receives it).
+__device__ __forceinline__ int wg_min_int(int v, RedLds<1>& s) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  v = wave_min_int(v);
+  if (lane == 0) s.i[wave] = v;
+  __syncthreads();
+  int m = s.i[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) m = min(m, s.i[w]);
+  __syncthreads();
+  return m;
+}
+
+// ---------------------------------------------------------------------------
+// Row statistics.  For a row z (logits) and s = log2(e) / T, the row's
+// softmax is p_v = 2^(z_v s - M) / D with M a reference in log2 units and
+// D = sum_v 2^(z_v s - M).  A chunk of the row reduces to (m_c, D_c): its
+// largest per-thread reference and its sum relative to it.  References are
+// rounded once (rs = round(max z * s)) and every exponent is formed as
+// fma(z, s, -rs), so the exact product z*s enters each element and no
+// per-thread rounding shift biases the normalised values.
+struct RowStat {
+  float m;     // largest thread reference of the chunk, log2 units (-inf: empty)
+  float pad;
+  double D;    // sum of 2^(z s - m) over the chunk
+};
+
+__device__ __forceinline__ float scale_of(float T) {
+  return static_cast<float>(kLog2eD / static_cast<double>(T));
+}
+
+// Chunk statistics of one row: tiles tile0 .. tile0+nt-1, S tiles per step.
+template <class E, int NT, int S>
+__device__ __forceinline__ void chunk_stats(const typename E::raw* __restrict__ row, int tile0, int nt, int V,
+                                            bool aligned, float s, RedLds<4>& red, float* m_out, double* d_out) {
+  constexpr int EPV = E::EPV;
+  float ref = -INFINITY, dsum = 0.f;
+#pragma unroll
+  for (int j0 = 0; j0 < NT; j0 += S) {
+    if (j0 >= nt) break;
+    float x[S][EPV];
+    load_tiles<E, S>(row, tile0 + j0, V, aligned, x);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[j][k]);
+    if (mx != -INFINITY) {
+      const float r = mx * s;
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < S; ++j)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) acc += __builtin_amdgcn_exp2f(fmaf(x[j][k], s, -r));
+      if (ref == -INFINITY) { ref = r; dsum = acc; }
+      else if (r > ref) { dsum = dsum * __builtin_amdgcn_exp2f(ref - r) + acc; ref = r; }
+      else dsum += acc * __builtin_amdgcn_exp2f(r - ref);
+    }
+  }
+  float m4[4] = {ref, -INFINITY, -INFINITY, -INFINITY};
+  wg_max<4>(m4, red);
+  double d4[4] = {0.0, 0.0, 0.0, 0.0};
+  if (dsum != dsum) d4[0] = dsum;  // NaN propagates (data error)
+  else if (ref != -INFINITY)
+    d4[0] = static_cast<double>(dsum) * static_cast<double>(__builtin_amdgcn_exp2f(ref - m4[0]));
+  wg_sum<4>(d4, red);
+  *m_out = m4[0];
+  *d_out = d4[0];
+}
+
+// Combine a row's C chunk statistics into (M, D).  Called by all 64 lanes of
+// one wave; every lane receives the result.  The order of the float64 sum is
+// fixed, so every kernel that combines the same row gets the same bits.
+__device__ __forceinline__ void combine_row(const RowStat* __restrict__ st, int C, float* M, double* D) {
+  const int lane = threadIdx.x & 63;
+  float m = -INFINITY;
+  for (int cc = lane; cc < C; cc += 64) m = fmaxf(m, st[cc].m);
+  m = wave_max(m);
+  double d = 0.0;
+  for (int cc = lane; cc < C; cc += 64) {
+    const float mc = st[cc].m;
+    const double dc = st[cc].D;
+    if (dc != dc) d += dc;
+    else if (mc != -INFINITY) d += dc * static_cast<double>(__builtin_amdgcn_exp2f(mc - m));
+  }
+  *M = m;
+  *D = wave_sum(d);
+}
+
+// Probability of one element given its row's (M, 1/D): 2^(z s - M) / D.
+__device__ __forceinline__ float prob(float z, float s, float M, float invD) {
+  return __builtin_amdgcn_exp2f(fmaf(z, s, -M)) * invD;
+}
+
+// Rows of a batch: target rows (b, i) for i < tper, then draft rows (b, i)
+// for i < dper, b < nb.  Row r of the statistics array is target row
+// (r / tper, r % tper) for r < nb * tper, then draft rows in the same order.
+struct RowsDesc {
+  const void* tgt; int64_t tsb, tsk; int tper;
+  const void* drf; int64_t dsb, dsk; int dper;
+  int nb;
+  const float* temp; float temp_scalar;  // per batch row, or one scalar (temp == nullptr)
+  int V, ntiles, C;
+  int vec_t, vec_d;
+};
+
+template <class E>
+__device__ __forceinline__ const typename E::raw* row_of(const RowsDesc& d, int r, int* b, bool* aligned) {
+  using raw = typename E::raw;
+  const int RT = d.nb * d.tper;
+  if (r < RT) {
+    *b = r / d.tper;
+    *aligned = d.vec_t != 0;
+    return static_cast<const raw*>(d.tgt) + static_cast<int64_t>(*b) * d.tsb + static_cast<int64_t>(r % d.tper) * d.tsk;
+  }
+  r -= RT;
+  *b = r / d.dper;
+  *aligned = d.vec_d != 0;
+  return static_cast<const raw*>(d.drf) + static_cast<int64_t>(*b) * d.dsb + static_cast<int64_t>(r % d.dper) * d.dsk;
+}
+
+__device__ __forceinline__ float temperature_of(const RowsDesc& d, int b) {
+  return d.temp ? d.temp[b] : d.temp_scalar;
+}
+__device__ __forceinline__ bool temperature_ok(float T) { return T > 0.f && T < INFINITY; }
+
+// One workgroup per (row, chunk): the chunk's statistics (pass 1).
+template <class E, int NT, int S>
+__global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat* __restrict__ stats) {
+  __shared__ RedLds<4> red;
+  const int r = blockIdx.x / d.C, c = blockIdx.x % d.C;
+  int b;
+  bool aligned;
+  const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+  const float T = temperature_of(d, b);
+  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+  const int tile0 = c * NT;
+  const int nt = min(NT, d.ntiles - tile0);
+  float m;
+  double D;
+  chunk_stats<E, NT, S>(row, tile0, nt, d.V, aligned, s, red, &m, &D);
+  if (threadIdx.x == 0) {
+    RowStat o;
+    o.m = m; o.pad = 0.f; o.D = D;
+    stats[blockIdx.x] = o;
+  }
+}
+
+}  // namespace sv

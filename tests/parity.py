@@ -1,0 +1,127 @@
+"""Comparison of GPU results with the float64 oracle, shared by the GPU tests.
+
+Accept lengths and emitted tokens must match bit for bit, except rows whose
+first divergence is a boundary draw: an accept decision whose uniform lies
+within BOUNDARY of p(x)/q(x), or a resample whose uniform lies within
+BOUNDARY of a step C(v)/Z of the residual CDF (values from the oracle).
+Those rows are counted and reported, not failed.  Float outputs are compared
+with the relative tolerance the method fixes for the input dtype.
+"""
+
+import numpy as np
+import torch
+
+from paper_2606_12370_amd import workloads as W
+
+BOUNDARY = 1e-6
+TOL = {W.F32: 1e-5, W.BF16: 2e-3}
+
+
+def host_logits(t, dtype):
+    """Exact float64 copy of a device logits tensor."""
+    if dtype == W.BF16:
+        bits = t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        return W.to_float64(bits, W.BF16)
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def device_inputs(d, device="cuda"):
+    """Move host workload arrays (numpy) to device tensors of the storage dtype."""
+    if d["dtype"] == W.BF16:
+        tgt = torch.from_numpy(d["target"].view(np.int16)).to(device).view(torch.bfloat16)
+        drf = torch.from_numpy(d["draft"].view(np.int16)).to(device).view(torch.bfloat16)
+    else:
+        tgt = torch.from_numpy(np.ascontiguousarray(d["target"])).to(device)
+        drf = torch.from_numpy(np.ascontiguousarray(d["draft"])).to(device)
+    return tgt, drf
+
+
+def rel_err(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return np.abs(a - b) / np.maximum(np.abs(b), 1e-300)
+
+
+def compare_verify(gpu, ref, dtype, rows=None, report=None):
+    """Compare gpu outputs (dict of tensors, all B rows) with oracle outputs
+    for `rows` (default all).  Returns a dict of counts; raises on failure."""
+    acc_g = gpu["accept_len"].cpu().numpy()
+    em_g = gpu["emitted"].cpu().numpy()
+    ov_g = gpu["overlap"].cpu().numpy()
+    if rows is not None:
+        acc_g, em_g, ov_g = acc_g[rows], em_g[rows], ov_g[rows]
+    acc_r, em_r = ref["accept_len"], ref["emitted"]
+    K = em_r.shape[1] - 1
+    bad_rows, boundary_rows = [], []
+    for r in np.nonzero((acc_g != acc_r) | np.any(em_g != em_r, axis=1))[0]:
+        ng, nr = int(acc_g[r]), int(acc_r[r])
+        if ng < 0 or nr < 0 or ng > K or nr > K:
+            bad_rows.append(r)
+            continue
+        if ng != nr:
+            i = min(ng, nr)  # first step where the two accept decisions differ
+            if abs(ref["u_accept"][r, i] - ref["ratio"][r, i]) <= BOUNDARY:
+                boundary_rows.append(r)
+                continue
+        elif np.array_equal(em_g[r, :ng], em_r[r, :nr]) and ref["resample_margin"][r] <= BOUNDARY:
+            boundary_rows.append(r)
+            continue
+        bad_rows.append(r)
+    if bad_rows:
+        r = bad_rows[0]
+        raise AssertionError("%d rows differ outside the boundary window; first row %d: gpu n=%d emitted=%s, "
+                             "oracle n=%d emitted=%s" % (len(bad_rows), r, acc_g[r], em_g[r], acc_r[r], em_r[r]))
+    err_rows = ref["row_error"]
+    assert np.all(acc_g[err_rows] == -1) and np.all(em_g[err_rows] == -1)
+    assert np.all(np.isnan(ov_g[err_rows]))
+    ok = ~err_rows
+    tol = TOL[dtype]
+    e_ov = rel_err(ov_g[ok], ref["overlap"][ok])
+    max_ov = float(e_ov.max()) if e_ov.size else 0.0
+    assert max_ov <= tol, "overlap relative error %.3e > %.1e" % (max_ov, tol)
+    out = {"rows": int(len(acc_r)), "boundary_rows": len(boundary_rows), "max_rel_overlap": max_ov}
+    for key in ("p_at_draft", "q_at_draft", "logz_target", "logz_draft"):
+        if key in gpu:
+            g = gpu[key].cpu().numpy()
+            if rows is not None:
+                g = g[rows]
+            e = rel_err(g[ok], ref[key][ok])
+            m = float(e.max()) if e.size else 0.0
+            assert m <= tol, "%s relative error %.3e > %.1e" % (key, m, tol)
+            out["max_rel_" + key] = m
+    if report is not None:
+        report.update(out)
+    return out
+
+
+def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True):
+    """Compare TV-loss outputs with the oracle (optionally for a subset of
+    positions).  The gradient is compared per (position, step) row in the
+    norm-wise sense, excluding elements whose indicator 1[q <= p] is decided
+    by rounding (|log q - log p| <= BOUNDARY)."""
+    tol = TOL[dtype]
+    ov = ov_g.cpu().numpy().astype(np.float64)
+    if positions is not None:
+        ov = ov[positions]
+    e_ov = rel_err(ov, ref["overlap"]).max()
+    assert e_ov <= tol, "overlap relative error %.3e" % e_ov
+    out = {"max_rel_overlap": float(e_ov)}
+    if loss_exact:
+        lg = float(loss_g.cpu().numpy()[0])
+        e_l = abs(lg - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
+        assert e_l <= tol, "loss relative error %.3e (gpu %r, oracle %r)" % (e_l, lg, ref["loss"])
+        out["rel_loss"] = float(e_l)
+    if grad_g is not None:
+        g = grad_g
+        if positions is not None:
+            g = g[torch.as_tensor(positions, device=g.device)]
+        g = g.cpu().numpy().astype(np.float64)
+        gr = ref["grad"]
+        tie = ref["tie_margin"] <= BOUNDARY
+        diff = np.where(tie, 0.0, np.abs(g - gr)).max(axis=-1)
+        scale = np.maximum(np.abs(gr).max(axis=-1), 1e-300)
+        worst = float((diff / scale).max())
+        assert worst <= tol, "gradient norm-wise relative error %.3e" % worst
+        out["max_normwise_grad"] = worst
+        out["tie_elements"] = int(tie.sum())
+    return out

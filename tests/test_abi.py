@@ -1,0 +1,131 @@
+"""The C ABI: the library loads, exports every function include/specverify.h
+declares, the ctypes prototypes agree with the header, and host-checkable
+argument errors come back synchronously (no GPU work is enqueued by any
+call in this file)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_12370_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specverify.h")
+
+
+def header_prototypes():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    protos = {}
+    for m in re.finditer(r"\b(?:spec_status|size_t|int|const char\*)\s+(spec_\w+)\s*\(([^;]*?)\)\s*;", src, re.S):
+        args = [a.strip() for a in m.group(2).split(",") if a.strip() and a.strip() != "void"]
+        protos[m.group(1)] = args
+    return protos
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.load_library()
+
+
+def test_exports_every_declared_function(lib):
+    protos = header_prototypes()
+    assert set(protos) == {"spec_verify_workspace_size", "spec_verify", "spec_tv_workspace_size",
+                           "spec_tv_loss_fwd_bwd", "spec_status_string", "spec_version"}
+    for name in protos:
+        assert hasattr(lib, name), name
+
+
+def test_ctypes_prototypes_match_header():
+    protos = header_prototypes()
+    assert len(protos["spec_verify"]) == len(binding.VERIFY_ARGTYPES)
+    assert len(protos["spec_tv_loss_fwd_bwd"]) == len(binding.TV_ARGTYPES)
+
+
+def test_version_and_status_strings(lib):
+    ver = int(re.search(r"#define SPEC_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert lib.spec_version() == ver
+    for code in (0, 1, 2, 4, 5):
+        assert lib.spec_status_string(code)
+    assert lib.spec_status_string(99) == b"unknown status"
+
+
+def test_workspace_sizes(lib):
+    assert lib.spec_verify_workspace_size(0, 3, 100, 1) == 0
+    assert lib.spec_verify_workspace_size(4, 0, 100, 1) == 0
+    assert lib.spec_verify_workspace_size(4, 9, 100, 1) == 0
+    assert lib.spec_verify_workspace_size(4, 3, 0, 1) == 0
+    assert lib.spec_verify_workspace_size(4, 3, 100, 7) == 0
+    a = lib.spec_verify_workspace_size(64, 3, 151936, 1)
+    b = lib.spec_verify_workspace_size(256, 3, 151936, 1)
+    assert 0 < a < b and a % 256 == 0
+    assert lib.spec_tv_workspace_size(16384, 3, 151936, 1) > 0
+    assert lib.spec_tv_workspace_size(16384, 0, 151936, 1) == 0
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def call_verify(lib, **kw):
+    args = dict(t=FAKE, tsb=400, tsk=100, d=FAKE, dsb=300, dsk=100, dtype=1, B=4, K=3, V=100, ids=FAKE,
+                temp=None, temp_s=1.0, seed=0, off=0, acc=FAKE, em=FAKE, ov=None, p=None, q=None,
+                lzt=None, lzd=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    return lib.spec_verify(*[args[k] for k in ("t", "tsb", "tsk", "d", "dsb", "dsk", "dtype", "B", "K", "V", "ids",
+                                               "temp", "temp_s", "seed", "off", "acc", "em", "ov", "p", "q", "lzt",
+                                               "lzd", "ws", "wsb", "stream")])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), 2),
+    (dict(K=9), 2),
+    (dict(B=0), 1),
+    (dict(V=0), 1),
+    (dict(K=0), 1),
+    (dict(t=None), 1),
+    (dict(d=None), 1),
+    (dict(ids=None), 1),
+    (dict(acc=None), 1),
+    (dict(em=None), 1),
+    (dict(tsb=-1), 1),
+    (dict(dsk=-100), 1),
+    (dict(temp_s=0.0), 1),
+    (dict(temp_s=float("nan")), 1),
+    (dict(temp_s=float("inf")), 1),
+    (dict(temp_s=-1.0), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=64), 4),
+    (dict(ws=FAKE + 4), 1),
+])
+def test_verify_argument_errors(lib, kw, status):
+    assert call_verify(lib, **kw) == status
+
+
+def call_tv(lib, **kw):
+    args = dict(t=FAKE, tsn=300, tsk=100, d=FAKE, dsn=300, dsk=100, dtype=1, N=4, K=3, V=100, T=1.0, mode=0,
+                scale=1.0, loss=FAKE, ov=None, grad=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    return lib.spec_tv_loss_fwd_bwd(*[args[k] for k in ("t", "tsn", "tsk", "d", "dsn", "dsk", "dtype", "N", "K", "V",
+                                                        "T", "mode", "scale", "loss", "ov", "grad", "ws", "wsb",
+                                                        "stream")])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=3), 2),
+    (dict(K=9), 2),
+    (dict(N=0), 1),
+    (dict(V=-5), 1),
+    (dict(t=None), 1),
+    (dict(loss=None), 1),
+    (dict(T=0.0), 1),
+    (dict(T=float("nan")), 1),
+    (dict(mode=3), 1),
+    (dict(scale=float("inf")), 1),
+    (dict(tsk=-1), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=100), 4),
+])
+def test_tv_argument_errors(lib, kw, status):
+    assert call_tv(lib, **kw) == status

@@ -1,0 +1,205 @@
+"""GPU parity of spec_verify against the float64 oracle (through the C ABI).
+
+Small cases are compared on every row; the full-size workloads (rollout
+B=64, the B=256 benchmark batch, the B=1024 / V=262144 batch) on every row or
+on a sample of rows, which the oracle can check one by one because every
+draw depends only on (seed, row, step, offset)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_12370_amd import binding
+from paper_2606_12370_amd import workloads as W
+from tests.parity import compare_verify, device_inputs, host_logits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    binding.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def run_numpy_case(d, seed=0, offset=0, scalar_t=None, debug=True):
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    if scalar_t is None:
+        T = torch.from_numpy(d["temperature"]).cuda()
+        T_ref = d["temperature"].astype(np.float64)
+    else:
+        T, T_ref = float(scalar_t), float(np.float32(scalar_t))
+    out = binding.verify(tgt, drf, ids, T, seed, offset, want_debug=debug)
+    torch.cuda.synchronize()
+    ref = oracle.verify_ref(W.to_float64(d["target"], d["dtype"]), W.to_float64(d["draft"], d["dtype"]),
+                            d["ids"], T_ref, seed, offset)
+    return out, ref
+
+
+def test_tiny_f32():
+    d = W.verify_inputs_numpy(**{k: v for k, v in W.CONFIGS["tiny_f32_b4_k1_v1024"].items()})
+    out, ref = run_numpy_case(d)
+    rep = compare_verify(out, ref, W.F32)
+    print("tiny", rep)
+    assert rep["boundary_rows"] == 0
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("B,K,V", [(6, 3, 20000), (3, 2, 2049), (5, 1, 1023), (4, 4, 7), (3, 1, 1),
+                                   (2, 8, 9000), (3, 3, 65536 + 24)])
+def test_ragged_multi_chunk(dtype, B, K, V):
+    d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 7 + B + K + V)
+    out, ref = run_numpy_case(d, seed=11, offset=3)
+    rep = compare_verify(out, ref, dtype)
+    print(dtype, B, K, V, rep)
+
+
+def test_scalar_temperature():
+    d = W.verify_inputs_numpy(5, 3, 5000, W.BF16, "rollout", 21)
+    out, ref = run_numpy_case(d, seed=5, scalar_t=0.8)
+    compare_verify(out, ref, W.BF16)
+
+
+def test_exactness_batch_and_chi_square():
+    """65536 rows, K=1, V=8: row-by-row parity, then the emitted-token
+    histogram of a shared target against softmax(z) (chi-square)."""
+    from scipy import stats
+    cfg = W.CONFIGS["exact_f32_b65536_k1_v8"]
+    d = W.verify_inputs_numpy(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], cfg["gen"], cfg["seed"])
+    out, ref = run_numpy_case(d, debug=False)
+    rep = compare_verify(out, ref, W.F32)
+    print("exact per-row", rep)
+    d = W.verify_inputs_numpy(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], cfg["gen"], cfg["seed"], shared_target=True)
+    out, ref = run_numpy_case(d, seed=123, debug=False)
+    compare_verify(out, ref, W.F32)
+    p, _ = oracle.softmax_t(d["target"][0, 0].astype(np.float64), 1.0)
+    counts = np.bincount(out["emitted"][:, 0].cpu().numpy(), minlength=8)
+    pval = stats.chisquare(counts, p * counts.sum()).pvalue
+    print("chi-square p-value", pval)
+    assert pval > 1e-3
+
+
+def test_q_equals_p_control_accepts_all():
+    cfg = W.CONFIGS["exact_f32_b65536_k1_v8"]
+    d = W.verify_inputs_numpy(cfg["B"], 1, 8, W.F32, "exact", cfg["seed"], q_equals_p=True)
+    out, ref = run_numpy_case(d, debug=False)
+    assert bool((out["accept_len"] == 1).all())
+    compare_verify(out, ref, W.F32)
+    d = W.verify_inputs_numpy(8, 3, 151936, W.BF16, "rollout", 44, q_equals_p=True)
+    out, ref = run_numpy_case(d, debug=False)
+    assert bool((out["accept_len"] == 3).all())
+    compare_verify(out, ref, W.BF16)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_row_data_errors(dtype):
+    d = W.verify_inputs_numpy(8, 2, 3000, dtype, "rollout", 9)
+    tgt = W.to_float64(d["target"], dtype).astype(np.float32)
+    drf = W.to_float64(d["draft"], dtype).astype(np.float32)
+    tgt[0, 1, 3] = np.nan
+    drf[1, 0, 0] = np.inf
+    tgt[2, 2, :] = -np.inf
+    d["ids"][3, 1] = 3000
+    d["temperature"][4] = 0.0
+    tgt[5, 0, :100] = -np.inf  # legal
+    d["ids"][6, 0] = -1
+    d["target"] = W.f32_to_bf16_bits(tgt) if dtype == W.BF16 else tgt
+    d["draft"] = W.f32_to_bf16_bits(drf) if dtype == W.BF16 else drf
+    out, ref = run_numpy_case(d)
+    assert list(ref["row_error"]) == [True, True, True, True, True, False, True, False]
+    compare_verify(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_unaligned_strided_views(dtype):
+    """Rows that are not 16-byte aligned and non-contiguous batch strides take
+    the element-wise load path; results must not change."""
+    B, K, V = 3, 2, 4099
+    d = W.verify_inputs_numpy(B, K, V, dtype, "rollout", 17)
+    tgt, drf = device_inputs(d)
+    big_t = torch.zeros((B, K + 2, V + 3), dtype=tgt.dtype, device="cuda")
+    big_d = torch.zeros((B, K + 1, V + 5), dtype=drf.dtype, device="cuda")
+    big_t[:, 1:K + 2, 1:V + 1] = tgt
+    big_d[:, :K, 3:V + 3] = drf
+    vt, vd = big_t[:, 1:K + 2, 1:V + 1], big_d[:, :K, 3:V + 3]
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    out_v = binding.verify(vt, vd, ids, T, 4, 0, want_debug=True)
+    out_c = binding.verify(tgt, drf, ids, T, 4, 0, want_debug=True)
+    torch.cuda.synchronize()
+    for k in out_c:
+        assert torch.equal(out_v[k].nan_to_num(), out_c[k].nan_to_num()), k
+    ref = oracle.verify_ref(W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype), d["ids"],
+                            d["temperature"].astype(np.float64), 4, 0)
+    compare_verify(out_v, ref, dtype)
+
+
+def test_determinism_and_seed():
+    d = W.verify_inputs_numpy(16, 3, 40000, W.BF16, "rollout_t", 5)
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    a = binding.verify(tgt, drf, ids, T, 99, 1, want_debug=True)
+    b = binding.verify(tgt, drf, ids, T, 99, 1, want_debug=True)
+    c = binding.verify(tgt, drf, ids, T, 100, 1)
+    torch.cuda.synchronize()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+    assert not torch.equal(a["emitted"], c["emitted"])
+
+
+def _sampled(cfg_name, nsample, seed=0):
+    cfg = W.CONFIGS[cfg_name]
+    d = W.verify_inputs_torch(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], cfg["gen"], cfg["seed"])
+    out = binding.verify(d["target"], d["draft"], d["ids"], d["temperature"], seed, 0, want_debug=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(cfg["seed"])
+    rows = np.sort(rng.choice(cfg["B"], size=min(nsample, cfg["B"]), replace=False))
+    ri = torch.as_tensor(rows, device="cuda")
+    ref = oracle.verify_ref(host_logits(d["target"][ri], cfg["dtype"]), host_logits(d["draft"][ri], cfg["dtype"]),
+                            d["ids"][ri].cpu().numpy(), d["temperature"][ri].cpu().numpy().astype(np.float64),
+                            seed, 0, rows=rows)
+    rep = compare_verify(out, ref, cfg["dtype"], rows=rows)
+    acc = out["accept_len"].cpu().numpy()
+    assert acc.min() >= 0 and acc.max() <= cfg["K"]
+    print(cfg_name, rep, "mean accept_len", acc.mean())
+    return rep
+
+
+def test_rollout_full_batch():
+    cfg = W.CONFIGS["rollout_bf16_b64_k3_v151936"]
+    d = W.verify_inputs_numpy(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], cfg["gen"], cfg["seed"])
+    out, ref = run_numpy_case(d, seed=0)
+    rep = compare_verify(out, ref, W.BF16)
+    print("rollout B=64", rep)
+
+
+def test_benchmark_batch_sampled_rows():
+    _sampled("verify_bf16_b256_k3_v151936", 24)
+
+
+def test_large_batch_sampled_rows():
+    _sampled("large_bf16_b1024_k3_v262144", 8, seed=7)
+
+
+def test_one_workspace_across_shapes_and_kernels():
+    """Calls of different shapes and of both entry points share one scratch
+    workspace filled with garbage: results must not depend on its contents."""
+    ws = torch.full((64 << 20,), 0xA5, dtype=torch.uint8, device="cuda")
+    td = W.tv_inputs_numpy(40, 3, 30000, W.BF16, 8)
+    tt, tq = device_inputs(td)
+    binding.tv_loss_fwd_bwd(tt, tq, 1.0, "prod", 1.0, ws=ws)
+    for (B, K, V, dt) in [(700, 1, 8, W.F32), (9, 3, 70000, W.BF16), (4000, 2, 100, W.F32)]:
+        d = W.verify_inputs_numpy(B, K, V, dt, "rollout_t", B + V)
+        tgt, drf = device_inputs(d)
+        ids = torch.from_numpy(d["ids"]).cuda()
+        T = torch.from_numpy(d["temperature"]).cuda()
+        out = binding.verify(tgt, drf, ids, T, 3, 0, ws=ws)
+        torch.cuda.synchronize()
+        ref = oracle.verify_ref(W.to_float64(d["target"], dt), W.to_float64(d["draft"], dt), d["ids"],
+                                d["temperature"].astype(np.float64), 3, 0)
+        compare_verify(out, ref, dt)
