@@ -25,7 +25,8 @@
  *    next.  Calls that share a workspace must not run concurrently (enqueue
  *    them on one stream).
  *  - Each call is a short fixed sequence of kernel launches on `stream`
- *    (spec_verify: 3, spec_tv_loss_fwd_bwd: 4); no launch waits on another
+ *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a
+ *    gradient); no launch waits on another
  *    workgroup, so any number of resident workgroups is enough.
  *  - Entry points are thread-safe; each call is independent.
  *  - Logits are bfloat16 (raw 16-bit patterns) or float32.  Arithmetic is
@@ -91,7 +92,9 @@ size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
  *                (which must then be finite and > 0)
  * accept_len     [B] int32 out
  * emitted_ids    [B, K+1] int32 out, contiguous
- * overlap        [B, K] float32 out (may be NULL)
+ * overlap        [B, K] float32 out, or NULL: then only the pair at the first
+ *                rejected step is read a second time (about 1.15 reads of the
+ *                logits instead of 1.9)
  * p_at_draft, q_at_draft  [B, K] float32 out: p_i(x_i), q_i(x_i) (may be NULL)
  * logz_target    [B, K+1] float32 out: natural-log partition function of z/T (may be NULL)
  * logz_draft     [B, K]   float32 out (may be NULL)

@@ -128,14 +128,16 @@ def _check_rows(t, name, shape):
 
 
 def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offset=0,
-           want_debug=False, ws=None, out=None):
+           want_debug=False, want_overlap=True, ws=None, out=None):
     """Chain rejection-sampling verification (spec_verify).
 
     target_logits [B, K+1, V], draft_logits [B, K, V] (bf16 or f32, same
     dtype, vocabulary dimension contiguous), draft_ids [B, K] int32,
     temperature: float or [B] float32 tensor.  Returns a dict with
-    accept_len [B], emitted [B, K+1], overlap [B, K] and, with want_debug,
-    p_at_draft, q_at_draft [B, K], logz_target [B, K+1], logz_draft [B, K].
+    accept_len [B], emitted [B, K+1], overlap [B, K] (unless want_overlap is
+    False, which lets the library skip most of the second read) and, with
+    want_debug, p_at_draft, q_at_draft [B, K], logz_target [B, K+1],
+    logz_draft [B, K].
     All work is enqueued on the current stream; nothing synchronises.
     """
     lib = load_library()
@@ -160,8 +162,9 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
         out = {
             "accept_len": torch.empty(B, dtype=torch.int32, device=dev),
             "emitted": torch.empty((B, K + 1), dtype=torch.int32, device=dev),
-            "overlap": torch.empty((B, K), dtype=torch.float32, device=dev),
         }
+        if want_overlap:
+            out["overlap"] = torch.empty((B, K), dtype=torch.float32, device=dev)
         if want_debug:
             out["p_at_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
             out["q_at_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)

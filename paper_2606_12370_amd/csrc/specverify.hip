@@ -54,27 +54,33 @@ bool tv_sizes_ok(int N, int K, int V, spec_dtype dt) {
 }
 
 struct VerifyLayout {
-  size_t stats = 0, pairs = 0, total = 0;
+  size_t stats = 0, norms = 0, decision = 0, pairs = 0, total = 0;
 };
 VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt) {
   VerifyLayout L;
   const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t rows = static_cast<size_t>(B) * (2 * K + 1);
   size_t off = 0;
-  L.stats = off; off = align_up(off + static_cast<size_t>(B) * (2 * K + 1) * C * sizeof(sv::RowStat), 256);
+  L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
+  L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
+  L.decision = off; off = align_up(off + static_cast<size_t>(B) * sizeof(int32_t), 256);
   L.pairs = off; off = align_up(off + static_cast<size_t>(B) * K * C * sizeof(sv::PairStat), 256);
   L.total = off;
   return L;
 }
 
 struct TvLayout {
-  size_t stats = 0, pairs = 0, loss = 0, total = 0;
+  size_t stats = 0, norms = 0, pairs = 0, coef = 0, loss = 0, total = 0;
 };
 TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
   TvLayout L;
   const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t rows = static_cast<size_t>(N) * 2 * K;
   size_t off = 0;
-  L.stats = off; off = align_up(off + static_cast<size_t>(N) * 2 * K * C * sizeof(sv::RowStat), 256);
+  L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
+  L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
   L.pairs = off; off = align_up(off + static_cast<size_t>(N) * K * C * sizeof(sv::TvPair), 256);
+  L.coef = off; off = align_up(off + static_cast<size_t>(N) * K * sizeof(float2), 256);
   L.loss = off; off = align_up(off + static_cast<size_t>(N) * sizeof(double), 256);
   L.total = off;
   return L;
@@ -91,6 +97,7 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) 
   const int C = a.rows.C;
   hipLaunchKernelGGL((sv::row_stats_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(rows * C)),
                      dim3(sv::kThreads), 0, s, a.rows, const_cast<sv::RowStat*>(a.stats));
+  hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
   hipLaunchKernelGGL((sv::pair_pass_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(int64_t{a.B} * a.K * C)),
                      dim3(sv::kThreads), 0, s, a);
   hipLaunchKernelGGL((sv::finish_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s,
@@ -104,13 +111,16 @@ spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
   const int C = a.rows.C;
   hipLaunchKernelGGL((sv::row_stats_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(2 * units * C)),
                      dim3(sv::kThreads), 0, s, a.rows, const_cast<sv::RowStat*>(a.stats));
+  hipLaunchKernelGGL(sv::row_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C,
+                     const_cast<sv::RowNorm*>(a.norms));
   hipLaunchKernelGGL((sv::tv_pair_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads),
                      0, s, a);
+  hipLaunchKernelGGL(sv::tv_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a);
   if (a.grad)
     hipLaunchKernelGGL((sv::tv_grad_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(units * C)),
                        dim3(sv::kThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(sv::tv_forward_kernel, dim3(static_cast<unsigned>(a.N)), dim3(64), 0, s, a);
   hipLaunchKernelGGL(sv::tv_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
@@ -181,6 +191,8 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
   a.logz_t = logz_target; a.logz_d = logz_draft;
   char* ws = static_cast<char*>(workspace);
   a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
+  a.norms = reinterpret_cast<sv::RowNorm*>(ws + L.norms);
+  a.decision = reinterpret_cast<int32_t*>(ws + L.decision);
   a.pairs = reinterpret_cast<sv::PairStat*>(ws + L.pairs);
   const int64_t rows = int64_t{B} * (2 * K + 1);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -222,7 +234,9 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   a.loss = loss; a.overlap = overlap; a.grad = grad_draft;
   char* ws = static_cast<char*>(workspace);
   a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
+  a.norms = reinterpret_cast<const sv::RowNorm*>(ws + L.norms);
   a.pairs = reinterpret_cast<sv::TvPair*>(ws + L.pairs);
+  a.coef = reinterpret_cast<float2*>(ws + L.coef);
   a.loss_pos = reinterpret_cast<double*>(ws + L.loss);
   a.vec_g = (grad_draft && aligned16(grad_draft) && (V % 4 == 0)) ? 1 : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);

@@ -307,9 +307,47 @@ __device__ __forceinline__ void combine_row(const RowStat* __restrict__ st, int 
   *D = wave_sum(d);
 }
 
+// A row's combined normaliser: p_v = 2^(z_v s - M) / D.
+struct RowNorm {
+  float M;      // log2 units; +inf / NaN / -inf mark a bad row
+  float invD;   // 1 / D rounded once
+  float L;      // log2(D) rounded once
+  float pad;
+  double D;
+};
+
+__device__ __forceinline__ RowNorm make_norm(float M, double D) {
+  RowNorm n;
+  n.M = M;
+  n.invD = static_cast<float>(1.0 / D);
+  n.L = static_cast<float>(log2(D));
+  n.pad = 0.f;
+  n.D = D;
+  return n;
+}
+__device__ __forceinline__ bool norm_ok(const RowNorm& n) { return n.D > 0.0 && n.D < INFINITY && n.M < INFINITY; }
+
+// One wave per row: combine every row's chunk statistics (4 rows per
+// 256-thread workgroup).
+__global__ __launch_bounds__(kThreads) void row_norm_kernel(const RowStat* __restrict__ stats, int rows, int C,
+                                                            RowNorm* __restrict__ out) {
+  const int r = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  float M;
+  double D;
+  combine_row(stats + static_cast<int64_t>(r) * C, C, &M, &D);
+  if ((threadIdx.x & 63) == 0) out[r] = make_norm(M, D);
+}
+
 // Probability of one element given its row's (M, 1/D): 2^(z s - M) / D.
 __device__ __forceinline__ float prob(float z, float s, float M, float invD) {
   return __builtin_amdgcn_exp2f(fmaf(z, s, -M)) * invD;
+}
+
+// min(p, q) from one exponential: 2^(min(z_t s - M_t - L_t, z_d s - M_d - L_d)).
+// One more rounding than prob() (L enters as a float), about 1e-6 relative.
+__device__ __forceinline__ float min_prob(float zt, float zd, float s, const RowNorm& t, const RowNorm& d) {
+  return __builtin_amdgcn_exp2f(fminf(fmaf(zt, s, -t.M) - t.L, fmaf(zd, s, -d.M) - d.L));
 }
 
 // Rows of a batch: target rows (b, i) for i < tper, then draft rows (b, i)

@@ -1,19 +1,23 @@
 // tv_kernel.h — fused TV-loss forward and gradient w.r.t. the draft logits
 // (paper Sec. 4.1 Eqs. tv_loss / tv_grad, App. A, App. F; Sec. 4.2 Eq.
-// e2e_tv) in four launches that never wait on each other inside a launch:
+// e2e_tv) in six short launches that never wait on each other inside a
+// launch:
 //
 //   1 row_stats   (sv_device.h) per-chunk statistics of every target and
 //                 draft row of the N positions x K steps.
-//   2 tv_pair     per (position n, step k, chunk): alpha partial sum min(p, q)
+//   2 row_norm    (sv_device.h) each row's normaliser.
+//   3 tv_pair     per (position n, step k, chunk): alpha partial sum min(p, q)
 //                 and S partial sum 1[q <= p] q.
-//   3 tv_grad     per (position n, step k, chunk): alpha_k and S_k of all K
-//                 steps of the position, the chain factor g_k = dL_n/dalpha_k
-//                 of the selected loss (prefix / suffix products), then
-//                 grad = scale g_k (1/T) q (1[q <= p] - S_k) written once.  The
-//                 first chunk of step 0 also writes alpha[n, :] and L_n.
-//   4 tv_loss     one workgroup adds the N position losses in a fixed order.
+//   4 tv_coef     per position: alpha_k and S_k of its K steps (chunk order
+//                 fixed), the chain factors g_k = dL_n/dalpha_k of the selected
+//                 loss from prefix / suffix products, the position loss L_n,
+//                 alpha[n, :], and the two gradient coefficients of each step.
+//   5 tv_grad     per (position, step, chunk): grad = q * (1[q <= p] ? A1 : A0)
+//                 with A1 = scale g_k (1 - S_k) / T, A0 = -scale g_k S_k / T,
+//                 written once (skipped for a forward-only call).
+//   6 tv_loss     one workgroup adds the N position losses in a fixed order.
 // The indicator 1[q <= p] is evaluated by the same code on the same bits in
-// launches 2 and 3, so S and the gradient always agree on it.
+// launches 3 and 5, so S and the gradient always agree on it.
 #pragma once
 
 #include "sv_device.h"
@@ -33,7 +37,9 @@ struct TvArgs {
   float inv_t;
   float* loss; float* overlap; float* grad;
   const RowStat* stats;  // [2 N K][C]
+  const RowNorm* norms;  // [2 N K]
   TvPair* pairs;         // [N K][C]
+  float2* coef;          // [N K]: (A1, A0)
   double* loss_pos;      // [N]
   int vec_g;
 };
@@ -76,41 +82,10 @@ __device__ __forceinline__ void tv_rows(const TvArgs& a, int n, int k, int* rt_i
   *rd_i = a.N * a.K + n * a.K + k;
 }
 
-// Both rows' normalisers, combined by wave 0 and shared through LDS.
-__device__ __forceinline__ void tv_normalisers(const TvArgs& a, int rt_i, int rd_i, float* sh4) {
-  const int C = a.rows.C;
-  if (threadIdx.x < 64) {
-    float Mt, Md;
-    double Dt, Dd;
-    combine_row(a.stats + static_cast<int64_t>(rt_i) * C, C, &Mt, &Dt);
-    combine_row(a.stats + static_cast<int64_t>(rd_i) * C, C, &Md, &Dd);
-    if (threadIdx.x == 0) {
-      sh4[0] = Mt; sh4[1] = static_cast<float>(1.0 / Dt);
-      sh4[2] = Md; sh4[3] = static_cast<float>(1.0 / Dd);
-    }
-  }
-  __syncthreads();
-}
-
-// Per-step overlap and alpha / S of every step of position n, summed over the
-// chunks by one wave in the same order as the gradient launch uses.
-__device__ __forceinline__ void position_sums(const TvArgs& a, int n, double* al, double* S) {
-  const int lane = threadIdx.x & 63, C = a.rows.C;
-  for (int kk = 0; kk < a.K; ++kk) {
-    double x = 0.0, y = 0.0;
-    const TvPair* ps = a.pairs + static_cast<int64_t>(n * a.K + kk) * C;
-    for (int cc = lane; cc < C; cc += 64) { x += ps[cc].alpha; y += ps[cc].S; }
-    x = wave_sum(x);
-    y = wave_sum(y);
-    if (lane == 0) { al[kk] = x; S[kk] = y; }
-  }
-}
-
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a) {
   constexpr int EPV = E::EPV;
   __shared__ RedLds<4> red;
-  __shared__ float sh4[4];
   const RowsDesc& d = a.rows;
   const int C = d.C;
   const int u = blockIdx.x / C, c = blockIdx.x % C;
@@ -121,14 +96,13 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a) {
   const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
   const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
   const float s = scale_of(d.temp_scalar);
-  tv_normalisers(a, rt_i, rd_i, sh4);
-  const float Mt = sh4[0], it = sh4[1], Md = sh4[2], id = sh4[3];
+  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
   const int tile0 = c * NT;
-  const int nt = min(NT, d.ntiles - tile0);
+  const int nt_tiles = min(NT, d.ntiles - tile0);
   float al = 0.f, sq = 0.f;
 #pragma unroll
   for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt) break;
+    if (j0 >= nt_tiles) break;
     float xt[S][EPV], xd[S][EPV];
     load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
     load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
@@ -136,8 +110,8 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a) {
     for (int j = 0; j < S; ++j)
 #pragma unroll
       for (int kk = 0; kk < EPV; ++kk) {
-        const float p = prob(xt[j][kk], s, Mt, it);
-        const float q = prob(xd[j][kk], s, Md, id);
+        const float p = prob(xt[j][kk], s, nt.M, nt.invD);
+        const float q = prob(xd[j][kk], s, nd.M, nd.invD);
         al += fminf(p, q);
         sq += (q <= p) ? q : 0.f;
       }
@@ -151,13 +125,39 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a) {
   }
 }
 
+// Per position (one wave each, 4 per workgroup): alpha_k, S_k, the chain
+// factors, the loss L_n, alpha[n, :] and the gradient coefficients.
+__global__ __launch_bounds__(kThreads) void tv_coef_kernel(TvArgs a) {
+  __shared__ double al[kWaves][SPEC_MAX_K_DEV], S[kWaves][SPEC_MAX_K_DEV];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n = blockIdx.x * kWaves + wave;
+  if (n >= a.N) return;
+  const int C = a.rows.C, K = a.K;
+  for (int kk = 0; kk < K; ++kk) {
+    double x = 0.0, y = 0.0;
+    const TvPair* ps = a.pairs + static_cast<int64_t>(n * K + kk) * C;
+    for (int cc = lane; cc < C; cc += 64) { x += ps[cc].alpha; y += ps[cc].S; }
+    x = wave_sum(x);
+    y = wave_sum(y);
+    if (lane == 0) { al[wave][kk] = x; S[wave][kk] = y; }
+  }
+  if (lane == 0) {
+    double g[SPEC_MAX_K_DEV];
+    const double L = chain_factors(al[wave], K, a.mode, g);
+    a.loss_pos[n] = a.scale * L;
+    for (int kk = 0; kk < K; ++kk) {
+      if (a.overlap) a.overlap[static_cast<int64_t>(n) * K + kk] = static_cast<float>(al[wave][kk]);
+      const double gk = a.scale * g[kk] * static_cast<double>(a.inv_t);
+      a.coef[static_cast<int64_t>(n) * K + kk] =
+          make_float2(static_cast<float>(gk * (1.0 - S[wave][kk])), static_cast<float>(gk * (-S[wave][kk])));
+    }
+  }
+}
+
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
-  __shared__ float sh4[4];
-  __shared__ float shA[2];
-  __shared__ double sh_al[SPEC_MAX_K_DEV], sh_S[SPEC_MAX_K_DEV];
   const RowsDesc& d = a.rows;
   const int C = d.C, K = a.K, V = d.V;
   const int u = blockIdx.x / C, c = blockIdx.x % C;
@@ -168,30 +168,14 @@ __global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a) {
   const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
   const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
   const float s = scale_of(d.temp_scalar);
-  if (threadIdx.x < 64) {
-    position_sums(a, n, sh_al, sh_S);
-    if (threadIdx.x == 0) {
-      double g[SPEC_MAX_K_DEV];
-      const double L = chain_factors(sh_al, K, a.mode, g);
-      const double gk = a.scale * g[k] * static_cast<double>(a.inv_t);
-      shA[0] = static_cast<float>(gk * (1.0 - sh_S[k]));
-      shA[1] = static_cast<float>(gk * (-sh_S[k]));
-      if (k == 0 && c == 0) {
-        if (a.overlap)
-          for (int kk = 0; kk < K; ++kk) a.overlap[static_cast<int64_t>(n) * K + kk] = static_cast<float>(sh_al[kk]);
-        a.loss_pos[n] = a.scale * L;
-      }
-    }
-  }
-  tv_normalisers(a, rt_i, rd_i, sh4);
-  const float Mt = sh4[0], it = sh4[1], Md = sh4[2], id = sh4[3];
-  const float A1 = shA[0], A0 = shA[1];
+  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
+  const float2 A = a.coef[u];
   float* gr = a.grad + static_cast<int64_t>(u) * V;
   const int tile0 = c * NT;
-  const int nt = min(NT, d.ntiles - tile0);
+  const int nt_tiles = min(NT, d.ntiles - tile0);
 #pragma unroll
   for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt) break;
+    if (j0 >= nt_tiles) break;
     float xt[S][EPV], xd[S][EPV];
     load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
     load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
@@ -201,9 +185,9 @@ __global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a) {
       float gv[EPV];
 #pragma unroll
       for (int kk = 0; kk < EPV; ++kk) {
-        const float p = prob(xt[j][kk], s, Mt, it);
-        const float q = prob(xd[j][kk], s, Md, id);
-        gv[kk] = q * ((q <= p) ? A1 : A0);
+        const float p = prob(xt[j][kk], s, nt.M, nt.invD);
+        const float q = prob(xd[j][kk], s, nd.M, nd.invD);
+        gv[kk] = q * ((q <= p) ? A.x : A.y);
       }
       if (a.vec_g && v0 + EPV <= V) {
 #pragma unroll
@@ -217,20 +201,6 @@ __global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a) {
           if (v0 + kk < V) gr[v0 + kk] = gv[kk];
       }
     }
-  }
-}
-
-// Position losses and overlaps without a gradient (forward only): one wave
-// per position.
-__global__ __launch_bounds__(64) void tv_forward_kernel(TvArgs a) {
-  __shared__ double al[SPEC_MAX_K_DEV], S[SPEC_MAX_K_DEV];
-  const int n = blockIdx.x;
-  position_sums(a, n, al, S);
-  if (threadIdx.x == 0) {
-    double g[SPEC_MAX_K_DEV];
-    if (a.overlap)
-      for (int k = 0; k < a.K; ++k) a.overlap[static_cast<int64_t>(n) * a.K + k] = static_cast<float>(al[k]);
-    a.loss_pos[n] = a.scale * chain_factors(al, a.K, a.mode, g);
   }
 }
 

@@ -1,19 +1,24 @@
 // verify_kernel.h — chain rejection-sampling verification (paper Sec. 2.2,
-// Eq. reject_sample; App. G.1, Alg. rs_multinomial) in three launches that
+// Eq. reject_sample; App. G.1, Alg. rs_multinomial) in four launches that
 // never wait on each other inside a launch:
 //
 //   1 row_stats   (sv_device.h) every target and draft row, split into
 //                 chunks of NT tiles: per-chunk (max reference, exp2 sum).
-//   2 pair_pass   every (target row i, draft row i) pair, i < K, chunk by
-//                 chunk: p and q from the combined row statistics, then the
-//                 chunk's overlap sum min(p, q) and residual mass
-//                 sum max(0, p - q).  Bonus rows need no second read.
-//   3 finish      one workgroup per batch row: accept tests from the two
-//                 gathered logits in float64 and Philox uniforms, accept
-//                 length, overlap, and the resample: the chunk whose
-//                 cumulative mass crosses u' Z is found from the per-chunk
-//                 masses, and only that chunk is read again to invert the
-//                 CDF inside it (tile sums, thread scan, element scan).
+//   2 decide      one workgroup per batch row: each row's normaliser from its
+//                 chunk statistics; the K accept tests in parallel lanes
+//                 (float64, u q(x) < p(x) with the two gathered logits and
+//                 Philox uniforms); accept length; every output except the
+//                 overlaps and the resampled token.
+//   3 pair_pass   every (target row i, draft row i) pair, chunk by chunk:
+//                 overlap sum min(p, q); for the row's first rejected step
+//                 also the residual mass sum max(0, p - q).  Bonus rows are
+//                 not read again, and without an overlap output only the
+//                 first rejected step's pair is.
+//   4 finish      one workgroup per batch row: overlaps; the chunk whose
+//                 cumulative residual (or bonus) mass crosses u' Z, found
+//                 from the per-chunk masses; only that chunk is read again
+//                 to invert the CDF inside it (tile sums, thread scan,
+//                 element scan).
 #pragma once
 
 #include "sv_device.h"
@@ -33,6 +38,8 @@ struct VerifyArgs {
   int32_t* accept_len; int32_t* emitted;
   float* overlap; float* p_at; float* q_at; float* logz_t; float* logz_d;
   const RowStat* stats;   // [rows][C]
+  RowNorm* norms;         // [rows]
+  int32_t* decision;      // [B]: accept length n, or -1 for a row with a data error
   PairStat* pairs;        // [B*K][C]
 };
 
@@ -41,54 +48,133 @@ __device__ __forceinline__ int draft_row(const VerifyArgs& a, int b, int i) {
   return a.B * (a.K + 1) + b * a.K + i;
 }
 
-// Pass 2 over one chunk of a (target, draft) pair: overlap and residual mass.
+// Row normalisers and accept decisions, one workgroup per batch row.
+template <class E>
+__global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
+  using raw = typename E::raw;
+  __shared__ RowNorm nrm[2 * SPEC_MAX_K_DEV + 1];
+  __shared__ double px[SPEC_MAX_K_DEV], qx[SPEC_MAX_K_DEV];
+  __shared__ int acc[SPEC_MAX_K_DEV], badx[SPEC_MAX_K_DEV];
+  const RowsDesc& d = a.rows;
+  const int K = a.K, C = d.C, V = d.V;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const float T = temperature_of(d, b);
+  const bool t_ok = temperature_ok(T);
+  const float s = t_ok ? scale_of(T) : 1.0f;
+  // row j < K+1: target row j; row K+1+i: draft row i (one wave per row)
+  for (int j = wave; j < 2 * K + 1; j += kWaves) {
+    const int r = j <= K ? target_row(a, b, j) : draft_row(a, b, j - K - 1);
+    float M;
+    double D;
+    combine_row(a.stats + static_cast<int64_t>(r) * C, C, &M, &D);
+    if (lane == 0) {
+      const RowNorm nm = make_norm(M, D);
+      nrm[j] = nm;
+      a.norms[r] = nm;
+    }
+  }
+  __syncthreads();
+  // accept tests in float64: u q(x) < p(x), no division; one lane per step
+  if (tid < K) {
+    const int i = tid;
+    const int x = a.ids[static_cast<int64_t>(b) * K + i];
+    const RowNorm& nt = nrm[i];
+    const RowNorm& nd = nrm[K + 1 + i];
+    int ok = 0, bad = 1;
+    double p = 0.0, q = 0.0;
+    if (x >= 0 && x < V) {
+      bad = 0;
+      if (t_ok && norm_ok(nt) && norm_ok(nd)) {
+        int bb;
+        bool al;
+        const raw* rt = row_of<E>(d, target_row(a, b, i), &bb, &al);
+        const raw* rd = row_of<E>(d, draft_row(a, b, i), &bb, &al);
+        p = exp2(static_cast<double>(E::one(rt + x)) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
+        q = exp2(static_cast<double>(E::one(rd + x)) * static_cast<double>(s) - static_cast<double>(nd.M)) / nd.D;
+        const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(i), a.offset, 0ull,
+                                           a.seed, 0ull);
+        ok = (u24(g.w[0]) * q < p) ? 1 : 0;
+      }
+    }
+    px[i] = p; qx[i] = q; acc[i] = ok; badx[i] = bad;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    bool err = !t_ok;
+    for (int j = 0; j < 2 * K + 1; ++j)
+      if (!norm_ok(nrm[j])) err = true;
+    int n = K;
+    for (int i = 0; i < K; ++i) {
+      if (badx[i]) err = true;
+      if (n == K && !acc[i]) n = i;  // the first rejection ends the chain
+    }
+    a.decision[b] = err ? -1 : n;
+    a.accept_len[b] = err ? -1 : n;
+    int32_t* em = a.emitted + static_cast<int64_t>(b) * (K + 1);
+    const int32_t* xb = a.ids + static_cast<int64_t>(b) * K;
+    for (int j = 0; j <= K; ++j)
+      if (err || j != n) em[j] = (!err && j < n) ? xb[j] : -1;  // emitted[n] is written by finish
+    for (int i = 0; i < K; ++i) {
+      const int64_t o = static_cast<int64_t>(b) * K + i;
+      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(px[i]);
+      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(qx[i]);
+      if (a.logz_d) a.logz_d[o] = err ? NAN : static_cast<float>((static_cast<double>(nrm[K + 1 + i].M) + log2(nrm[K + 1 + i].D)) * kLn2D);
+      if (a.overlap && err) a.overlap[o] = NAN;
+    }
+    if (a.logz_t)
+      for (int i = 0; i <= K; ++i)
+        a.logz_t[static_cast<int64_t>(b) * (K + 1) + i] =
+            err ? NAN : static_cast<float>((static_cast<double>(nrm[i].M) + log2(nrm[i].D)) * kLn2D);
+  }
+}
+
+// Pass 2 over one chunk of a (target, draft) pair: overlap, and the residual
+// mass when this is the row's first rejected step.
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a) {
   constexpr int EPV = E::EPV;
   __shared__ RedLds<4> red;
-  __shared__ float sh_f[4];
   const RowsDesc& d = a.rows;
   const int C = d.C;
   const int u = blockIdx.x / C, c = blockIdx.x % C;
   const int b = u / a.K, i = u % a.K;
+  const int n = a.decision[b];
+  if (n < 0) return;  // data error: finish ignores this row's partials
+  const bool need_z = i == n;
+  if (!need_z && a.overlap == nullptr) return;  // no overlap requested: only the residual step is read again
   const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
   int bb;
   bool al_t, al_d;
   const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
   const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
-  const float T = temperature_of(d, b);
-  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-  if (threadIdx.x < 64) {
-    float Mt, Md;
-    double Dt, Dd;
-    combine_row(a.stats + static_cast<int64_t>(rt_i) * C, C, &Mt, &Dt);
-    combine_row(a.stats + static_cast<int64_t>(rd_i) * C, C, &Md, &Dd);
-    if (threadIdx.x == 0) {
-      sh_f[0] = Mt; sh_f[1] = static_cast<float>(1.0 / Dt);
-      sh_f[2] = Md; sh_f[3] = static_cast<float>(1.0 / Dd);
-    }
-  }
-  __syncthreads();
-  const float Mt = sh_f[0], it = sh_f[1], Md = sh_f[2], id = sh_f[3];
+  const float s = scale_of(temperature_of(d, b));
+  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
   const int tile0 = c * NT;
-  const int nt = min(NT, d.ntiles - tile0);
+  const int nt_tiles = min(NT, d.ntiles - tile0);
   float al = 0.f, zr = 0.f;
 #pragma unroll
   for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt) break;
+    if (j0 >= nt_tiles) break;
     float xt[S][EPV], xd[S][EPV];
     load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
     load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
+    if (need_z) {
 #pragma unroll
-    for (int j = 0; j < S; ++j)
+      for (int j = 0; j < S; ++j)
 #pragma unroll
-      for (int k = 0; k < EPV; ++k) {
-        const float p = prob(xt[j][k], s, Mt, it);
-        const float q = prob(xd[j][k], s, Md, id);
-        const float mn = fminf(p, q);
-        al += mn;
-        zr += p - mn;
-      }
+        for (int k = 0; k < EPV; ++k) {
+          const float p = prob(xt[j][k], s, nt.M, nt.invD);
+          const float mn = fminf(p, prob(xd[j][k], s, nd.M, nd.invD));
+          al += mn;
+          zr += p - mn;
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < S; ++j)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) al += min_prob(xt[j][k], xd[j][k], s, nt, nd);
+    }
   }
   double v[4] = {static_cast<double>(al), static_cast<double>(zr), 0.0, 0.0};
   wg_sum<4>(v, red);
@@ -116,16 +202,12 @@ __device__ __forceinline__ void vector_masses(const typename E::raw* rt, const t
 }
 
 struct FinishShared {
-  float M[2 * SPEC_MAX_K_DEV + 1];
-  double D[2 * SPEC_MAX_K_DEV + 1];
   double alpha[SPEC_MAX_K_DEV];
-  double px[SPEC_MAX_K_DEV], qx[SPEC_MAX_K_DEV];
   double tin;
-  int err, n, cstar, residual, token;
+  int cstar, residual, token;
 };
 
-// One workgroup per batch row: accept tests, accept length, overlap and the
-// resampled / bonus token.
+// One workgroup per batch row: overlaps and the resampled / bonus token.
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   constexpr int EPV = E::EPV;
@@ -137,74 +219,21 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   const RowsDesc& d = a.rows;
   const int K = a.K, C = d.C, V = d.V;
   const int b = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const float T = temperature_of(d, b);
-  const bool t_ok = temperature_ok(T);
-  const float s = t_ok ? scale_of(T) : 1.0f;
-  const int32_t* xb = a.ids + static_cast<int64_t>(b) * K;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int n = a.decision[b];
+  if (n < 0) return;  // data error: decide has written every output of the row
+  const float s = scale_of(temperature_of(d, b));
 
-  // row normalisers of the 2K+1 rows and the overlap of every draft step (wave 0)
-  if (tid < 64) {
-    for (int i = 0; i <= K; ++i) {
-      float M;
-      double D;
-      combine_row(a.stats + static_cast<int64_t>(target_row(a, b, i)) * C, C, &M, &D);
-      if (lane == 0) { sh.M[i] = M; sh.D[i] = D; }
-    }
-    for (int i = 0; i < K; ++i) {
-      float M;
-      double D;
-      combine_row(a.stats + static_cast<int64_t>(draft_row(a, b, i)) * C, C, &M, &D);
-      if (lane == 0) { sh.M[K + 1 + i] = M; sh.D[K + 1 + i] = D; }
-    }
-    for (int i = 0; i < K; ++i) {
-      double al = 0.0;
-      const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + i) * C;
-      for (int cc = lane; cc < C; cc += 64) al += ps[cc].alpha;
-      al = wave_sum(al);
-      if (lane == 0) sh.alpha[i] = al;
-    }
+  // overlap of every draft step (one wave per step, chunk order fixed)
+  for (int i = wave; i < K && a.overlap != nullptr; i += kWaves) {
+    double al = 0.0;
+    const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + i) * C;
+    for (int cc = lane; cc < C; cc += 64) al += ps[cc].alpha;
+    al = wave_sum(al);
+    if (lane == 0) sh.alpha[i] = al;
   }
-  __syncthreads();
-
-  // accept tests in float64, u q(x) < p(x) with no division; first rejection ends the chain
-  if (tid == 0) {
-    bool err = !t_ok;
-    for (int i = 0; i < 2 * K + 1; ++i)
-      if (!(sh.D[i] > 0.0 && sh.D[i] < INFINITY && sh.M[i] < INFINITY)) err = true;
-    int n = K;
-    for (int i = 0; i < K; ++i) {
-      const int x = xb[i];
-      sh.px[i] = 0.0;
-      sh.qx[i] = 0.0;
-      if (x < 0 || x >= V) { err = true; continue; }
-      if (err) continue;
-      int bb;
-      bool al;
-      const raw* rt = row_of<E>(d, target_row(a, b, i), &bb, &al);
-      const raw* rd = row_of<E>(d, draft_row(a, b, i), &bb, &al);
-      const double px = exp2(static_cast<double>(E::one(rt + x)) * static_cast<double>(s) -
-                             static_cast<double>(sh.M[i])) / sh.D[i];
-      const double qx = exp2(static_cast<double>(E::one(rd + x)) * static_cast<double>(s) -
-                             static_cast<double>(sh.M[K + 1 + i])) / sh.D[K + 1 + i];
-      sh.px[i] = px;
-      sh.qx[i] = qx;
-      if (n == K) {
-        const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(i), a.offset, 0ull,
-                                           a.seed, 0ull);
-        if (!(u24(g.w[0]) * qx < px)) n = i;
-      }
-    }
-    sh.err = err ? 1 : 0;
-    sh.n = n;
-    sh.cstar = -1;
-  }
-  __syncthreads();
-  const bool err = sh.err != 0;
-  const int n = sh.n;
-
   // the chunk holding the sampling target (wave 0)
-  if (!err && tid < 64) {
+  if (wave == 0) {
     const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + (n < K ? n : 0)) * C;
     double zs = 0.0;
     if (n < K) {
@@ -214,15 +243,14 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     // residual of the rejected step; p_n itself for the bonus row or an empty residual
     const bool residual = n < K && zs > 0.0;
     const RowStat* st = a.stats + static_cast<int64_t>(target_row(a, b, n)) * C;
-    const float Mn = sh.M[n];
-    const double Dn = sh.D[n];
+    const RowNorm nn = a.norms[target_row(a, b, n)];
     const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(n), a.offset, 0ull,
                                        a.seed, 0ull);
     double tot = 0.0;
     for (int cc = lane; cc < C; cc += 64) {
       const float mc = st[cc].m;
       tot += residual ? ps[cc].Z
-                      : (mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - Mn)) / Dn);
+                      : (mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - nn.M)) / nn.D);
     }
     tot = wave_sum(tot);
     const double target = u24(g.w[1]) * tot;
@@ -234,7 +262,7 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
       if (cc < C) {
         const float mc = st[cc].m;
         zc = residual ? ps[cc].Z
-                      : (mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - Mn)) / Dn);
+                      : (mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - nn.M)) / nn.D);
       }
       const double incl = carry + wave_incl_scan(zc);
       const double excl = incl - zc;
@@ -259,24 +287,23 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
 
   // inverse CDF inside the chosen chunk (whole workgroup)
   int token = -1;
-  if (!err && sh.cstar >= 0) {
+  if (sh.cstar >= 0) {
     const int cstar = sh.cstar;
     const bool residual = sh.residual != 0;
     int bb;
     bool al_t, al_d;
     const raw* rt = row_of<E>(d, target_row(a, b, n), &bb, &al_t);
     const raw* rd = row_of<E>(d, draft_row(a, b, n < K ? n : 0), &bb, &al_d);
-    const float Mt = sh.M[n], it = static_cast<float>(1.0 / sh.D[n]);
-    const float Md = n < K ? sh.M[K + 1 + n] : 0.f;
-    const float id = n < K ? static_cast<float>(1.0 / sh.D[K + 1 + n]) : 0.f;
+    const RowNorm nt = a.norms[target_row(a, b, n)];
+    const RowNorm nd = a.norms[draft_row(a, b, n < K ? n : 0)];
     const int tile0 = cstar * NT;
-    const int nt = min(NT, d.ntiles - tile0);
+    const int nt_tiles = min(NT, d.ntiles - tile0);
     float tsum[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) tsum[j] = 0.f;
 #pragma unroll
     for (int j0 = 0; j0 < NT; j0 += S) {
-      if (j0 >= nt) break;
+      if (j0 >= nt_tiles) break;
       float xt[S][EPV], xd[S][EPV];
       load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
       if (residual) load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
@@ -284,20 +311,20 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
       for (int j = 0; j < S; ++j)
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
-          const float p = prob(xt[j][k], s, Mt, it);
-          tsum[j0 + j] += residual ? p - fminf(p, prob(xd[j][k], s, Md, id)) : p;
+          const float p = prob(xt[j][k], s, nt.M, nt.invD);
+          tsum[j0 + j] += residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
         }
     }
     double W[NT];
 #pragma unroll
-    for (int j = 0; j < NT; ++j) W[j] = (j < nt) ? static_cast<double>(tsum[j]) : 0.0;
+    for (int j = 0; j < NT; ++j) W[j] = (j < nt_tiles) ? static_cast<double>(tsum[j]) : 0.0;
     wg_sum<NT>(W, redv);  // tile totals, identical in every thread
     const double tin = sh.tin;
     int jstar = -1, jlast = -1;
     double cum = 0.0, t_in = 0.0;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-      if (j < nt) {
+      if (j < nt_tiles) {
         if (W[j] > 0.0) jlast = j;
         if (jstar < 0 && cum + W[j] > tin) { jstar = j; t_in = tin - cum; }
         cum += W[j];
@@ -323,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
       if (tid == tstar) {
         const int v0 = (tile0 + jstar) * TILE + tid * EPV;
         float r[EPV];
-        vector_masses<E>(rt, rd, residual, v0, V, s, Mt, it, Md, id, r);
+        vector_masses<E>(rt, rd, residual, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
         const double tl = t_in - excl;
         float cumf = 0.f;
         int kstar = -1, klast = -1;
@@ -341,24 +368,11 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     }
   }
 
-  // outputs: every per-row output has this single writer
+  // the overlaps and emitted[n] have this single writer
   if (tid == 0) {
-    int32_t* em = a.emitted + static_cast<int64_t>(b) * (K + 1);
-    a.accept_len[b] = err ? -1 : n;
-    for (int j = 0; j <= K; ++j) em[j] = err ? -1 : ((j < n) ? xb[j] : ((j == n) ? token : -1));
-    for (int i = 0; i < K; ++i) {
-      const int64_t o = static_cast<int64_t>(b) * K + i;
-      if (a.overlap) a.overlap[o] = err ? NAN : static_cast<float>(sh.alpha[i]);
-      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(sh.px[i]);
-      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(sh.qx[i]);
-      if (a.logz_d)
-        a.logz_d[o] = err ? NAN
-                          : static_cast<float>((static_cast<double>(sh.M[K + 1 + i]) + log2(sh.D[K + 1 + i])) * kLn2D);
-    }
-    if (a.logz_t)
-      for (int i = 0; i <= K; ++i)
-        a.logz_t[static_cast<int64_t>(b) * (K + 1) + i] =
-            err ? NAN : static_cast<float>((static_cast<double>(sh.M[i]) + log2(sh.D[i])) * kLn2D);
+    a.emitted[static_cast<int64_t>(b) * (K + 1) + n] = token;
+    if (a.overlap)
+      for (int i = 0; i < K; ++i) a.overlap[static_cast<int64_t>(b) * K + i] = static_cast<float>(sh.alpha[i]);
   }
 }
 

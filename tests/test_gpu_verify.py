@@ -152,6 +152,25 @@ def test_determinism_and_seed():
     assert not torch.equal(a["emitted"], c["emitted"])
 
 
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_without_overlap_output(dtype):
+    """With no overlap requested only the first rejected pair is read again;
+    accept lengths, tokens and the debug outputs must not change."""
+    d = W.verify_inputs_numpy(24, 3, 50000, dtype, "rollout_t", 77)
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    full = binding.verify(tgt, drf, ids, T, 5, 2, want_debug=True)
+    lean = binding.verify(tgt, drf, ids, T, 5, 2, want_debug=True, want_overlap=False)
+    torch.cuda.synchronize()
+    assert "overlap" not in lean
+    for k in lean:
+        assert torch.equal(full[k], lean[k]), k
+    ref = oracle.verify_ref(W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype), d["ids"],
+                            d["temperature"].astype(np.float64), 5, 2)
+    compare_verify(lean, ref, dtype)
+
+
 def _sampled(cfg_name, nsample, seed=0):
     cfg = W.CONFIGS[cfg_name]
     d = W.verify_inputs_torch(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], cfg["gen"], cfg["seed"])
