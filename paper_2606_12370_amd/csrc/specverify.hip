@@ -22,6 +22,13 @@ using sv::F32;
 constexpr int kNtBf16 = 8;
 constexpr int kNtF32 = 16;
 constexpr int kStep = 4;
+constexpr int kChunkElems = 16384;
+static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
+static_assert(kNtF32 * sv::kThreads * sv::F32::EPV == kChunkElems, "chunk geometry");
+static_assert(kChunkElems % (sv::kThreads * sv::BF16H::EPV) == 0, "chunk geometry");
+
+template <class E> struct GradElem { using type = E; };
+template <> struct GradElem<sv::BF16> { using type = sv::BF16H; };
 
 int epv_of(spec_dtype dt) { return dt == SPEC_BF16 ? BF16::EPV : F32::EPV; }
 int nt_of(spec_dtype dt) { return dt == SPEC_BF16 ? kNtBf16 : kNtF32; }
@@ -118,9 +125,11 @@ spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
                      0, s, a);
   hipLaunchKernelGGL(sv::tv_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
+  // the gradient pass reads bf16 as 4-element vectors: one coalesced float4 store per lane
+  using G = typename GradElem<E>::type;
   if (a.grad)
-    hipLaunchKernelGGL((sv::tv_grad_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(units * C)),
-                       dim3(sv::kThreads), 0, s, a);
+    hipLaunchKernelGGL((sv::tv_grad_kernel<G, kChunkElems / (sv::kThreads * G::EPV), kStep>),
+                       dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a);
   hipLaunchKernelGGL(sv::tv_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }

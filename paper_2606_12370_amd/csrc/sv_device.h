@@ -19,15 +19,20 @@ constexpr double kLn2D = 0.69314718055994530942;
 // 16-byte vector types the compiler treats as native vectors (needed by the
 // non-temporal load / store builtins).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // Element types: logits arrive as bfloat16 bit patterns or float32.  Each
-// thread owns one 16-byte vector per tile, i.e. EPV consecutive elements.
+// thread owns one vector per tile, i.e. EPV consecutive elements, loaded with
+// one instruction.  BF16 and F32 use 16-byte vectors; BF16H reads bfloat16
+// as 8-byte vectors of 4, so that a pass writing one float32 per element
+// stores one contiguous 16-byte vector per lane.
 struct BF16 {
   using raw = uint16_t;
+  using vec = u32x4;
   static constexpr int EPV = 8;
-  static __device__ __forceinline__ void widen(const uint4 v, float (&x)[8]) {
+  static __device__ __forceinline__ void widen(const vec v, float (&x)[8]) {
     x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xffff0000u);
     x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xffff0000u);
     x[4] = __uint_as_float(v.z << 16); x[5] = __uint_as_float(v.z & 0xffff0000u);
@@ -38,10 +43,22 @@ struct BF16 {
   }
 };
 
+struct BF16H {
+  using raw = uint16_t;
+  using vec = u32x2;
+  static constexpr int EPV = 4;
+  static __device__ __forceinline__ void widen(const vec v, float (&x)[4]) {
+    x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xffff0000u);
+    x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xffff0000u);
+  }
+  static __device__ __forceinline__ float one(const raw* p) { return BF16::one(p); }
+};
+
 struct F32 {
   using raw = float;
+  using vec = u32x4;
   static constexpr int EPV = 4;
-  static __device__ __forceinline__ void widen(const uint4 v, float (&x)[4]) {
+  static __device__ __forceinline__ void widen(const vec v, float (&x)[4]) {
     x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y);
     x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
   }
@@ -51,7 +68,7 @@ struct F32 {
 // Load S tiles (tile0 .. tile0+S-1) of a row: x[j][k] receives element
 // (tile0 + j) * 256 * EPV + t * EPV + k of the row, t = threadIdx.x.  Elements
 // at or beyond V are -inf (probability 0).  With `aligned` (row base 16-byte
-// aligned) every full vector is one 16-byte load, all issued back to back; a
+// aligned) every full vector is one vector load, all issued back to back; a
 // vector past V is read from the row start and discarded (no branch around
 // the load); the one vector that straddles V (V not a multiple of EPV) is
 // completed element by element.  Unaligned rows are read element by element.
@@ -62,17 +79,17 @@ __device__ __forceinline__ void load_tiles(const typename E::raw* __restrict__ r
   constexpr int TILE = 256 * EPV;
   const int t = threadIdx.x;
   if (aligned) {
-    u32x4 w[S];
+    typename E::vec w[S];
 #pragma unroll
     for (int j = 0; j < S; ++j) {
       const int v0 = (tile0 + j) * TILE + t * EPV;
       const int off = (v0 + EPV <= V) ? v0 : 0;
-      w[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + off));
+      w[j] = __builtin_nontemporal_load(reinterpret_cast<const typename E::vec*>(row + off));
     }
 #pragma unroll
     for (int j = 0; j < S; ++j) {
       const int v0 = (tile0 + j) * TILE + t * EPV;
-      E::widen(make_uint4(w[j].x, w[j].y, w[j].z, w[j].w), x[j]);
+      E::widen(w[j], x[j]);
       if (v0 + EPV > V) {
 #pragma unroll
         for (int k = 0; k < EPV; ++k) x[j][k] = (v0 + k < V) ? E::one(row + v0 + k) : -INFINITY;

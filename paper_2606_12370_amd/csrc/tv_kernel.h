@@ -171,8 +171,10 @@ __global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a) {
   const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
   const float2 A = a.coef[u];
   float* gr = a.grad + static_cast<int64_t>(u) * V;
+  // this kernel may read with a narrower vector than the statistics passes, so
+  // its tile count comes from its own tile width (the chunk is the same)
   const int tile0 = c * NT;
-  const int nt_tiles = min(NT, d.ntiles - tile0);
+  const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
 #pragma unroll
   for (int j0 = 0; j0 < NT; j0 += S) {
     if (j0 >= nt_tiles) break;
