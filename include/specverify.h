@@ -117,7 +117,10 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
                         float* logz_target, float* logz_draft,
                         void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of workspace spec_tv_loss_fwd_bwd needs (0 on invalid sizes). */
+/* Bytes of workspace spec_tv_loss_fwd_bwd needs (0 on invalid sizes).  It
+ * includes about one bit per logit (N*K*ceil(V/16384)*2048 bytes, about 1/32
+ * of the gradient): the indicator 1[q <= p] of the forward pass, which the
+ * gradient pass reads instead of the target logits. */
 size_t spec_tv_workspace_size(int N, int K, int V, spec_dtype dtype);
 
 /*

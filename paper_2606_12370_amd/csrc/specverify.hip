@@ -6,6 +6,9 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <map>
+#include <mutex>
+#include <utility>
 
 #include "specverify.h"
 #include "sv_device.h"
@@ -77,7 +80,7 @@ VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt) {
 }
 
 struct TvLayout {
-  size_t stats = 0, norms = 0, pairs = 0, coef = 0, loss = 0, total = 0;
+  size_t stats = 0, norms = 0, pairs = 0, coef = 0, loss = 0, bits = 0, bits_stride = 0, total = 0;
 };
 TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
   TvLayout L;
@@ -89,6 +92,9 @@ TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
   L.pairs = off; off = align_up(off + static_cast<size_t>(N) * K * C * sizeof(sv::TvPair), 256);
   L.coef = off; off = align_up(off + static_cast<size_t>(N) * K * sizeof(float2), 256);
   L.loss = off; off = align_up(off + static_cast<size_t>(N) * sizeof(double), 256);
+  // indicator bits 1[q <= p] for the gradient pass: one 64-bit word per thread and chunk
+  L.bits_stride = C * sv::kChunkWords * sizeof(uint64_t);
+  L.bits = off; off = align_up(off + static_cast<size_t>(N) * K * L.bits_stride, 256);
   L.total = off;
   return L;
 }
@@ -99,14 +105,49 @@ bool rows_vec_aligned(const void* base, int64_t s0, int64_t s1, size_t esize) {
          ((s1 * static_cast<int64_t>(esize)) % 16 == 0);
 }
 
+// Workgroups of `kernel` (256 threads, static LDS only) the current device
+// holds at once, queried once per (device, kernel).  The second passes over
+// the pairs are launched with min(tasks, this) workgroups striding over their
+// tasks (no partial last round of workgroups); every streaming kernel is
+// written grid-stride, and the others run one workgroup per task, which
+// measured faster for them.
+// Returns 0 if the runtime cannot tell (the caller then launches one
+// workgroup per task).
+int64_t resident_blocks(const void* kernel) {
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, int64_t> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> g(mu);
+  const auto key = std::make_pair(dev, kernel);
+  const auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int cus = 0, per_cu = 0;
+  int64_t n = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, sv::kThreads, 0) == hipSuccess)
+    n = int64_t{cus} * per_cu;
+  cache[key] = n;
+  return n;
+}
+
+unsigned grid_for(const void* kernel, int64_t tasks) {
+  const int64_t r = resident_blocks(kernel);
+  return static_cast<unsigned>((r > 0 && r < tasks) ? r : tasks);
+}
+
 template <class E, int NT>
 spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) {
   const int C = a.rows.C;
-  hipLaunchKernelGGL((sv::row_stats_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(rows * C)),
-                     dim3(sv::kThreads), 0, s, a.rows, const_cast<sv::RowStat*>(a.stats));
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  // one workgroup per task: measured faster for this first, purely streaming pass
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(rows * C)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), rows * C);
   hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
-  hipLaunchKernelGGL((sv::pair_pass_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(int64_t{a.B} * a.K * C)),
-                     dim3(sv::kThreads), 0, s, a);
+  void (*pp)(sv::VerifyArgs, int64_t) = sv::pair_pass_kernel<E, NT, kStep>;
+  const int64_t pairs = int64_t{a.B} * a.K * C;
+  hipLaunchKernelGGL(pp, dim3(grid_for(reinterpret_cast<const void*>(pp), pairs)), dim3(sv::kThreads), 0, s, a,
+                     pairs);
   hipLaunchKernelGGL((sv::finish_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s,
                      a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
@@ -116,20 +157,24 @@ template <class E, int NT>
 spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
   const int64_t units = int64_t{a.N} * a.K;
   const int C = a.rows.C;
-  hipLaunchKernelGGL((sv::row_stats_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(2 * units * C)),
-                     dim3(sv::kThreads), 0, s, a.rows, const_cast<sv::RowStat*>(a.stats));
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(2 * units * C)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), 2 * units * C);
   hipLaunchKernelGGL(sv::row_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C,
                      const_cast<sv::RowNorm*>(a.norms));
-  hipLaunchKernelGGL((sv::tv_pair_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads),
-                     0, s, a);
+  void (*tp)(sv::TvArgs, int64_t) = sv::tv_pair_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(tp, dim3(grid_for(reinterpret_cast<const void*>(tp), units * C)), dim3(sv::kThreads), 0, s, a,
+                     units * C);
   hipLaunchKernelGGL(sv::tv_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
   // the gradient pass reads bf16 as 4-element vectors: one coalesced float4 store per lane
   using G = typename GradElem<E>::type;
-  if (a.grad)
-    hipLaunchKernelGGL((sv::tv_grad_kernel<G, kChunkElems / (sv::kThreads * G::EPV), kStep>),
-                       dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a);
+  if (a.grad) {
+    void (*tg)(sv::TvArgs, int64_t) = sv::tv_grad_kernel<G, kChunkElems / (sv::kThreads * G::EPV), kStep, E::EPV>;
+    // one workgroup per task (measured faster than a resident grid for this read+write pass)
+    hipLaunchKernelGGL(tg, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a, units * C);
+  }
   hipLaunchKernelGGL(sv::tv_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
@@ -248,6 +293,8 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   a.coef = reinterpret_cast<float2*>(ws + L.coef);
   a.loss_pos = reinterpret_cast<double*>(ws + L.loss);
   a.vec_g = (grad_draft && aligned16(grad_draft) && (V % 4 == 0)) ? 1 : 0;
+  a.bits = grad_draft ? reinterpret_cast<uint8_t*>(ws + L.bits) : nullptr;
+  a.bits_stride = static_cast<int64_t>(L.bits_stride);
   hipStream_t s = static_cast<hipStream_t>(stream);
   return dtype == SPEC_BF16 ? launch_tv<BF16, kNtBf16>(a, s) : launch_tv<F32, kNtF32>(a, s);
 }

@@ -401,23 +401,27 @@ __device__ __forceinline__ bool temperature_ok(float T) { return T > 0.f && T < 
 
 // One workgroup per (row, chunk): the chunk's statistics (pass 1).
 template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat* __restrict__ stats) {
+__global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat* __restrict__ stats, int64_t ntasks) {
   __shared__ RedLds<4> red;
-  const int r = blockIdx.x / d.C, c = blockIdx.x % d.C;
-  int b;
-  bool aligned;
-  const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
-  const float T = temperature_of(d, b);
-  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-  const int tile0 = c * NT;
-  const int nt = min(NT, d.ntiles - tile0);
-  float m;
-  double D;
-  chunk_stats<E, NT, S>(row, tile0, nt, d.V, aligned, s, red, &m, &D);
-  if (threadIdx.x == 0) {
-    RowStat o;
-    o.m = m; o.pad = 0.f; o.D = D;
-    stats[blockIdx.x] = o;
+  // persistent: the grid is sized to what the device holds at once and
+  // strides over the (row, chunk) tasks
+  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
+    const int r = static_cast<int>(t / d.C), c = static_cast<int>(t - static_cast<int64_t>(t / d.C) * d.C);
+    int b;
+    bool aligned;
+    const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+    const float T = temperature_of(d, b);
+    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+    const int tile0 = c * NT;
+    const int nt = min(NT, d.ntiles - tile0);
+    float m;
+    double D;
+    chunk_stats<E, NT, S>(row, tile0, nt, d.V, aligned, s, red, &m, &D);
+    if (threadIdx.x == 0) {
+      RowStat o;
+      o.m = m; o.pad = 0.f; o.D = D;
+      stats[t] = o;
+    }
   }
 }
 

@@ -41,6 +41,8 @@ struct TvArgs {
   TvPair* pairs;         // [N K][C]
   float2* coef;          // [N K]: (A1, A0)
   double* loss_pos;      // [N]
+  uint8_t* bits;         // [N K][bits_stride]: bit (v % 8) of byte v / 8 = 1[q_v <= p_v]; NULL without gradient
+  int64_t bits_stride;   // bytes per (position, step)
   int vec_g;
 };
 
@@ -82,46 +84,79 @@ __device__ __forceinline__ void tv_rows(const TvArgs& a, int n, int k, int* rt_i
   *rd_i = a.N * a.K + n * a.K + k;
 }
 
+// Indicator bits 1[q <= p] of the forward pass, for the gradient pass.  The
+// thread that handles elements of a chunk keeps their bits in one 64-bit word
+// (tile j of the chunk at bits j*EPV .. j*EPV+EPV-1, EPV elements per vector)
+// and stores it once per chunk: word (chunk, thread) of a (position, step)
+// row, 2 KB per chunk.  kChunkWords = threads per chunk.
+constexpr int kChunkWords = kThreads;
+
+// The 4 bits of elements e .. e+3 (e % 4 == 0, offset e inside chunk c) for
+// data read EPVW elements per vector by the forward pass.
+template <int EPVW>
+__device__ __forceinline__ uint32_t load_bits4(const uint8_t* row_bits, int c, int e) {
+  static_assert(EPVW == 8 || EPVW == 4, "vector width");
+  constexpr int TILEW = kThreads * EPVW;
+  const int wt = (e % TILEW) / EPVW;                // the writing thread
+  const int bit = (e / TILEW) * EPVW + (e % EPVW);  // its bit of element e
+  const uint32_t byte = row_bits[(static_cast<int64_t>(c) * kChunkWords + wt) * 8 + (bit >> 3)];
+  return (byte >> (bit & 7)) & 15u;
+}
+
 template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a) {
+__global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   __shared__ RedLds<4> red;
   const RowsDesc& d = a.rows;
   const int C = d.C;
-  const int u = blockIdx.x / C, c = blockIdx.x % C;
-  const int n = u / a.K, k = u % a.K;
-  int rt_i, rd_i, bb;
-  bool al_t, al_d;
-  tv_rows<E>(a, n, k, &rt_i, &rd_i);
-  const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
-  const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
-  const float s = scale_of(d.temp_scalar);
-  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-  const int tile0 = c * NT;
-  const int nt_tiles = min(NT, d.ntiles - tile0);
-  float al = 0.f, sq = 0.f;
+  // persistent: strides over the (position step, chunk) tasks
+  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
+    const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
+    const int n = u / a.K, k = u % a.K;
+    int rt_i, rd_i, bb;
+    bool al_t, al_d;
+    tv_rows<E>(a, n, k, &rt_i, &rd_i);
+    const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
+    const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
+    const float s = scale_of(d.temp_scalar);
+    const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
+    const int tile0 = c * NT;
+    const int nt_tiles = min(NT, d.ntiles - tile0);
+    static_assert(NT * EPV <= 64, "indicator bits of a chunk fit one word per thread");
+    float al = 0.f, sq = 0.f;
+    uint64_t mbits = 0;
 #pragma unroll
-  for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt_tiles) break;
-    float xt[S][EPV], xd[S][EPV];
-    load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
-    load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
+    for (int j0 = 0; j0 < NT; j0 += S) {
+      if (j0 >= nt_tiles) break;
+      float xt[S][EPV], xd[S][EPV];
+      load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
+      load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
 #pragma unroll
-    for (int j = 0; j < S; ++j)
+      for (int j = 0; j < S; ++j) {
+        uint32_t m = 0;
 #pragma unroll
-      for (int kk = 0; kk < EPV; ++kk) {
-        const float p = prob(xt[j][kk], s, nt.M, nt.invD);
-        const float q = prob(xd[j][kk], s, nd.M, nd.invD);
-        al += fminf(p, q);
-        sq += (q <= p) ? q : 0.f;
+        for (int kk = 0; kk < EPV; ++kk) {
+          const float p = prob(xt[j][kk], s, nt.M, nt.invD);
+          const float q = prob(xd[j][kk], s, nd.M, nd.invD);
+          al += fminf(p, q);
+          const bool le = q <= p;
+          sq += le ? q : 0.f;
+          m |= le ? (1u << kk) : 0u;
+        }
+        mbits |= static_cast<uint64_t>(m) << ((j0 + j) * EPV);
       }
-  }
-  double v[4] = {static_cast<double>(al), static_cast<double>(sq), 0.0, 0.0};
-  wg_sum<4>(v, red);
-  if (threadIdx.x == 0) {
-    TvPair o;
-    o.alpha = v[0]; o.S = v[1];
-    a.pairs[blockIdx.x] = o;
+    }
+    // the gradient pass reads these indicator bits instead of the target row
+    if (a.bits)
+      reinterpret_cast<uint64_t*>(a.bits + static_cast<int64_t>(u) * a.bits_stride)[
+          static_cast<int64_t>(c) * kChunkWords + threadIdx.x] = mbits;
+    double v[4] = {static_cast<double>(al), static_cast<double>(sq), 0.0, 0.0};
+    wg_sum<4>(v, red);
+    if (threadIdx.x == 0) {
+      TvPair o;
+      o.alpha = v[0]; o.S = v[1];
+      a.pairs[t] = o;
+    }
   }
 }
 
@@ -154,53 +189,61 @@ __global__ __launch_bounds__(kThreads) void tv_coef_kernel(TvArgs a) {
   }
 }
 
-template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a) {
+template <class E, int NT, int S, int EPVW>
+__global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a, int64_t ntasks) {
+  static_assert(E::EPV == 4, "the gradient pass reads 4 elements per vector");
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   const RowsDesc& d = a.rows;
   const int C = d.C, K = a.K, V = d.V;
-  const int u = blockIdx.x / C, c = blockIdx.x % C;
-  const int n = u / K, k = u % K;
-  int rt_i, rd_i, bb;
-  bool al_t, al_d;
-  tv_rows<E>(a, n, k, &rt_i, &rd_i);
-  const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
-  const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
-  const float s = scale_of(d.temp_scalar);
-  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-  const float2 A = a.coef[u];
-  float* gr = a.grad + static_cast<int64_t>(u) * V;
-  // this kernel may read with a narrower vector than the statistics passes, so
-  // its tile count comes from its own tile width (the chunk is the same)
-  const int tile0 = c * NT;
-  const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
+  // persistent: strides over the (position step, chunk) tasks
+  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
+    const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
+    const int n = u / K, k = u % K;
+    int rt_i, rd_i, bb;
+    bool al_d;
+    tv_rows<E>(a, n, k, &rt_i, &rd_i);
+    const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
+    const float s = scale_of(d.temp_scalar);
+    const RowNorm nd = a.norms[rd_i];
+    const float2 A = a.coef[u];
+    float* gr = a.grad + static_cast<int64_t>(u) * V;
+    const uint8_t* rb = a.bits + static_cast<int64_t>(u) * a.bits_stride;
+    // this kernel may read with a narrower vector than the statistics passes, so
+    // its tile count comes from its own tile width (the chunk is the same)
+    const int tile0 = c * NT;
+    const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
 #pragma unroll
-  for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt_tiles) break;
-    float xt[S][EPV], xd[S][EPV];
-    load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
-    load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
+    for (int j0 = 0; j0 < NT; j0 += S) {
+      if (j0 >= nt_tiles) break;
+      float xd[S][EPV];
+      uint32_t le[S];
 #pragma unroll
-    for (int j = 0; j < S; ++j) {
-      const int v0 = (tile0 + j0 + j) * TILE + threadIdx.x * EPV;
-      float gv[EPV];
-#pragma unroll
-      for (int kk = 0; kk < EPV; ++kk) {
-        const float p = prob(xt[j][kk], s, nt.M, nt.invD);
-        const float q = prob(xd[j][kk], s, nd.M, nd.invD);
-        gv[kk] = q * ((q <= p) ? A.x : A.y);
+      for (int j = 0; j < S; ++j) {
+        const int v0 = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV;
+        le[j] = v0 < V ? load_bits4<EPVW>(rb, c, v0 - c * NT * TILE) : 0u;
       }
-      if (a.vec_g && v0 + EPV <= V) {
+      load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
 #pragma unroll
-        for (int h = 0; h < EPV; h += 4) {
-          f32x4 w4 = {gv[h], gv[h + 1], gv[h + 2], gv[h + 3]};
-          __builtin_nontemporal_store(w4, reinterpret_cast<f32x4*>(gr + v0 + h));
+      for (int j = 0; j < S; ++j) {
+        const int v0 = (tile0 + j0 + j) * TILE + threadIdx.x * EPV;
+        float gv[EPV];
+#pragma unroll
+        for (int kk = 0; kk < EPV; ++kk) {
+          const float q = prob(xd[j][kk], s, nd.M, nd.invD);
+          gv[kk] = q * (((le[j] >> kk) & 1u) ? A.x : A.y);
         }
-      } else {
+        if (a.vec_g && v0 + EPV <= V) {
 #pragma unroll
-        for (int kk = 0; kk < EPV; ++kk)
-          if (v0 + kk < V) gr[v0 + kk] = gv[kk];
+          for (int h = 0; h < EPV; h += 4) {
+            f32x4 w4 = {gv[h], gv[h + 1], gv[h + 2], gv[h + 3]};
+            __builtin_nontemporal_store(w4, reinterpret_cast<f32x4*>(gr + v0 + h));
+          }
+        } else {
+#pragma unroll
+          for (int kk = 0; kk < EPV; ++kk)
+            if (v0 + kk < V) gr[v0 + kk] = gv[kk];
+        }
       }
     }
   }

@@ -48,39 +48,32 @@ __device__ __forceinline__ int draft_row(const VerifyArgs& a, int b, int i) {
   return a.B * (a.K + 1) + b * a.K + i;
 }
 
-// Row normalisers and accept decisions, one workgroup per batch row.
+struct DecideShared {
+  RowNorm nrm[2 * SPEC_MAX_K_DEV + 1];  // target rows 0..K, then draft rows 0..K-1
+  double px[SPEC_MAX_K_DEV], qx[SPEC_MAX_K_DEV];
+  int acc[SPEC_MAX_K_DEV], badx[SPEC_MAX_K_DEV];
+  int n;
+};
+
+// Accept tests and every per-row output except the overlaps and emitted[n],
+// for batch row b whose 2K+1 row normalisers are in sh.nrm (`fail` forces a
+// row error).  Whole workgroup; returns the accept length n, or -1 for a row
+// with a data error (then every output of the row has been written).
 template <class E>
-__global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
+__device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& sh) {
   using raw = typename E::raw;
-  __shared__ RowNorm nrm[2 * SPEC_MAX_K_DEV + 1];
-  __shared__ double px[SPEC_MAX_K_DEV], qx[SPEC_MAX_K_DEV];
-  __shared__ int acc[SPEC_MAX_K_DEV], badx[SPEC_MAX_K_DEV];
   const RowsDesc& d = a.rows;
-  const int K = a.K, C = d.C, V = d.V;
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int K = a.K, V = d.V;
+  const int tid = threadIdx.x;
   const float T = temperature_of(d, b);
   const bool t_ok = temperature_ok(T);
   const float s = t_ok ? scale_of(T) : 1.0f;
-  // row j < K+1: target row j; row K+1+i: draft row i (one wave per row)
-  for (int j = wave; j < 2 * K + 1; j += kWaves) {
-    const int r = j <= K ? target_row(a, b, j) : draft_row(a, b, j - K - 1);
-    float M;
-    double D;
-    combine_row(a.stats + static_cast<int64_t>(r) * C, C, &M, &D);
-    if (lane == 0) {
-      const RowNorm nm = make_norm(M, D);
-      nrm[j] = nm;
-      a.norms[r] = nm;
-    }
-  }
-  __syncthreads();
   // accept tests in float64: u q(x) < p(x), no division; one lane per step
   if (tid < K) {
     const int i = tid;
     const int x = a.ids[static_cast<int64_t>(b) * K + i];
-    const RowNorm& nt = nrm[i];
-    const RowNorm& nd = nrm[K + 1 + i];
+    const RowNorm& nt = sh.nrm[i];
+    const RowNorm& nd = sh.nrm[K + 1 + i];
     int ok = 0, bad = 1;
     double p = 0.0, q = 0.0;
     if (x >= 0 && x < V) {
@@ -97,91 +90,123 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
         ok = (u24(g.w[0]) * q < p) ? 1 : 0;
       }
     }
-    px[i] = p; qx[i] = q; acc[i] = ok; badx[i] = bad;
+    sh.px[i] = p; sh.qx[i] = q; sh.acc[i] = ok; sh.badx[i] = bad;
   }
   __syncthreads();
   if (tid == 0) {
-    bool err = !t_ok;
+    bool err = !t_ok || fail;
     for (int j = 0; j < 2 * K + 1; ++j)
-      if (!norm_ok(nrm[j])) err = true;
+      if (!norm_ok(sh.nrm[j])) err = true;
     int n = K;
     for (int i = 0; i < K; ++i) {
-      if (badx[i]) err = true;
-      if (n == K && !acc[i]) n = i;  // the first rejection ends the chain
+      if (sh.badx[i]) err = true;
+      if (n == K && !sh.acc[i]) n = i;  // the first rejection ends the chain
     }
-    a.decision[b] = err ? -1 : n;
     a.accept_len[b] = err ? -1 : n;
     int32_t* em = a.emitted + static_cast<int64_t>(b) * (K + 1);
     const int32_t* xb = a.ids + static_cast<int64_t>(b) * K;
     for (int j = 0; j <= K; ++j)
-      if (err || j != n) em[j] = (!err && j < n) ? xb[j] : -1;  // emitted[n] is written by finish
+      if (err || j != n) em[j] = (!err && j < n) ? xb[j] : -1;  // emitted[n] is written with the sampled token
     for (int i = 0; i < K; ++i) {
       const int64_t o = static_cast<int64_t>(b) * K + i;
-      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(px[i]);
-      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(qx[i]);
-      if (a.logz_d) a.logz_d[o] = err ? NAN : static_cast<float>((static_cast<double>(nrm[K + 1 + i].M) + log2(nrm[K + 1 + i].D)) * kLn2D);
+      const RowNorm& nd = sh.nrm[K + 1 + i];
+      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(sh.px[i]);
+      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(sh.qx[i]);
+      if (a.logz_d) a.logz_d[o] = err ? NAN : static_cast<float>((static_cast<double>(nd.M) + log2(nd.D)) * kLn2D);
       if (a.overlap && err) a.overlap[o] = NAN;
     }
     if (a.logz_t)
       for (int i = 0; i <= K; ++i)
         a.logz_t[static_cast<int64_t>(b) * (K + 1) + i] =
-            err ? NAN : static_cast<float>((static_cast<double>(nrm[i].M) + log2(nrm[i].D)) * kLn2D);
+            err ? NAN : static_cast<float>((static_cast<double>(sh.nrm[i].M) + log2(sh.nrm[i].D)) * kLn2D);
+    sh.n = err ? -1 : n;
   }
+  __syncthreads();
+  return sh.n;
+}
+
+// Row normalisers and accept decisions, one workgroup per batch row.
+template <class E>
+__global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
+  __shared__ DecideShared sh;
+  const RowsDesc& d = a.rows;
+  const int K = a.K, C = d.C;
+  const int b = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // row j < K+1: target row j; row K+1+i: draft row i (one wave per row)
+  for (int j = wave; j < 2 * K + 1; j += kWaves) {
+    const int r = j <= K ? target_row(a, b, j) : draft_row(a, b, j - K - 1);
+    float M;
+    double D;
+    combine_row(a.stats + static_cast<int64_t>(r) * C, C, &M, &D);
+    if (lane == 0) {
+      const RowNorm nm = make_norm(M, D);
+      sh.nrm[j] = nm;
+      a.norms[r] = nm;
+    }
+  }
+  __syncthreads();
+  const int n = decide_row<E>(a, b, false, sh);
+  if (threadIdx.x == 0) a.decision[b] = n;
 }
 
 // Pass 2 over one chunk of a (target, draft) pair: overlap, and the residual
 // mass when this is the row's first rejected step.
 template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a) {
+__global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   __shared__ RedLds<4> red;
   const RowsDesc& d = a.rows;
   const int C = d.C;
-  const int u = blockIdx.x / C, c = blockIdx.x % C;
-  const int b = u / a.K, i = u % a.K;
-  const int n = a.decision[b];
-  if (n < 0) return;  // data error: finish ignores this row's partials
-  const bool need_z = i == n;
-  if (!need_z && a.overlap == nullptr) return;  // no overlap requested: only the residual step is read again
-  const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
-  int bb;
-  bool al_t, al_d;
-  const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
-  const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
-  const float s = scale_of(temperature_of(d, b));
-  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-  const int tile0 = c * NT;
-  const int nt_tiles = min(NT, d.ntiles - tile0);
-  float al = 0.f, zr = 0.f;
+  // persistent: the grid is sized to what the device holds at once and
+  // strides over the (pair, chunk) tasks
+  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
+    const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
+    const int b = u / a.K, i = u % a.K;
+    const int n = a.decision[b];
+    if (n < 0) continue;  // data error: finish ignores this row's partials
+    const bool need_z = i == n;
+    if (!need_z && a.overlap == nullptr) continue;  // no overlap requested: only the residual step is read again
+    const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
+    int bb;
+    bool al_t, al_d;
+    const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
+    const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
+    const float s = scale_of(temperature_of(d, b));
+    const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
+    const int tile0 = c * NT;
+    const int nt_tiles = min(NT, d.ntiles - tile0);
+    float al = 0.f, zr = 0.f;
 #pragma unroll
-  for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt_tiles) break;
-    float xt[S][EPV], xd[S][EPV];
-    load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
-    load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
-    if (need_z) {
+    for (int j0 = 0; j0 < NT; j0 += S) {
+      if (j0 >= nt_tiles) break;
+      float xt[S][EPV], xd[S][EPV];
+      load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
+      load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
+      if (need_z) {
 #pragma unroll
-      for (int j = 0; j < S; ++j)
+        for (int j = 0; j < S; ++j)
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          const float p = prob(xt[j][k], s, nt.M, nt.invD);
-          const float mn = fminf(p, prob(xd[j][k], s, nd.M, nd.invD));
-          al += mn;
-          zr += p - mn;
-        }
-    } else {
+          for (int k = 0; k < EPV; ++k) {
+            const float p = prob(xt[j][k], s, nt.M, nt.invD);
+            const float mn = fminf(p, prob(xd[j][k], s, nd.M, nd.invD));
+            al += mn;
+            zr += p - mn;
+          }
+      } else {
 #pragma unroll
-      for (int j = 0; j < S; ++j)
+        for (int j = 0; j < S; ++j)
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) al += min_prob(xt[j][k], xd[j][k], s, nt, nd);
+          for (int k = 0; k < EPV; ++k) al += min_prob(xt[j][k], xd[j][k], s, nt, nd);
+      }
     }
-  }
-  double v[4] = {static_cast<double>(al), static_cast<double>(zr), 0.0, 0.0};
-  wg_sum<4>(v, red);
-  if (threadIdx.x == 0) {
-    PairStat o;
-    o.alpha = v[0]; o.Z = v[1];
-    a.pairs[blockIdx.x] = o;
+    double v[4] = {static_cast<double>(al), static_cast<double>(zr), 0.0, 0.0};
+    wg_sum<4>(v, red);
+    if (threadIdx.x == 0) {
+      PairStat o;
+      o.alpha = v[0]; o.Z = v[1];
+      a.pairs[t] = o;
+    }
   }
 }
 
@@ -201,17 +226,141 @@ __device__ __forceinline__ void vector_masses(const typename E::raw* rt, const t
   }
 }
 
+// The chunk holding the sampling target, found by one wave from per-chunk
+// masses mass(cc) >= 0: with the total Z and the uniform u, target = u Z; the
+// chunk is the first whose cumulative mass exceeds the target (strict ">", so
+// a chunk without mass is never chosen).  *tin receives the target's offset
+// inside the chunk; if rounding puts the target past the last cumulative sum,
+// the last chunk with mass is chosen and *tin = +inf (its last element with
+// mass).  Returns -1 when no chunk has mass.
+template <class Mass>
+__device__ __forceinline__ int select_chunk(int C, double u, Mass mass, double* tin) {
+  const int lane = threadIdx.x & 63;
+  double tot = 0.0;
+  for (int cc = lane; cc < C; cc += 64) tot += mass(cc);
+  tot = wave_sum(tot);
+  const double target = u * tot;
+  double carry = 0.0, t_in = 0.0;
+  int cstar = -1, clast = -1;
+  for (int c0 = 0; c0 < C; c0 += 64) {
+    const int cc = c0 + lane;
+    const double zc = (cc < C) ? mass(cc) : 0.0;
+    const double incl = carry + wave_incl_scan(zc);
+    const double excl = incl - zc;
+    const uint64_t hit = __ballot(cc < C && incl > target && excl <= target && zc > 0.0);
+    const uint64_t pos = __ballot(cc < C && zc > 0.0);
+    if (pos) clast = c0 + 63 - __clzll(pos);
+    if (cstar < 0 && hit) {
+      const int l = __ffsll(static_cast<long long>(hit)) - 1;
+      cstar = c0 + l;
+      t_in = target - __shfl(excl, l, 64);
+    }
+    carry = __shfl(incl, 63, 64);
+  }
+  if (cstar < 0) { cstar = clast; t_in = INFINITY; }
+  *tin = t_in;
+  return cstar;
+}
+
+struct SampleShared {
+  int token;
+};
+
+// Inverse CDF inside chunk `cstar` (NT tiles of kThreads vectors, read S
+// tiles at a time), whole workgroup: per-tile masses, the tile holding `tin`,
+// a workgroup scan of the per-thread masses of that tile, then an element
+// scan in the winning thread.  The residual mass max(0, p - q) is p - min(p, q)
+// element by element; the bonus / fallback mass is p.  Every thread returns
+// the token (-1 if the chunk has no mass).
+template <class E, int NT, int S>
+__device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typename E::raw* rd, bool al_d,
+                               bool residual, int cstar, double tin, int V, int ntiles, float s, const RowNorm& nt,
+                               const RowNorm& nd, RedLds<NT>& redv, RedLds<1>& red1, SampleShared& sh) {
+  constexpr int EPV = E::EPV;
+  constexpr int TILE = kThreads * EPV;
+  const int tid = threadIdx.x;
+  const int tile0 = cstar * NT;
+  const int nt_tiles = min(NT, ntiles - tile0);
+  float tsum[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) tsum[j] = 0.f;
+#pragma unroll
+  for (int j0 = 0; j0 < NT; j0 += S) {
+    if (j0 >= nt_tiles) break;
+    float xt[S][EPV], xd[S][EPV];
+    load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
+    if (residual) load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) {
+        const float p = prob(xt[j][k], s, nt.M, nt.invD);
+        tsum[j0 + j] += residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
+      }
+  }
+  double W[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) W[j] = (j < nt_tiles) ? static_cast<double>(tsum[j]) : 0.0;
+  wg_sum<NT>(W, redv);  // tile totals, identical in every thread
+  int jstar = -1, jlast = -1;
+  double cum = 0.0, t_in = 0.0;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    if (j < nt_tiles) {
+      if (W[j] > 0.0) jlast = j;
+      if (jstar < 0 && cum + W[j] > tin) { jstar = j; t_in = tin - cum; }
+      cum += W[j];
+    }
+  }
+  bool clamp = false;
+  if (jstar < 0) { jstar = jlast; clamp = true; }
+  if (jstar < 0) return -1;
+  float w = 0.f;
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+    if (j == jstar) w = tsum[j];
+  double incl;
+  const double excl = wg_scan(static_cast<double>(w), red1, &incl);
+  int tstar = kThreads;
+  if (!clamp) tstar = wg_min_int((incl > t_in && excl <= t_in && w > 0.f) ? tid : kThreads, red1);
+  if (tstar == kThreads) {
+    clamp = true;
+    tstar = -wg_min_int((w > 0.f) ? -tid : 1, red1);
+  }
+  if (tid == 0) sh.token = -1;
+  __syncthreads();
+  if (tid == tstar) {
+    const int v0 = (tile0 + jstar) * TILE + tid * EPV;
+    float r[EPV];
+    vector_masses<E>(rt, rd, residual, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+    const double tl = t_in - excl;
+    float cumf = 0.f;
+    int kstar = -1, klast = -1;
+#pragma unroll
+    for (int k = 0; k < EPV; ++k) {
+      cumf += r[k];
+      if (r[k] > 0.f) klast = k;
+      if (kstar < 0 && !clamp && r[k] > 0.f && static_cast<double>(cumf) > tl) kstar = k;
+    }
+    if (kstar < 0) kstar = klast;
+    if (kstar >= 0) sh.token = v0 + kstar;
+  }
+  __syncthreads();
+  const int token = sh.token;
+  __syncthreads();
+  return token;
+}
+
 struct FinishShared {
   double alpha[SPEC_MAX_K_DEV];
   double tin;
-  int cstar, residual, token;
+  int cstar, residual;
+  SampleShared smp;
 };
 
 // One workgroup per batch row: overlaps and the resampled / bonus token.
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
-  constexpr int EPV = E::EPV;
-  constexpr int TILE = kThreads * EPV;
   using raw = typename E::raw;
   __shared__ FinishShared sh;
   __shared__ RedLds<NT> redv;
@@ -246,37 +395,12 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     const RowNorm nn = a.norms[target_row(a, b, n)];
     const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(n), a.offset, 0ull,
                                        a.seed, 0ull);
-    double tot = 0.0;
-    for (int cc = lane; cc < C; cc += 64) {
+    double tin;
+    const int cstar = select_chunk(C, u24(g.w[1]), [&](int cc) -> double {
+      if (residual) return ps[cc].Z;
       const float mc = st[cc].m;
-      tot += residual ? ps[cc].Z
-                      : (mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - nn.M)) / nn.D);
-    }
-    tot = wave_sum(tot);
-    const double target = u24(g.w[1]) * tot;
-    double carry = 0.0, tin = 0.0;
-    int cstar = -1, clast = -1;
-    for (int c0 = 0; c0 < C; c0 += 64) {
-      const int cc = c0 + lane;
-      double zc = 0.0;
-      if (cc < C) {
-        const float mc = st[cc].m;
-        zc = residual ? ps[cc].Z
-                      : (mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - nn.M)) / nn.D);
-      }
-      const double incl = carry + wave_incl_scan(zc);
-      const double excl = incl - zc;
-      const uint64_t hit = __ballot(cc < C && incl > target && excl <= target && zc > 0.0);
-      const uint64_t pos = __ballot(cc < C && zc > 0.0);
-      if (pos) clast = c0 + 63 - __clzll(pos);
-      if (cstar < 0 && hit) {
-        const int l = __ffsll(static_cast<long long>(hit)) - 1;
-        cstar = c0 + l;
-        tin = target - __shfl(excl, l, 64);
-      }
-      carry = __shfl(incl, 63, 64);
-    }
-    if (cstar < 0) { cstar = clast; tin = INFINITY; }  // past the end by rounding: last element with mass
+      return mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - nn.M)) / nn.D;
+    }, &tin);
     if (lane == 0) {
       sh.cstar = cstar;
       sh.tin = tin;
@@ -285,87 +409,16 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   }
   __syncthreads();
 
-  // inverse CDF inside the chosen chunk (whole workgroup)
   int token = -1;
   if (sh.cstar >= 0) {
-    const int cstar = sh.cstar;
-    const bool residual = sh.residual != 0;
     int bb;
     bool al_t, al_d;
     const raw* rt = row_of<E>(d, target_row(a, b, n), &bb, &al_t);
     const raw* rd = row_of<E>(d, draft_row(a, b, n < K ? n : 0), &bb, &al_d);
     const RowNorm nt = a.norms[target_row(a, b, n)];
     const RowNorm nd = a.norms[draft_row(a, b, n < K ? n : 0)];
-    const int tile0 = cstar * NT;
-    const int nt_tiles = min(NT, d.ntiles - tile0);
-    float tsum[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) tsum[j] = 0.f;
-#pragma unroll
-    for (int j0 = 0; j0 < NT; j0 += S) {
-      if (j0 >= nt_tiles) break;
-      float xt[S][EPV], xd[S][EPV];
-      load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
-      if (residual) load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
-#pragma unroll
-      for (int j = 0; j < S; ++j)
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          const float p = prob(xt[j][k], s, nt.M, nt.invD);
-          tsum[j0 + j] += residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
-        }
-    }
-    double W[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) W[j] = (j < nt_tiles) ? static_cast<double>(tsum[j]) : 0.0;
-    wg_sum<NT>(W, redv);  // tile totals, identical in every thread
-    const double tin = sh.tin;
-    int jstar = -1, jlast = -1;
-    double cum = 0.0, t_in = 0.0;
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      if (j < nt_tiles) {
-        if (W[j] > 0.0) jlast = j;
-        if (jstar < 0 && cum + W[j] > tin) { jstar = j; t_in = tin - cum; }
-        cum += W[j];
-      }
-    }
-    bool clamp = false;
-    if (jstar < 0) { jstar = jlast; clamp = true; }
-    if (jstar >= 0) {
-      float w = 0.f;
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-        if (j == jstar) w = tsum[j];
-      double incl;
-      const double excl = wg_scan(static_cast<double>(w), red1, &incl);
-      int tstar = kThreads;
-      if (!clamp) tstar = wg_min_int((incl > t_in && excl <= t_in && w > 0.f) ? tid : kThreads, red1);
-      if (tstar == kThreads) {
-        clamp = true;
-        tstar = -wg_min_int((w > 0.f) ? -tid : 1, red1);
-      }
-      if (tid == 0) sh.token = -1;
-      __syncthreads();
-      if (tid == tstar) {
-        const int v0 = (tile0 + jstar) * TILE + tid * EPV;
-        float r[EPV];
-        vector_masses<E>(rt, rd, residual, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
-        const double tl = t_in - excl;
-        float cumf = 0.f;
-        int kstar = -1, klast = -1;
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          cumf += r[k];
-          if (r[k] > 0.f) klast = k;
-          if (kstar < 0 && !clamp && r[k] > 0.f && static_cast<double>(cumf) > tl) kstar = k;
-        }
-        if (kstar < 0) kstar = klast;
-        if (kstar >= 0) sh.token = v0 + kstar;
-      }
-      __syncthreads();
-      token = sh.token;
-    }
+    token = sample_in_chunk<E, NT, S>(rt, al_t, rd, al_d, sh.residual != 0, sh.cstar, sh.tin, V, d.ntiles, s, nt, nd,
+                                      redv, red1, sh.smp);
   }
 
   // the overlaps and emitted[n] have this single writer

@@ -58,6 +58,17 @@ def test_ragged_multi_chunk(dtype, B, K, V):
     print(dtype, B, K, V, rep)
 
 
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_large_ragged_vocabulary(dtype):
+    """A vocabulary of about two million entries, not a multiple of any tile:
+    129 chunks per row, ragged last chunk and vector."""
+    V = 256 * 8192 + 8195
+    d = W.verify_inputs_numpy(2, 2, V, dtype, "rollout_t", 31)
+    out, ref = run_numpy_case(d, seed=2, offset=1)
+    rep = compare_verify(out, ref, dtype)
+    print(dtype, V, rep)
+
+
 def test_scalar_temperature():
     d = W.verify_inputs_numpy(5, 3, 5000, W.BF16, "rollout", 21)
     out, ref = run_numpy_case(d, seed=5, scalar_t=0.8)
