@@ -15,6 +15,9 @@ verify   Chain rejection-sampling verification (Sec. 2.2 Eq. reject_sample,
          App. G.1 Alg. rs_multinomial).
 tv       TV loss, its gradient and the end-to-end multi-step TV loss
          (Sec. 4.1 Eqs. tv_loss / tv_grad, Sec. 4.2 Eq. e2e_tv, App. A).
+variants Target-only verification (Sec. 2.2 Eq. target_only), the draft-stage
+         sampler (App. G.1 draft stage) and per-step diagnostics (entropies,
+         alpha^TO, alpha^RS and its split, the App. E decision boundary).
 
 Every function is pinned by the ``-m "not gpu"`` tests against something
 other than itself (numpy's own Philox, scipy routines, closed forms,

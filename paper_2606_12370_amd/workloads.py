@@ -18,7 +18,8 @@ against 4 target positions, K = 1..3.  Recipes (all per batch row b):
       both rounded to the storage dtype (round-to-nearest-even),
       temperature T_b = 1, or T_b ~ U[0.6, 1.2] for the large batch;
   draft ids: x[b, i] ~ softmax(stored draft[b, i, :] / T_b), drawn with the
-      Gumbel-max trick from the stored (rounded) logits;
+      Gumbel-max trick from the stored (rounded) logits; for target-only
+      verification the greedy ids argmax_v draft[b, i, v] instead;
   TV loss: s_n ~ U[1, 8], target ~ N(0, s_n^2), draft = target + N(0, 1).
 
 Two backends: ``numpy`` (host, ``numpy.random.default_rng``) for the small
@@ -122,6 +123,12 @@ def verify_inputs_numpy(B, K, V, dtype, gen, seed, shared_target=False, q_equals
     ids = _gumbel_ids(id_rng, to_float64(drf, dtype), T.astype(np.float64)[:, None, None])
     del tgt64
     return dict(target=tgt, draft=drf, ids=ids, temperature=T, dtype=dtype, B=B, K=K, V=V)
+
+
+def greedy_ids(draft, dtype):
+    """The draft's greedy tokens (first index of each row's largest stored
+    logit), the draft choice target-only verification assumes."""
+    return np.argmax(to_float64(draft, dtype), axis=-1).astype(np.int32)
 
 
 def tv_inputs_numpy(N, K, V, dtype, seed, noise=1.0, q_equals_p=False):
