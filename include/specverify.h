@@ -7,6 +7,8 @@
  * rs_multinomial) define chain rejection-sampling verification of K draft
  * tokens; Sec. 4.1 (Eqs. tv_loss, tv_grad), App. A and Sec. 4.2 (Eq. e2e_tv)
  * define the TV loss, its gradient and the end-to-end multi-step TV loss.
+ * Sec. 2.2 (Eq. target_only) defines target-only verification, App. G.1 the
+ * draft-stage sampler, Sec. 3 and App. E the acceptance diagnostics.
  *
  * Conventions shared by every entry point
  *  - All tensor pointers are DEVICE pointers owned by the caller.  The
@@ -25,9 +27,10 @@
  *    next.  Calls that share a workspace must not run concurrently (enqueue
  *    them on one stream).
  *  - Each call is a short fixed sequence of kernel launches on `stream`
- *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a
- *    gradient); no launch waits on another
- *    workgroup, so any number of resident workgroups is enough.
+ *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a gradient,
+ *    spec_verify_target_only: 2, spec_sample: 2, spec_diagnostics: 4); no
+ *    launch waits on another workgroup, so any number of resident
+ *    workgroups is enough.
  *  - Entry points are thread-safe; each call is independent.
  *  - Logits are bfloat16 (raw 16-bit patterns) or float32.  Arithmetic is
  *    float32 per element with float64 accumulation across vectors, threads
@@ -149,6 +152,121 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
                                  float temperature, spec_tv_mode mode, float scale,
                                  float* loss, float* overlap, float* grad_draft,
                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spec_verify_target_only needs (0 on invalid sizes). */
+size_t spec_verify_target_only_workspace_size(int B, int K, int V, spec_dtype dtype);
+
+/*
+ * spec_verify_target_only — target-only verification of K greedy draft
+ * tokens for B batch rows (Sec. 2.2, Eq. target_only).  The draft logits are
+ * not read: the acceptance rule uses the target's probabilities only.
+ *
+ * For row b, with T = temperature[b] (or temperature_scalar):
+ *   p_i = softmax(target[b, i, :] / T), i = 0..K (row K: bonus position)
+ *   step i accepts x_i = draft_ids[b, i] (the draft's greedy token) iff u_i < p_i(x_i)
+ *   n = first rejected step (K if none); accept_len[b] = n
+ *   emitted[b, 0..n-1] = x_0..x_{n-1}; emitted[b, n+1..K] = -1
+ *   emitted[b, n] = smallest v with C(v) > u' * Z, C the cumulative sum of
+ *       r(v) = p_n(v) * 1[v != x_n] if n < K, else r = p_K; Z = sum r (if Z
+ *       is 0 the sample is drawn from p_n).  The emitted token at position n
+ *       is thereby distributed exactly as p_n.
+ * Uniforms: the same Philox4x64-10 blocks as spec_verify (counter (b, i,
+ *   offset, 0), key (seed, 0); word 0 accept test, word 1 resample).
+ *
+ * target_logits  [B, K+1, V] element strides (t_stride_b, t_stride_k), dtype
+ * draft_ids      [B, K] int32, contiguous
+ * temperature    [B] float32 device array, or NULL: temperature_scalar (finite, > 0)
+ * accept_len     [B] int32 out; emitted_ids [B, K+1] int32 out, contiguous
+ * p_at_draft     [B, K] float32 out: p_i(x_i) (may be NULL)
+ * logz_target    [B, K+1] float32 out: natural-log partition function of z/T (may be NULL)
+ * workspace      device memory of at least spec_verify_target_only_workspace_size bytes
+ * Row data errors behave as in spec_verify (accept_len = -1, emitted = -1, NaN).
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= B.
+ */
+spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                                    spec_dtype dtype, int B, int K, int V,
+                                    const int32_t* draft_ids,
+                                    const float* temperature, float temperature_scalar,
+                                    uint64_t seed, uint64_t offset,
+                                    int32_t* accept_len, int32_t* emitted_ids,
+                                    float* p_at_draft, float* logz_target,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spec_sample needs (0 on invalid sizes). */
+size_t spec_sample_workspace_size(int R, int V, spec_dtype dtype);
+
+/*
+ * spec_sample — draft-stage token choice for R rows of logits (App. G.1, the
+ * draft stage: temperature softmax and a multinomial draw).
+ *
+ * Row r with T = temperature[r] (or temperature_scalar):
+ *   T > 0:  tokens[r] = smallest v with C(v) > u, C the cumulative sum of
+ *           softmax(logits[r, :] / T), u = (word0 >> 40) * 2^-24 of
+ *           Philox4x64-10(counter = (r, 0, offset, 1), key = (seed, 0))
+ *           (counter word 3 = 1 keeps this stream apart from verification's);
+ *           logz[r] = natural-log partition function of z/T
+ *   T == 0: tokens[r] = the greedy token, the first index of the largest
+ *           logit (the draft choice of spec_verify_target_only); logz[r] = NaN
+ *
+ * logits       [R, V], element stride stride_r between rows, dtype
+ * temperature  [R] float32 device array, or NULL: temperature_scalar (finite, >= 0)
+ * tokens       [R] int32 out
+ * logz         [R] float32 out (may be NULL)
+ * workspace    device memory of at least spec_sample_workspace_size bytes
+ * Row data errors (NaN or +inf logits, all -inf, a per-row temperature that
+ * is negative or not finite) give tokens[r] = -1 and logz[r] = NaN.
+ * Limits: 1 <= R, 1 <= V < 2^31.
+ */
+spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, int R, int V,
+                        const float* temperature, float temperature_scalar,
+                        uint64_t seed, uint64_t offset,
+                        int32_t* tokens, float* logz,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Columns of the per-step output of spec_diagnostics. */
+typedef enum {
+  SPEC_DIAG_ENTROPY_TARGET = 0, /* H(p_i) in nats (Sec. 3.1)                               */
+  SPEC_DIAG_ENTROPY_DRAFT = 1,  /* H(q_i) in nats                                           */
+  SPEC_DIAG_MAX_P = 2,          /* max_v p_i(v) (Prop. to_entropy: >= exp(-H(p_i)))         */
+  SPEC_DIAG_ALPHA_TO = 3,       /* p_i(argmax q_i), Eq. target_only                         */
+  SPEC_DIAG_ALPHA_RS = 4,       /* sum_v min(p_i, q_i) = 1 - d_TV(p_i, q_i), Eq. reject_sample */
+  SPEC_DIAG_ALPHA_P_GT_Q = 5,   /* sum over p > q of q                                      */
+  SPEC_DIAG_ALPHA_Q_GE_P = 6,   /* sum over q >= p of p (columns 5 + 6 = column 4)          */
+  SPEC_DIAG_NCOLS = 7
+} spec_diag_column;
+
+/* Bytes of workspace spec_diagnostics needs (0 on invalid sizes). */
+size_t spec_diagnostics_workspace_size(int B, int K, int V, spec_dtype dtype);
+
+/*
+ * spec_diagnostics — per-step acceptance diagnostics (Sec. 3: target entropy
+ * against acceptance; App. E: rejection sampling is preferred over
+ * target-only verification iff d_TV(p, q) < 1 - p(argmax q)).
+ *
+ * For row b and step i < K, with T as in spec_verify, p_i = softmax(target[b, i] / T)
+ * and q_i = softmax(draft[b, i] / T):
+ *   diag[b, i, c] for the columns c of spec_diag_column;
+ *   greedy_draft[b, i] = argmax_v q_i(v), first index among ties (may be NULL);
+ *   rs_preferred[b, i] = 1 if alpha^RS > alpha^TO else 0 (may be NULL).
+ * The split alpha_{p>q} / alpha_{q>=p} decides p > q per token in float32:
+ * tokens whose p and q agree to about 1e-6 relative may land on either side.
+ *
+ * target_logits  [B, >= K, V] element strides (t_stride_b, t_stride_k); rows
+ *                i < K are read, so a [B, K+1, V] verification tensor can be passed
+ * draft_logits   [B, K, V] element strides (d_stride_b, d_stride_k)
+ * temperature    [B] float32 device array, or NULL: temperature_scalar (finite, > 0)
+ * diag           [B, K, SPEC_DIAG_NCOLS] float32 out, contiguous
+ * workspace      device memory of at least spec_diagnostics_workspace_size bytes
+ * Row data errors (as in spec_verify, without draft ids) give NaN in every
+ * column, greedy_draft = -1 and rs_preferred = -1.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= B.
+ */
+spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                             const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                             spec_dtype dtype, int B, int K, int V,
+                             const float* temperature, float temperature_scalar,
+                             float* diag, int32_t* greedy_draft, int32_t* rs_preferred,
+                             void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* spec_status_string(spec_status s);

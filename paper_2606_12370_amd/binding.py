@@ -39,6 +39,10 @@ _SZ = _c.c_size_t
 VERIFY_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _P, _P, _F, _U64, _U64,
                    _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
 TV_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _SZ, _P]
+TO_ARGTYPES = [_P, _I64, _I64, _I, _I, _I, _I, _P, _P, _F, _U64, _U64, _P, _P, _P, _P, _P, _SZ, _P]
+SAMPLE_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _P, _SZ, _P]
+DIAG_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _P, _F, _P, _P, _P, _P, _SZ, _P]
+DIAG_COLUMNS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")
 
 
 class SpecError(RuntimeError):
@@ -72,6 +76,18 @@ def load_library():
         lib.spec_verify.argtypes = VERIFY_ARGTYPES
         lib.spec_tv_loss_fwd_bwd.restype = _I
         lib.spec_tv_loss_fwd_bwd.argtypes = TV_ARGTYPES
+        lib.spec_verify_target_only_workspace_size.restype = _SZ
+        lib.spec_verify_target_only_workspace_size.argtypes = [_I, _I, _I, _I]
+        lib.spec_verify_target_only.restype = _I
+        lib.spec_verify_target_only.argtypes = TO_ARGTYPES
+        lib.spec_sample_workspace_size.restype = _SZ
+        lib.spec_sample_workspace_size.argtypes = [_I, _I, _I]
+        lib.spec_sample.restype = _I
+        lib.spec_sample.argtypes = SAMPLE_ARGTYPES
+        lib.spec_diagnostics_workspace_size.restype = _SZ
+        lib.spec_diagnostics_workspace_size.argtypes = [_I, _I, _I, _I]
+        lib.spec_diagnostics.restype = _I
+        lib.spec_diagnostics.argtypes = DIAG_ARGTYPES
         _lib = lib
         return lib
 
@@ -102,6 +118,21 @@ def tv_workspace_size(N, K, V, dtype=torch.bfloat16):
     return int(load_library().spec_tv_workspace_size(N, K, V, code))
 
 
+def target_only_workspace_size(B, K, V, dtype=torch.bfloat16):
+    code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
+    return int(load_library().spec_verify_target_only_workspace_size(B, K, V, code))
+
+
+def sample_workspace_size(R, V, dtype=torch.bfloat16):
+    code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
+    return int(load_library().spec_sample_workspace_size(R, V, code))
+
+
+def diagnostics_workspace_size(B, K, V, dtype=torch.bfloat16):
+    code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
+    return int(load_library().spec_diagnostics_workspace_size(B, K, V, code))
+
+
 def _dev_key(device):
     device = torch.device(device)
     index = device.index if device.index is not None else torch.cuda.current_device()
@@ -125,6 +156,19 @@ def _check_rows(t, name, shape):
         raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
     if t.stride(2) != 1:
         raise ValueError("%s: the vocabulary dimension must be contiguous" % name)
+
+
+def _temperature_arg(temperature, n):
+    if torch.is_tensor(temperature):
+        if temperature.dtype != torch.float32 or not temperature.is_contiguous() or temperature.numel() != n:
+            raise ValueError("temperature tensor must be contiguous float32 [%d]" % n)
+        return _ptr(temperature), 1.0
+    return None, float(temperature)
+
+
+def _check_ids(ids, B, K):
+    if ids.dtype != torch.int32 or not ids.is_contiguous() or tuple(ids.shape) != (B, K):
+        raise ValueError("draft_ids must be a contiguous int32 [B, K] tensor")
 
 
 def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offset=0,
@@ -224,3 +268,114 @@ def tv_loss_fwd_bwd(target_logits, draft_logits, temperature=1.0, mode="e2e", sc
     if st != 0:
         raise SpecError("spec_tv_loss_fwd_bwd", st)
     return loss, overlap, grad
+
+
+def verify_target_only(target_logits, draft_ids, temperature=1.0, seed=0, offset=0, want_debug=False,
+                       ws=None, out=None):
+    """Target-only verification of greedy draft tokens (spec_verify_target_only).
+
+    target_logits [B, K+1, V] (bf16 or f32, vocabulary dimension contiguous),
+    draft_ids [B, K] int32 (the draft's greedy tokens), temperature: float or
+    [B] float32 tensor.  Returns a dict with accept_len [B], emitted [B, K+1]
+    and, with want_debug, p_at_draft [B, K] and logz_target [B, K+1].
+    """
+    lib = load_library()
+    B, K1, V = target_logits.shape
+    K = K1 - 1
+    _check_rows(target_logits, "target_logits", (B, K + 1, V))
+    _check_ids(draft_ids, B, K)
+    dev = target_logits.device
+    t_ptr, t_scalar = _temperature_arg(temperature, B)
+    code = _dtype_code(target_logits)
+    if out is None:
+        out = {
+            "accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+            "emitted": torch.empty((B, K + 1), dtype=torch.int32, device=dev),
+        }
+        if want_debug:
+            out["p_at_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
+            out["logz_target"] = torch.empty((B, K + 1), dtype=torch.float32, device=dev)
+    need = int(lib.spec_verify_target_only_workspace_size(B, K, V, code))
+    if need == 0:
+        raise ValueError("unsupported target-only shape B=%d K=%d V=%d" % (B, K, V))
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib.spec_verify_target_only(
+        _ptr(target_logits), target_logits.stride(0), target_logits.stride(1), code, B, K, V,
+        _ptr(draft_ids), t_ptr, t_scalar, int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
+        _ptr(out["accept_len"]), _ptr(out["emitted"]), _ptr(out.get("p_at_draft")),
+        _ptr(out.get("logz_target")), _ptr(ws), ws.numel(), _stream(dev))
+    if st != 0:
+        raise SpecError("spec_verify_target_only", st)
+    return out
+
+
+def sample(logits, temperature=1.0, seed=0, offset=0, want_logz=False, ws=None, out=None):
+    """Draft-stage sampling (spec_sample) of one token per row.
+
+    logits [R, V] (bf16 or f32, vocabulary dimension contiguous, any row
+    stride); temperature: float or [R] float32 tensor, 0 meaning greedy.
+    Returns a dict with tokens [R] int32 and, with want_logz, logz [R].
+    """
+    lib = load_library()
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be [R, V] with a contiguous vocabulary dimension")
+    R, V = logits.shape
+    dev = logits.device
+    t_ptr, t_scalar = _temperature_arg(temperature, R)
+    code = _dtype_code(logits)
+    if out is None:
+        out = {"tokens": torch.empty(R, dtype=torch.int32, device=dev)}
+        if want_logz:
+            out["logz"] = torch.empty(R, dtype=torch.float32, device=dev)
+    need = int(lib.spec_sample_workspace_size(R, V, code))
+    if need == 0:
+        raise ValueError("unsupported sample shape R=%d V=%d" % (R, V))
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib.spec_sample(
+        _ptr(logits), logits.stride(0), code, R, V, t_ptr, t_scalar,
+        int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
+        _ptr(out["tokens"]), _ptr(out.get("logz")), _ptr(ws), ws.numel(), _stream(dev))
+    if st != 0:
+        raise SpecError("spec_sample", st)
+    return out
+
+
+def diagnostics(target_logits, draft_logits, temperature=1.0, ws=None):
+    """Per-step acceptance diagnostics (spec_diagnostics).
+
+    target_logits [B, >= K, V] (the first K rows of each batch row are used),
+    draft_logits [B, K, V].  Returns a dict with one [B, K] float32 tensor per
+    name in DIAG_COLUMNS (views of one [B, K, 7] tensor, also returned as
+    "table"), greedy_draft [B, K] int32 and rs_preferred [B, K] int32.
+    """
+    lib = load_library()
+    B, K, V = draft_logits.shape
+    if target_logits.dim() != 3 or target_logits.shape[0] != B or target_logits.shape[1] < K \
+            or target_logits.shape[2] != V or target_logits.stride(2) != 1:
+        raise ValueError("target_logits must be [B, >=K, V] with a contiguous vocabulary dimension")
+    _check_rows(draft_logits, "draft_logits", (B, K, V))
+    if draft_logits.dtype != target_logits.dtype:
+        raise TypeError("target and draft logits must share a dtype")
+    dev = target_logits.device
+    t_ptr, t_scalar = _temperature_arg(temperature, B)
+    code = _dtype_code(target_logits)
+    table = torch.empty((B, K, len(DIAG_COLUMNS)), dtype=torch.float32, device=dev)
+    greedy = torch.empty((B, K), dtype=torch.int32, device=dev)
+    prefer = torch.empty((B, K), dtype=torch.int32, device=dev)
+    need = int(lib.spec_diagnostics_workspace_size(B, K, V, code))
+    if need == 0:
+        raise ValueError("unsupported diagnostics shape B=%d K=%d V=%d" % (B, K, V))
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib.spec_diagnostics(
+        _ptr(target_logits), target_logits.stride(0), target_logits.stride(1),
+        _ptr(draft_logits), draft_logits.stride(0), draft_logits.stride(1),
+        code, B, K, V, t_ptr, t_scalar, _ptr(table), _ptr(greedy), _ptr(prefer),
+        _ptr(ws), ws.numel(), _stream(dev))
+    if st != 0:
+        raise SpecError("spec_diagnostics", st)
+    out = {name: table[..., c] for c, name in enumerate(DIAG_COLUMNS)}
+    out.update(table=table, greedy_draft=greedy, rs_preferred=prefer)
+    return out

@@ -13,6 +13,7 @@
 #include "specverify.h"
 #include "sv_device.h"
 #include "tv_kernel.h"
+#include "variants_kernel.h"
 #include "verify_kernel.h"
 
 namespace {
@@ -29,6 +30,7 @@ constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
 static_assert(kNtF32 * sv::kThreads * sv::F32::EPV == kChunkElems, "chunk geometry");
 static_assert(kChunkElems % (sv::kThreads * sv::BF16H::EPV) == 0, "chunk geometry");
+static_assert(sv::kDiagCols == SPEC_DIAG_NCOLS, "diagnostics columns");
 
 template <class E> struct GradElem { using type = E; };
 template <> struct GradElem<sv::BF16> { using type = sv::BF16H; };
@@ -63,6 +65,10 @@ bool tv_sizes_ok(int N, int K, int V, spec_dtype dt) {
   return rows * geometry(V, dt).C < (int64_t{1} << 31);
 }
 
+bool rows_ok(int64_t rows, int V, spec_dtype dt) {
+  return rows >= 1 && V >= 1 && rows * geometry(V, dt).C < (int64_t{1} << 31);
+}
+
 struct VerifyLayout {
   size_t stats = 0, norms = 0, decision = 0, pairs = 0, total = 0;
 };
@@ -95,6 +101,37 @@ TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
   // indicator bits 1[q <= p] for the gradient pass: one 64-bit word per thread and chunk
   L.bits_stride = C * sv::kChunkWords * sizeof(uint64_t);
   L.bits = off; off = align_up(off + static_cast<size_t>(N) * K * L.bits_stride, 256);
+  L.total = off;
+  return L;
+}
+
+struct ToLayout {
+  size_t stats = 0, total = 0;
+};
+ToLayout to_layout(int B, int K, int V, spec_dtype dt) {
+  ToLayout L;
+  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  L.stats = 0;
+  L.total = align_up(static_cast<size_t>(B) * (K + 1) * C * sizeof(sv::RowStat), 256);
+  return L;
+}
+
+size_t sample_ws(int R, int V, spec_dtype dt) {
+  return align_up(static_cast<size_t>(R) * geometry(V, dt).C * sizeof(sv::RowStat), 256);
+}
+
+struct DiagLayout {
+  size_t stats = 0, norms = 0, info = 0, pairs = 0, total = 0;
+};
+DiagLayout diag_layout(int B, int K, int V, spec_dtype dt) {
+  DiagLayout L;
+  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t rows = static_cast<size_t>(B) * 2 * K;
+  size_t off = 0;
+  L.stats = off; off = align_up(off + rows * C * sizeof(sv::DiagStat), 256);
+  L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
+  L.info = off; off = align_up(off + rows * sizeof(sv::DiagRow), 256);
+  L.pairs = off; off = align_up(off + static_cast<size_t>(B) * K * C * sizeof(sv::DiagPair), 256);
   L.total = off;
   return L;
 }
@@ -176,6 +213,45 @@ spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(tg, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a, units * C);
   }
   hipLaunchKernelGGL(sv::tv_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
+spec_status launch_to(const sv::ToArgs& a, hipStream_t s) {
+  const int64_t tasks = int64_t{a.B} * (a.K + 1) * a.rows.C;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), tasks);
+  hipLaunchKernelGGL((sv::to_verify_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
+                     s, a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
+spec_status launch_sample(const sv::SampleArgs& a, hipStream_t s) {
+  const int64_t tasks = int64_t{a.R} * a.rows.C;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), tasks);
+  hipLaunchKernelGGL((sv::sample_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.R)), dim3(sv::kThreads), 0, s,
+                     a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
+spec_status launch_diag(const sv::DiagArgs& a, hipStream_t s) {
+  const int C = a.rows.C;
+  const int64_t units = int64_t{a.B} * a.K;
+  void (*ds)(sv::RowsDesc, sv::DiagStat*, int64_t) = sv::diag_stats_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(ds, dim3(static_cast<unsigned>(2 * units * C)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::DiagStat*>(a.stats), 2 * units * C);
+  hipLaunchKernelGGL(sv::diag_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C, a.norms, a.info);
+  void (*dp)(sv::DiagArgs, int64_t) = sv::diag_pair_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(dp, dim3(grid_for(reinterpret_cast<const void*>(dp), units * C)), dim3(sv::kThreads), 0, s, a,
+                     units * C);
+  hipLaunchKernelGGL((sv::diag_finish_kernel<E>), dim3(static_cast<unsigned>((units + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
@@ -297,6 +373,120 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   a.bits_stride = static_cast<int64_t>(L.bits_stride);
   hipStream_t s = static_cast<hipStream_t>(stream);
   return dtype == SPEC_BF16 ? launch_tv<BF16, kNtBf16>(a, s) : launch_tv<F32, kNtF32>(a, s);
+}
+
+size_t spec_verify_target_only_workspace_size(int B, int K, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (B < 1 || K < 1 || K > SPEC_MAX_K || !rows_ok(int64_t{B} * (K + 1), V, dtype)) return 0;
+  return to_layout(B, K, V, dtype).total;
+}
+
+spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                                    spec_dtype dtype, int B, int K, int V, const int32_t* draft_ids,
+                                    const float* temperature, float temperature_scalar, uint64_t seed,
+                                    uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* p_at_draft,
+                                    float* logz_target, void* workspace, size_t workspace_bytes, void* stream) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
+  if (B < 1 || K < 1 || !rows_ok(int64_t{B} * (K + 1), V, dtype)) return SPEC_EINVAL;
+  if (!target_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
+  if (t_stride_b < 0 || t_stride_k < 0) return SPEC_EINVAL;
+  if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
+  const ToLayout L = to_layout(B, K, V, dtype);
+  if (!workspace || workspace_bytes < L.total) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  sv::ToArgs a{};
+  a.rows.tgt = target_logits; a.rows.tsb = t_stride_b; a.rows.tsk = t_stride_k; a.rows.tper = K + 1;
+  a.rows.drf = nullptr; a.rows.dsb = 0; a.rows.dsk = 0; a.rows.dper = 1;
+  a.rows.nb = B;
+  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, esize_of(dtype)) ? 1 : 0;
+  a.rows.vec_d = 0;
+  a.B = B; a.K = K;
+  a.ids = draft_ids;
+  a.seed = seed; a.offset = offset;
+  a.accept_len = accept_len; a.emitted = emitted_ids; a.p_at = p_at_draft; a.logz_t = logz_target;
+  a.stats = reinterpret_cast<const sv::RowStat*>(static_cast<char*>(workspace) + L.stats);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_to<BF16, kNtBf16>(a, s) : launch_to<F32, kNtF32>(a, s);
+}
+
+size_t spec_sample_workspace_size(int R, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (!rows_ok(R, V, dtype)) return 0;
+  return sample_ws(R, V, dtype);
+}
+
+spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, int R, int V,
+                        const float* temperature, float temperature_scalar, uint64_t seed, uint64_t offset,
+                        int32_t* tokens, float* logz, void* workspace, size_t workspace_bytes, void* stream) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (!rows_ok(R, V, dtype)) return SPEC_EINVAL;
+  if (!logits || !tokens || stride_r < 0) return SPEC_EINVAL;
+  if (!temperature && !(temperature_scalar >= 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
+  if (!workspace || workspace_bytes < sample_ws(R, V, dtype)) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  sv::SampleArgs a{};
+  a.rows.tgt = logits; a.rows.tsb = stride_r; a.rows.tsk = 0; a.rows.tper = 1;
+  a.rows.drf = nullptr; a.rows.dsb = 0; a.rows.dsk = 0; a.rows.dper = 1;
+  a.rows.nb = R;
+  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(logits, stride_r, 0, esize_of(dtype)) ? 1 : 0;
+  a.rows.vec_d = 0;
+  a.R = R;
+  a.seed = seed; a.offset = offset;
+  a.token = tokens; a.logz = logz;
+  a.stats = reinterpret_cast<const sv::RowStat*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_sample<BF16, kNtBf16>(a, s) : launch_sample<F32, kNtF32>(a, s);
+}
+
+size_t spec_diagnostics_workspace_size(int B, int K, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (B < 1 || K < 1 || K > SPEC_MAX_K || !rows_ok(int64_t{B} * 2 * K, V, dtype)) return 0;
+  return diag_layout(B, K, V, dtype).total;
+}
+
+spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                             const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k, spec_dtype dtype,
+                             int B, int K, int V, const float* temperature, float temperature_scalar, float* diag,
+                             int32_t* greedy_draft, int32_t* rs_preferred, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
+  if (B < 1 || K < 1 || !rows_ok(int64_t{B} * 2 * K, V, dtype)) return SPEC_EINVAL;
+  if (!target_logits || !draft_logits || !diag) return SPEC_EINVAL;
+  if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
+  const DiagLayout L = diag_layout(B, K, V, dtype);
+  if (!workspace || workspace_bytes < L.total) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  const size_t es = esize_of(dtype);
+  sv::DiagArgs a{};
+  a.rows.tgt = target_logits; a.rows.tsb = t_stride_b; a.rows.tsk = t_stride_k; a.rows.tper = K;
+  a.rows.drf = draft_logits; a.rows.dsb = d_stride_b; a.rows.dsk = d_stride_k; a.rows.dper = K;
+  a.rows.nb = B;
+  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, es) ? 1 : 0;
+  a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_b, d_stride_k, es) ? 1 : 0;
+  a.B = B; a.K = K;
+  a.out = diag; a.greedy = greedy_draft; a.prefer = rs_preferred;
+  char* ws = static_cast<char*>(workspace);
+  a.stats = reinterpret_cast<const sv::DiagStat*>(ws + L.stats);
+  a.norms = reinterpret_cast<sv::RowNorm*>(ws + L.norms);
+  a.info = reinterpret_cast<sv::DiagRow*>(ws + L.info);
+  a.pairs = reinterpret_cast<sv::DiagPair*>(ws + L.pairs);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_diag<BF16, kNtBf16>(a, s) : launch_diag<F32, kNtF32>(a, s);
 }
 
 }  // extern "C"

@@ -210,14 +210,15 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
   }
 }
 
-// Residual (or target) mass of the EPV elements of one thread's vector.
+// Residual (or target) mass of the EPV elements of one thread's vector;
+// element `excl` (-1: none) has mass 0.
 template <class E>
 __device__ __forceinline__ void vector_masses(const typename E::raw* rt, const typename E::raw* rd, bool residual,
-                                              int v0, int V, float s, float Mt, float it, float Md, float id,
-                                              float (&r)[E::EPV]) {
+                                              int excl, int v0, int V, float s, float Mt, float it, float Md,
+                                              float id, float (&r)[E::EPV]) {
 #pragma unroll
   for (int k = 0; k < E::EPV; ++k) {
-    if (v0 + k < V) {
+    if (v0 + k < V && v0 + k != excl) {
       const float p = prob(E::one(rt + v0 + k), s, Mt, it);
       r[k] = residual ? p - fminf(p, prob(E::one(rd + v0 + k), s, Md, id)) : p;
     } else {
@@ -266,22 +267,23 @@ struct SampleShared {
   int token;
 };
 
-// Inverse CDF inside chunk `cstar` (NT tiles of kThreads vectors, read S
-// tiles at a time), whole workgroup: per-tile masses, the tile holding `tin`,
-// a workgroup scan of the per-thread masses of that tile, then an element
-// scan in the winning thread.  The residual mass max(0, p - q) is p - min(p, q)
-// element by element; the bonus / fallback mass is p.  Every thread returns
-// the token (-1 if the chunk has no mass).
+// Per-tile masses of chunk `c` (NT tiles of kThreads vectors, read S tiles at
+// a time), per thread: tsum[j] = this thread's mass in tile j.  The mass of an
+// element is the residual max(0, p - q) = p - min(p, q) (`residual`), else p;
+// element `excl` (-1: none) has mass 0.  Returns the number of tiles in the
+// chunk.
 template <class E, int NT, int S>
-__device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typename E::raw* rd, bool al_d,
-                               bool residual, int cstar, double tin, int V, int ntiles, float s, const RowNorm& nt,
-                               const RowNorm& nd, RedLds<NT>& redv, RedLds<1>& red1, SampleShared& sh) {
+__device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
+                                           bool al_d, bool residual, int excl, int c, int V, int ntiles, float s,
+                                           const RowNorm& nt, const RowNorm& nd, float (&tsum)[NT]) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
-  const int tid = threadIdx.x;
-  const int tile0 = cstar * NT;
+  const int tile0 = c * NT;
   const int nt_tiles = min(NT, ntiles - tile0);
-  float tsum[NT];
+  // the excluded element, as (tile, lane of this thread's vector), or none
+  const int ex_rel = excl - tile0 * TILE;
+  const int ex_tile = (excl >= 0 && ex_rel >= 0 && ex_rel < NT * TILE) ? ex_rel / TILE : -1;
+  const int ex_k = (ex_tile >= 0 && (ex_rel % TILE) / EPV == static_cast<int>(threadIdx.x)) ? ex_rel % EPV : -1;
 #pragma unroll
   for (int j = 0; j < NT; ++j) tsum[j] = 0.f;
 #pragma unroll
@@ -295,9 +297,29 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
 #pragma unroll
       for (int k = 0; k < EPV; ++k) {
         const float p = prob(xt[j][k], s, nt.M, nt.invD);
-        tsum[j0 + j] += residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
+        float m = residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
+        if (j0 + j == ex_tile && k == ex_k) m = 0.f;
+        tsum[j0 + j] += m;
       }
   }
+  return nt_tiles;
+}
+
+// Inverse CDF inside chunk `cstar`, whole workgroup: per-tile masses
+// (tile_masses), the tile holding `tin`, a workgroup scan of the per-thread
+// masses of that tile, then an element scan in the winning thread.  Every
+// thread returns the token (-1 if the chunk has no mass).
+template <class E, int NT, int S>
+__device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typename E::raw* rd, bool al_d,
+                               bool residual, int excl, int cstar, double tin, int V, int ntiles, float s,
+                               const RowNorm& nt, const RowNorm& nd, RedLds<NT>& redv, RedLds<1>& red1,
+                               SampleShared& sh) {
+  constexpr int EPV = E::EPV;
+  constexpr int TILE = kThreads * EPV;
+  const int tid = threadIdx.x;
+  const int tile0 = cstar * NT;
+  float tsum[NT];
+  const int nt_tiles = tile_masses<E, NT, S>(rt, al_t, rd, al_d, residual, excl, cstar, V, ntiles, s, nt, nd, tsum);
   double W[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) W[j] = (j < nt_tiles) ? static_cast<double>(tsum[j]) : 0.0;
@@ -320,9 +342,9 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
   for (int j = 0; j < NT; ++j)
     if (j == jstar) w = tsum[j];
   double incl;
-  const double excl = wg_scan(static_cast<double>(w), red1, &incl);
+  const double excl_sum = wg_scan(static_cast<double>(w), red1, &incl);
   int tstar = kThreads;
-  if (!clamp) tstar = wg_min_int((incl > t_in && excl <= t_in && w > 0.f) ? tid : kThreads, red1);
+  if (!clamp) tstar = wg_min_int((incl > t_in && excl_sum <= t_in && w > 0.f) ? tid : kThreads, red1);
   if (tstar == kThreads) {
     clamp = true;
     tstar = -wg_min_int((w > 0.f) ? -tid : 1, red1);
@@ -332,8 +354,8 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
   if (tid == tstar) {
     const int v0 = (tile0 + jstar) * TILE + tid * EPV;
     float r[EPV];
-    vector_masses<E>(rt, rd, residual, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
-    const double tl = t_in - excl;
+    vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+    const double tl = t_in - excl_sum;
     float cumf = 0.f;
     int kstar = -1, klast = -1;
 #pragma unroll
@@ -417,8 +439,8 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     const raw* rd = row_of<E>(d, draft_row(a, b, n < K ? n : 0), &bb, &al_d);
     const RowNorm nt = a.norms[target_row(a, b, n)];
     const RowNorm nd = a.norms[draft_row(a, b, n < K ? n : 0)];
-    token = sample_in_chunk<E, NT, S>(rt, al_t, rd, al_d, sh.residual != 0, sh.cstar, sh.tin, V, d.ntiles, s, nt, nd,
-                                      redv, red1, sh.smp);
+    token = sample_in_chunk<E, NT, S>(rt, al_t, rd, al_d, sh.residual != 0, -1, sh.cstar, sh.tin, V, d.ntiles, s, nt,
+                                      nd, redv, red1, sh.smp);
   }
 
   // the overlaps and emitted[n] have this single writer

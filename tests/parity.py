@@ -42,6 +42,15 @@ def rel_err(a, b):
     return np.abs(a - b) / np.maximum(np.abs(b), 1e-300)
 
 
+def logz_err(a, b):
+    """Error of a log-partition function M + log D: absolute below 1 in
+    magnitude (where it sits near 0 the relative error means nothing),
+    relative above."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return np.abs(a - b) / np.maximum(np.abs(b), 1.0)
+
+
 def compare_verify(gpu, ref, dtype, rows=None, report=None):
     """Compare gpu outputs (dict of tensors, all B rows) with oracle outputs
     for `rows` (default all).  Returns a dict of counts; raises on failure."""
@@ -127,3 +136,121 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
         out["max_normwise_grad"] = worst
         out["tie_elements"] = int(tie.sum())
     return out
+
+
+def compare_target_only(gpu, ref, dtype, rows=None):
+    """Target-only verification: accept lengths and tokens bit for bit except
+    boundary draws (|u - p(x)| <= BOUNDARY for an accept test, or a resample
+    uniform within BOUNDARY of a CDF step); p(x) and log Z within the dtype's
+    tolerance.  Returns a dict of counts; raises on failure."""
+    acc_g = gpu["accept_len"].cpu().numpy()
+    em_g = gpu["emitted"].cpu().numpy()
+    if rows is not None:
+        acc_g, em_g = acc_g[rows], em_g[rows]
+    acc_r, em_r = ref["accept_len"], ref["emitted"]
+    K = em_r.shape[1] - 1
+    bad_rows, boundary_rows = [], []
+    for r in np.nonzero((acc_g != acc_r) | np.any(em_g != em_r, axis=1))[0]:
+        ng, nr = int(acc_g[r]), int(acc_r[r])
+        if ng < 0 or nr < 0 or ng > K or nr > K:
+            bad_rows.append(r)
+            continue
+        if ng != nr:
+            i = min(ng, nr)
+            if abs(ref["u_accept"][r, i] - ref["p_at_draft"][r, i]) <= BOUNDARY:
+                boundary_rows.append(r)
+                continue
+        elif np.array_equal(em_g[r, :ng], em_r[r, :nr]) and ref["resample_margin"][r] <= BOUNDARY:
+            boundary_rows.append(r)
+            continue
+        bad_rows.append(r)
+    if bad_rows:
+        r = bad_rows[0]
+        raise AssertionError("%d rows differ outside the boundary window; first row %d: gpu n=%d emitted=%s, "
+                             "oracle n=%d emitted=%s" % (len(bad_rows), r, acc_g[r], em_g[r], acc_r[r], em_r[r]))
+    err_rows = ref["row_error"]
+    assert np.all(acc_g[err_rows] == -1) and np.all(em_g[err_rows] == -1)
+    ok = ~err_rows
+    tol = TOL[dtype]
+    out = {"rows": int(len(acc_r)), "boundary_rows": len(boundary_rows)}
+    for key in ("p_at_draft", "logz_target"):
+        if key in gpu:
+            g = gpu[key].cpu().numpy()
+            if rows is not None:
+                g = g[rows]
+            assert np.all(np.isnan(g[err_rows]))
+            e = rel_err(g[ok], ref[key][ok]) if key == "p_at_draft" else logz_err(g[ok], ref[key][ok])
+            m = float(e.max()) if e.size else 0.0
+            assert m <= tol, "%s relative error %.3e > %.1e" % (key, m, tol)
+            out["max_rel_" + key] = m
+    return out
+
+
+def compare_sample(gpu, ref, dtype, rows=None):
+    """Draft-stage sampler: tokens bit for bit except draws within BOUNDARY of
+    a CDF step; greedy rows exact; log Z within the dtype's tolerance."""
+    tok = gpu["tokens"].cpu().numpy()
+    lz = gpu["logz"].cpu().numpy() if "logz" in gpu else None
+    if rows is not None:
+        tok = tok[rows]
+        lz = lz[rows] if lz is not None else None
+    diff = np.nonzero(tok != ref["token"])[0]
+    boundary = [r for r in diff if ref["margin"][r] <= BOUNDARY]
+    bad = [r for r in diff if not ref["margin"][r] <= BOUNDARY]
+    if bad:
+        r = bad[0]
+        raise AssertionError("%d rows differ; first row %d: gpu %d, oracle %d (margin %.3e)"
+                             % (len(bad), r, tok[r], ref["token"][r], ref["margin"][r]))
+    out = {"rows": int(len(tok)), "boundary_rows": len(boundary)}
+    if lz is not None:
+        samp = np.isfinite(ref["logz"])
+        assert np.all(np.isnan(lz[~samp]))
+        e = logz_err(lz[samp], ref["logz"][samp])
+        out["max_rel_logz"] = float(e.max()) if e.size else 0.0
+        assert out["max_rel_logz"] <= TOL[dtype]
+    return out
+
+
+def compare_diagnostics(gpu, ref, dtype, rows=None):
+    """Per-step diagnostics.  Relative tolerance of the dtype for max p,
+    alpha^TO and alpha^RS; entropies are a difference of two terms of size
+    log V, so their error is absolute: |dH| <= tol * max(1, H).  The split of
+    alpha^RS by the larger side may move by the mass of tokens whose p and q
+    agree to within the float32 decision precision (the oracle's tie_mass),
+    on top of tol * alpha^RS.  Greedy tokens exact; the preference flag exact
+    unless |alpha^RS - alpha^TO| is within the tolerance."""
+    tol = TOL[dtype]
+    g = {k: gpu[k].cpu().numpy().astype(np.float64) for k in DIAG_KEYS}
+    greedy = gpu["greedy_draft"].cpu().numpy()
+    prefer = gpu["rs_preferred"].cpu().numpy()
+    if rows is not None:
+        g = {k: v[rows] for k, v in g.items()}
+        greedy, prefer = greedy[rows], prefer[rows]
+    err = np.broadcast_to(ref["row_error"][:, None], ref["alpha_rs"].shape)
+    ok = ~err
+    for k in DIAG_KEYS:
+        assert np.all(np.isnan(g[k][err])), k
+    assert np.all(greedy[err] == -1) and np.all(prefer[err] == -1)
+    out = {"rows": int(len(err))}
+    for k in ("entropy_target", "entropy_draft"):
+        e = np.abs(g[k][ok] - ref[k][ok]) / np.maximum(1.0, np.abs(ref[k][ok]))
+        out["max_" + k] = float(e.max()) if e.size else 0.0
+        assert out["max_" + k] <= tol, (k, out["max_" + k])
+    for k in ("max_p", "alpha_to", "alpha_rs"):
+        e = rel_err(g[k][ok], ref[k][ok])
+        out["max_rel_" + k] = float(e.max()) if e.size else 0.0
+        assert out["max_rel_" + k] <= tol, (k, out["max_rel_" + k])
+    for k in ("alpha_p_gt_q", "alpha_q_ge_p"):
+        lim = tol * ref["alpha_rs"][ok] + ref["tie_mass"][ok]
+        e = np.abs(g[k][ok] - ref[k][ok])
+        assert np.all(e <= lim), (k, float((e - lim).max()))
+        out["max_abs_" + k] = float(e.max()) if e.size else 0.0
+    assert np.array_equal(greedy[ok], ref["greedy_draft"][ok])
+    amb = np.abs(ref["alpha_rs"] - ref["alpha_to"]) <= tol * np.maximum(ref["alpha_rs"], ref["alpha_to"])
+    sure = ok & ~amb
+    assert np.array_equal(prefer[sure], ref["rs_preferred"][sure].astype(np.int32))
+    out["ambiguous_preference"] = int((ok & amb).sum())
+    return out
+
+
+DIAG_KEYS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")

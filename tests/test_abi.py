@@ -33,7 +33,10 @@ def lib():
 def test_exports_every_declared_function(lib):
     protos = header_prototypes()
     assert set(protos) == {"spec_verify_workspace_size", "spec_verify", "spec_tv_workspace_size",
-                           "spec_tv_loss_fwd_bwd", "spec_status_string", "spec_version"}
+                           "spec_tv_loss_fwd_bwd", "spec_status_string", "spec_version",
+                           "spec_verify_target_only_workspace_size", "spec_verify_target_only",
+                           "spec_sample_workspace_size", "spec_sample",
+                           "spec_diagnostics_workspace_size", "spec_diagnostics"}
     for name in protos:
         assert hasattr(lib, name), name
 
@@ -42,6 +45,19 @@ def test_ctypes_prototypes_match_header():
     protos = header_prototypes()
     assert len(protos["spec_verify"]) == len(binding.VERIFY_ARGTYPES)
     assert len(protos["spec_tv_loss_fwd_bwd"]) == len(binding.TV_ARGTYPES)
+    assert len(protos["spec_verify_target_only"]) == len(binding.TO_ARGTYPES)
+    assert len(protos["spec_sample"]) == len(binding.SAMPLE_ARGTYPES)
+    assert len(protos["spec_diagnostics"]) == len(binding.DIAG_ARGTYPES)
+
+
+def test_diag_columns_match_header():
+    src = open(HEADER).read()
+    cols = re.findall(r"SPEC_DIAG_(\w+) = (\d+)", src)
+    named = {name.lower(): int(v) for name, v in cols}
+    assert named.pop("ncols") == len(binding.DIAG_COLUMNS)
+    assert sorted(named.values()) == list(range(len(binding.DIAG_COLUMNS)))
+    for name, v in named.items():
+        assert binding.DIAG_COLUMNS[v] == name, (name, v)
 
 
 def test_version_and_status_strings(lib):
@@ -63,6 +79,15 @@ def test_workspace_sizes(lib):
     assert 0 < a < b and a % 256 == 0
     assert lib.spec_tv_workspace_size(16384, 3, 151936, 1) > 0
     assert lib.spec_tv_workspace_size(16384, 0, 151936, 1) == 0
+    # target-only: statistics of the K+1 target rows only
+    to = lib.spec_verify_target_only_workspace_size(256, 3, 151936, 1)
+    assert to == 256 * 4 * 10 * 16
+    assert lib.spec_verify_target_only_workspace_size(256, 9, 151936, 1) == 0
+    assert lib.spec_sample_workspace_size(768, 151936, 1) == 768 * 10 * 16
+    assert lib.spec_sample_workspace_size(0, 151936, 1) == 0
+    assert lib.spec_sample_workspace_size(4, 0, 0) == 0
+    assert lib.spec_diagnostics_workspace_size(256, 3, 151936, 1) > 0
+    assert lib.spec_diagnostics_workspace_size(256, 0, 151936, 1) == 0
 
 
 FAKE = 0x10000  # never dereferenced: every call below fails validation first
@@ -129,3 +154,85 @@ def call_tv(lib, **kw):
 ])
 def test_tv_argument_errors(lib, kw, status):
     assert call_tv(lib, **kw) == status
+
+
+def call_to(lib, **kw):
+    args = dict(t=FAKE, tsb=400, tsk=100, dtype=1, B=4, K=3, V=100, ids=FAKE, temp=None, temp_s=1.0, seed=0,
+                off=0, acc=FAKE, em=FAKE, p=None, lzt=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    return lib.spec_verify_target_only(*[args[k] for k in ("t", "tsb", "tsk", "dtype", "B", "K", "V", "ids", "temp",
+                                                           "temp_s", "seed", "off", "acc", "em", "p", "lzt", "ws",
+                                                           "wsb", "stream")])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), 2),
+    (dict(K=9), 2),
+    (dict(B=0), 1),
+    (dict(K=0), 1),
+    (dict(V=0), 1),
+    (dict(t=None), 1),
+    (dict(ids=None), 1),
+    (dict(acc=None), 1),
+    (dict(em=None), 1),
+    (dict(tsk=-1), 1),
+    (dict(temp_s=0.0), 1),
+    (dict(temp_s=float("nan")), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=64), 4),
+    (dict(ws=FAKE + 8), 1),
+])
+def test_target_only_argument_errors(lib, kw, status):
+    assert call_to(lib, **kw) == status
+
+
+def call_sample(lib, **kw):
+    args = dict(z=FAKE, sr=100, dtype=1, R=4, V=100, temp=None, temp_s=1.0, seed=0, off=0, tok=FAKE, lz=None,
+                ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    return lib.spec_sample(*[args[k] for k in ("z", "sr", "dtype", "R", "V", "temp", "temp_s", "seed", "off", "tok",
+                                               "lz", "ws", "wsb", "stream")])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=5), 2),
+    (dict(R=0), 1),
+    (dict(V=0), 1),
+    (dict(z=None), 1),
+    (dict(tok=None), 1),
+    (dict(sr=-1), 1),
+    (dict(temp_s=-0.5), 1),
+    (dict(temp_s=float("inf")), 1),
+    (dict(temp_s=float("nan")), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=8), 4),
+    (dict(ws=FAKE + 4), 1),
+])
+def test_sample_argument_errors(lib, kw, status):
+    assert call_sample(lib, **kw) == status
+
+
+def call_diag(lib, **kw):
+    args = dict(t=FAKE, tsb=400, tsk=100, d=FAKE, dsb=300, dsk=100, dtype=1, B=4, K=3, V=100, temp=None,
+                temp_s=1.0, out=FAKE, g=None, pr=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    return lib.spec_diagnostics(*[args[k] for k in ("t", "tsb", "tsk", "d", "dsb", "dsk", "dtype", "B", "K", "V",
+                                                    "temp", "temp_s", "out", "g", "pr", "ws", "wsb", "stream")])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=2), 2),
+    (dict(K=9), 2),
+    (dict(B=0), 1),
+    (dict(K=0), 1),
+    (dict(V=0), 1),
+    (dict(t=None), 1),
+    (dict(d=None), 1),
+    (dict(out=None), 1),
+    (dict(dsb=-3), 1),
+    (dict(temp_s=0.0), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=16), 4),
+])
+def test_diagnostics_argument_errors(lib, kw, status):
+    assert call_diag(lib, **kw) == status
