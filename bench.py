@@ -14,7 +14,9 @@ read once) to the launch time measured with HIP events on the launch stream.
 `cpu_baseline` times the float64 CPU oracle on a bounded sample of rows of
 the same workload.  The fused TV-loss forward+backward on the training
 workload (N=16384 positions x 3 steps) is timed too and reported under
-`tv_loss` (not part of `value`).
+`tv_loss`; target-only verification, the draft-stage sampler (the B*K draft
+rows) and the per-step diagnostics on the same batch under `target_only`,
+`sample` and `diagnostics` (none of them part of `value`).
 """
 
 import argparse
@@ -92,6 +94,71 @@ def cpu_baseline(d_host, K, budget_s=10.0):
     }
 
 
+def timed(torch, stream, fn, steps):
+    """Mean milliseconds of fn(it) over `steps` calls, HIP events on `stream`."""
+    fn(0)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for it in range(steps):
+        fn(it)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def hbm_roofline(nbytes, ms, key):
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(key, nbytes)}
+
+
+def bench_variants(torch, binding, copies, stream, steps, B, K, V):
+    """Target-only verification, the draft-stage sampler and the per-step
+    diagnostics on the same batch (reported beside `value`, not in it)."""
+    out = {}
+    greedy = [torch.argmax(c["draft"].float(), dim=-1).to(torch.int32).contiguous() for c in copies]
+    to_out = {"accept_len": torch.empty(B, dtype=torch.int32, device="cuda"),
+              "emitted": torch.empty((B, K + 1), dtype=torch.int32, device="cuda")}
+
+    def to_step(it):
+        c = copies[it % len(copies)]
+        binding.verify_target_only(c["target"], greedy[it % len(copies)], c["temperature"], seed=it, out=to_out)
+
+    ms = timed(torch, stream, to_step, steps)
+    nbytes = B * (K + 1) * V * 2 + B * K * 4 + B * 4 + B * 4 + B * (K + 1) * 4
+    out["target_only"] = {"ms_per_call": ms, "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
+                          "mean_accept_len": float(to_out["accept_len"].float().mean()),
+                          "roofline": hbm_roofline(nbytes, ms, "target_only_bf16_b256_k3_v151936")}
+    R = B * K
+    flats = [c["draft"].reshape(R, V) for c in copies]
+    temps = [c["temperature"].repeat_interleave(K).contiguous() for c in copies]
+    s_out = {"tokens": torch.empty(R, dtype=torch.int32, device="cuda")}
+
+    def sample_step(it):
+        binding.sample(flats[it % len(copies)], temps[it % len(copies)], seed=it, out=s_out)
+
+    ms = timed(torch, stream, sample_step, steps)
+    nbytes = R * V * 2 + R * 4 + R * 4
+    out["sample"] = {"ms_per_call": ms, "rows": R, "rows_per_s": R / (ms * 1e-3),
+                     "roofline": hbm_roofline(nbytes, ms, "sample_bf16_r768_v151936")}
+    diag = {}
+
+    def diag_step(it):
+        c = copies[it % len(copies)]
+        diag["d"] = binding.diagnostics(c["target"], c["draft"], c["temperature"])
+
+    ms = timed(torch, stream, diag_step, steps)
+    nbytes = B * 2 * K * V * 2 + B * 4 + B * K * (7 * 4 + 4 + 4)
+    d = diag["d"]
+    out["diagnostics"] = {"ms_per_call": ms, "roofline": hbm_roofline(nbytes, ms, "diagnostics_bf16_b256_k3_v151936"),
+                          "mean_alpha_rs": float(d["alpha_rs"].mean()), "mean_alpha_to": float(d["alpha_to"].mean()),
+                          "mean_entropy_target": float(d["entropy_target"].mean()),
+                          "rs_preferred_fraction": float(d["rs_preferred"].float().mean())}
+    return out
+
+
 def copy_calibration(torch, dev, gib=1, reps=3):
     """A plain device-to-device copy of known size, for scaling the FETCH_SIZE
     and WRITE_SIZE counters of the other kernels in the same profile."""
@@ -113,6 +180,9 @@ def main():
     ap.add_argument("--no-tv", action="store_true")
     ap.add_argument("--tv-steps", type=int, default=3)
     ap.add_argument("--no-verify", action="store_true", help="skip the verify benchmark (profiling runs)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip target-only verification, the sampler and the diagnostics")
+    ap.add_argument("--variant-steps", type=int, default=20)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
@@ -152,9 +222,10 @@ def main():
                    "temperature": "per row, 1.0", "input_copies": 2},
     }
 
-    if not args.no_verify:
+    if not args.no_verify or not args.no_variants:
         log("generating inputs B=%d K=%d V=%d bf16" % (B, K, V))
         copies = [W.verify_inputs_torch(B, K, V, W.BF16, cfg["gen"], cfg["seed"] + 100 * c) for c in range(2)]
+    if not args.no_verify:
         outs = [{
             "accept_len": torch.empty(B, dtype=torch.int32, device=dev),
             "emitted": torch.empty((B, K + 1), dtype=torch.int32, device=dev),
@@ -194,7 +265,12 @@ def main():
             "mean_accept_len": float(acc.mean()),
             "wall_s_timed_region": wall,
         })
-        del copies, outs
+        del outs
+    if not args.no_variants:
+        log("timing target-only verification, the sampler and the diagnostics")
+        result.update(bench_variants(torch, binding, copies, stream, args.variant_steps, B, K, V))
+    if not args.no_verify or not args.no_variants:
+        del copies
         torch.cuda.empty_cache()
 
     if not args.no_tv:
