@@ -18,6 +18,8 @@ tv       TV loss, its gradient and the end-to-end multi-step TV loss
 variants Target-only verification (Sec. 2.2 Eq. target_only), the draft-stage
          sampler (App. G.1 draft stage) and per-step diagnostics (entropies,
          alpha^TO, alpha^RS and its split, the App. E decision boundary).
+gumbel   Gumbel-max verification (App. G.2, Alg. rs_gumbel) and the
+         Gumbel-max draft sampler.
 
 Every function is pinned by the ``-m "not gpu"`` tests against something
 other than itself (numpy's own Philox, scipy routines, closed forms,
