@@ -16,7 +16,9 @@ the same workload.  The fused TV-loss forward+backward on the training
 workload (N=16384 positions x 3 steps) is timed too and reported under
 `tv_loss`; target-only verification, the draft-stage sampler (the B*K draft
 rows) and the per-step diagnostics on the same batch under `target_only`,
-`sample` and `diagnostics` (none of them part of `value`).
+`sample` and `diagnostics`, and the Gumbel-max variants of verification and
+sampling under `verify_gumbel` and `sample_gumbel` (none of them part of
+`value`).
 """
 
 import argparse
@@ -143,6 +145,27 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
     nbytes = R * V * 2 + R * 4 + R * 4
     out["sample"] = {"ms_per_call": ms, "rows": R, "rows_per_s": R / (ms * 1e-3),
                      "roofline": hbm_roofline(nbytes, ms, "sample_bf16_r768_v151936")}
+    g_out = {"accept_len": torch.empty(B, dtype=torch.int32, device="cuda"),
+             "emitted": torch.empty((B, K + 1), dtype=torch.int32, device="cuda"),
+             "overlap": torch.empty((B, K), dtype=torch.float32, device="cuda")}
+
+    def gumbel_step(it):
+        c = copies[it % len(copies)]
+        binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=g_out, gumbel=True)
+
+    ms = timed(torch, stream, gumbel_step, steps)
+    nbytes = B * (2 * K + 1) * V * 2 + B * K * 4 + B * 4 + B * 4 + B * (K + 1) * 4 + B * K * 4
+    out["verify_gumbel"] = {"ms_per_call": ms, "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
+                            "roofline": hbm_roofline(nbytes, ms, "verify_gumbel_bf16_b256_k3_v151936")}
+    sg_out = {"tokens": torch.empty(R, dtype=torch.int32, device="cuda")}
+
+    def sample_gumbel_step(it):
+        binding.sample_gumbel(flats[it % len(copies)], temps[it % len(copies)], seed=it, out=sg_out)
+
+    ms = timed(torch, stream, sample_gumbel_step, steps)
+    nbytes = R * V * 2 + R * 4 + R * 4
+    out["sample_gumbel"] = {"ms_per_call": ms, "rows": R, "rows_per_s": R / (ms * 1e-3),
+                            "roofline": hbm_roofline(nbytes, ms, "sample_gumbel_bf16_r768_v151936")}
     diag = {}
 
     def diag_step(it):

@@ -8,7 +8,8 @@
  * tokens; Sec. 4.1 (Eqs. tv_loss, tv_grad), App. A and Sec. 4.2 (Eq. e2e_tv)
  * define the TV loss, its gradient and the end-to-end multi-step TV loss.
  * Sec. 2.2 (Eq. target_only) defines target-only verification, App. G.1 the
- * draft-stage sampler, Sec. 3 and App. E the acceptance diagnostics.
+ * draft-stage sampler, Sec. 3 and App. E the acceptance diagnostics, App. G.2
+ * (Alg. rs_gumbel) Gumbel-max verification and the Gumbel-max draft sampler.
  *
  * Conventions shared by every entry point
  *  - All tensor pointers are DEVICE pointers owned by the caller.  The
@@ -28,7 +29,8 @@
  *    them on one stream).
  *  - Each call is a short fixed sequence of kernel launches on `stream`
  *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a gradient,
- *    spec_verify_target_only: 2, spec_sample: 2, spec_diagnostics: 4); no
+ *    spec_verify_target_only: 2, spec_sample: 2, spec_diagnostics: 4,
+ *    spec_verify_gumbel: 4, or 3 without overlaps, spec_sample_gumbel: 2); no
  *    launch waits on another workgroup, so any number of resident
  *    workgroups is enough.
  *  - Entry points are thread-safe; each call is independent.
@@ -152,6 +154,55 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
                                  float temperature, spec_tv_mode mode, float scale,
                                  float* loss, float* overlap, float* grad_draft,
                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spec_verify_gumbel needs (0 on invalid sizes). */
+size_t spec_verify_gumbel_workspace_size(int B, int K, int V, spec_dtype dtype);
+
+/*
+ * spec_verify_gumbel — chain rejection-sampling verification with the
+ * token at the emitting position drawn by the Gumbel-max trick (App. G.2,
+ * Alg. rs_gumbel).  Arguments, outputs, accept tests, uniforms of the accept
+ * tests and row-error handling are those of spec_verify; only emitted[b, n]
+ * differs:
+ *   emitted[b, n] = argmax_v [ log r(v) + G_v ],  r = max(0, p_n - q_n) if n < K,
+ *                   and log r replaced by z_K / T for the bonus (n = K);
+ *                   first index among ties; r = p_n if the residual has no mass
+ *   G_v = -log(-log U_v), U_v = (bits + 1/2) * 2^-24, bits = the top 24 bits
+ *         (v even) or bits 8..31 (v odd) of word (v >> 1) & 3 of
+ *         Philox4x64-10(counter = (b, v >> 3, offset, 2), key = (seed, 0))
+ * With overlap == NULL the pairs are not read a second time; the emitting
+ * row (pair) is then the only one read again, in full.
+ */
+spec_status spec_verify_gumbel(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                               const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                               spec_dtype dtype, int B, int K, int V,
+                               const int32_t* draft_ids,
+                               const float* temperature, float temperature_scalar,
+                               uint64_t seed, uint64_t offset,
+                               int32_t* accept_len, int32_t* emitted_ids,
+                               float* overlap, float* p_at_draft, float* q_at_draft,
+                               float* logz_target, float* logz_draft,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spec_sample_gumbel needs (0 on invalid sizes). */
+size_t spec_sample_gumbel_workspace_size(int R, int V, spec_dtype dtype);
+
+/*
+ * spec_sample_gumbel — the Gumbel-max draft stage (App. G.2): row r with
+ * T = temperature[r] (or temperature_scalar) > 0 gets
+ *   tokens[r] = argmax_v [ logits[r, v] / T + G_v ] (first index among ties),
+ * G_v as in spec_verify_gumbel with counter (r, v >> 3, offset, 3); T == 0
+ * takes the greedy token (first index of the largest logit).  One read of
+ * the logits, no normaliser.
+ * logits [R, V] with row stride stride_r; temperature [R] or NULL (scalar,
+ * finite, >= 0); tokens [R] int32 out.  Row data errors (NaN or +inf
+ * logits, all -inf, a negative or non-finite per-row temperature) give -1.
+ * Limits: 1 <= R, 1 <= V < 2^31.
+ */
+spec_status spec_sample_gumbel(const void* logits, int64_t stride_r, spec_dtype dtype, int R, int V,
+                               const float* temperature, float temperature_scalar,
+                               uint64_t seed, uint64_t offset, int32_t* tokens,
+                               void* workspace, size_t workspace_bytes, void* stream);
 
 /* Bytes of workspace spec_verify_target_only needs (0 on invalid sizes). */
 size_t spec_verify_target_only_workspace_size(int B, int K, int V, spec_dtype dtype);

@@ -41,6 +41,7 @@ VERIFY_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _P, _P, _F, _
 TV_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _SZ, _P]
 TO_ARGTYPES = [_P, _I64, _I64, _I, _I, _I, _I, _P, _P, _F, _U64, _U64, _P, _P, _P, _P, _P, _SZ, _P]
 SAMPLE_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _P, _SZ, _P]
+SAMPLE_GUMBEL_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _SZ, _P]
 DIAG_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _P, _F, _P, _P, _P, _P, _SZ, _P]
 DIAG_COLUMNS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")
 
@@ -88,6 +89,14 @@ def load_library():
         lib.spec_diagnostics_workspace_size.argtypes = [_I, _I, _I, _I]
         lib.spec_diagnostics.restype = _I
         lib.spec_diagnostics.argtypes = DIAG_ARGTYPES
+        lib.spec_verify_gumbel_workspace_size.restype = _SZ
+        lib.spec_verify_gumbel_workspace_size.argtypes = [_I, _I, _I, _I]
+        lib.spec_verify_gumbel.restype = _I
+        lib.spec_verify_gumbel.argtypes = VERIFY_ARGTYPES
+        lib.spec_sample_gumbel_workspace_size.restype = _SZ
+        lib.spec_sample_gumbel_workspace_size.argtypes = [_I, _I, _I]
+        lib.spec_sample_gumbel.restype = _I
+        lib.spec_sample_gumbel.argtypes = SAMPLE_GUMBEL_ARGTYPES
         _lib = lib
         return lib
 
@@ -106,6 +115,16 @@ def _ptr(t):
 
 def _stream(device):
     return _P(torch.cuda.current_stream(device).cuda_stream)
+
+
+def verify_gumbel_workspace_size(B, K, V, dtype=torch.bfloat16):
+    code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
+    return int(load_library().spec_verify_gumbel_workspace_size(B, K, V, code))
+
+
+def sample_gumbel_workspace_size(R, V, dtype=torch.bfloat16):
+    code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
+    return int(load_library().spec_sample_gumbel_workspace_size(R, V, code))
 
 
 def verify_workspace_size(B, K, V, dtype=torch.bfloat16):
@@ -172,8 +191,9 @@ def _check_ids(ids, B, K):
 
 
 def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offset=0,
-           want_debug=False, want_overlap=True, ws=None, out=None):
-    """Chain rejection-sampling verification (spec_verify).
+           want_debug=False, want_overlap=True, ws=None, out=None, gumbel=False):
+    """Chain rejection-sampling verification (spec_verify, or with
+    gumbel=True spec_verify_gumbel: the emitted token drawn by Gumbel-max).
 
     target_logits [B, K+1, V], draft_logits [B, K, V] (bf16 or f32, same
     dtype, vocabulary dimension contiguous), draft_ids [B, K] int32,
@@ -214,12 +234,14 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
             out["q_at_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
             out["logz_target"] = torch.empty((B, K + 1), dtype=torch.float32, device=dev)
             out["logz_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
-    need = int(lib.spec_verify_workspace_size(B, K, V, code))
+    size_fn = lib.spec_verify_gumbel_workspace_size if gumbel else lib.spec_verify_workspace_size
+    fn, name = (lib.spec_verify_gumbel, "spec_verify_gumbel") if gumbel else (lib.spec_verify, "spec_verify")
+    need = int(size_fn(B, K, V, code))
     if need == 0:
         raise ValueError("unsupported verify shape B=%d K=%d V=%d" % (B, K, V))
     if ws is None:
         ws = workspace(need, dev)
-    st = lib.spec_verify(
+    st = fn(
         _ptr(target_logits), target_logits.stride(0), target_logits.stride(1),
         _ptr(draft_logits), draft_logits.stride(0), draft_logits.stride(1),
         code, B, K, V, _ptr(ids), t_ptr, t_scalar, int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
@@ -228,7 +250,7 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
         _ptr(out.get("logz_target")), _ptr(out.get("logz_draft")),
         _ptr(ws), ws.numel(), _stream(dev))
     if st != 0:
-        raise SpecError("spec_verify", st)
+        raise SpecError(name, st)
     return out
 
 
@@ -378,4 +400,33 @@ def diagnostics(target_logits, draft_logits, temperature=1.0, ws=None):
         raise SpecError("spec_diagnostics", st)
     out = {name: table[..., c] for c, name in enumerate(DIAG_COLUMNS)}
     out.update(table=table, greedy_draft=greedy, rs_preferred=prefer)
+    return out
+
+
+def sample_gumbel(logits, temperature=1.0, seed=0, offset=0, ws=None, out=None):
+    """Gumbel-max draft sampling (spec_sample_gumbel) of one token per row.
+
+    logits [R, V] (bf16 or f32, vocabulary dimension contiguous, any row
+    stride); temperature: float or [R] float32 tensor, 0 meaning greedy.
+    Returns a dict with tokens [R] int32.
+    """
+    lib = load_library()
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be [R, V] with a contiguous vocabulary dimension")
+    R, V = logits.shape
+    dev = logits.device
+    t_ptr, t_scalar = _temperature_arg(temperature, R)
+    code = _dtype_code(logits)
+    if out is None:
+        out = {"tokens": torch.empty(R, dtype=torch.int32, device=dev)}
+    need = int(lib.spec_sample_gumbel_workspace_size(R, V, code))
+    if need == 0:
+        raise ValueError("unsupported sample shape R=%d V=%d" % (R, V))
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib.spec_sample_gumbel(
+        _ptr(logits), logits.stride(0), code, R, V, t_ptr, t_scalar,
+        int(seed) & (2**64 - 1), int(offset) & (2**64 - 1), _ptr(out["tokens"]), _ptr(ws), ws.numel(), _stream(dev))
+    if st != 0:
+        raise SpecError("spec_sample_gumbel", st)
     return out

@@ -12,6 +12,7 @@
 
 #include "specverify.h"
 #include "sv_device.h"
+#include "gumbel_kernel.h"
 #include "tv_kernel.h"
 #include "variants_kernel.h"
 #include "verify_kernel.h"
@@ -70,9 +71,9 @@ bool rows_ok(int64_t rows, int V, spec_dtype dt) {
 }
 
 struct VerifyLayout {
-  size_t stats = 0, norms = 0, decision = 0, pairs = 0, total = 0;
+  size_t stats = 0, norms = 0, decision = 0, pairs = 0, gbest = 0, total = 0;
 };
-VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt) {
+VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt, bool gumbel = false) {
   VerifyLayout L;
   const size_t C = static_cast<size_t>(geometry(V, dt).C);
   const size_t rows = static_cast<size_t>(B) * (2 * K + 1);
@@ -81,6 +82,9 @@ VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt) {
   L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
   L.decision = off; off = align_up(off + static_cast<size_t>(B) * sizeof(int32_t), 256);
   L.pairs = off; off = align_up(off + static_cast<size_t>(B) * K * C * sizeof(sv::PairStat), 256);
+  if (gumbel) {  // per (batch row, chunk) best Gumbel keys
+    L.gbest = off; off = align_up(off + static_cast<size_t>(B) * C * sizeof(sv::GumbelBest), 256);
+  }
   L.total = off;
   return L;
 }
@@ -191,6 +195,38 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) 
 }
 
 template <class E, int NT>
+spec_status launch_verify_gumbel(const sv::VerifyArgs& a, sv::GumbelBest* gbest, int64_t rows, hipStream_t s) {
+  const int C = a.rows.C;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(rows * C)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), rows * C);
+  hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
+  if (a.overlap) {  // overlaps only: the Gumbel pass needs no residual mass
+    void (*pp)(sv::VerifyArgs, int64_t) = sv::pair_pass_kernel<E, NT, kStep>;
+    const int64_t pairs = int64_t{a.B} * a.K * C;
+    hipLaunchKernelGGL(pp, dim3(grid_for(reinterpret_cast<const void*>(pp), pairs)), dim3(sv::kThreads), 0, s, a,
+                       pairs);
+  }
+  void (*gp)(sv::VerifyArgs, sv::GumbelBest*, int64_t) = sv::gumbel_pass_kernel<E, NT, kStep>;
+  const int64_t tasks = int64_t{a.B} * C;
+  hipLaunchKernelGGL(gp, dim3(grid_for(reinterpret_cast<const void*>(gp), tasks)), dim3(sv::kThreads), 0, s, a,
+                     gbest, tasks);
+  hipLaunchKernelGGL(sv::gumbel_finish_kernel, dim3(static_cast<unsigned>((a.B + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a, static_cast<const sv::GumbelBest*>(gbest));
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
+spec_status launch_sample_gumbel(const sv::GumbelSampleArgs& a, hipStream_t s) {
+  const int64_t tasks = int64_t{a.R} * a.rows.C;
+  void (*gp)(sv::GumbelSampleArgs, int64_t) = sv::gumbel_sample_pass_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(gp, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a, tasks);
+  hipLaunchKernelGGL(sv::gumbel_sample_finish_kernel, dim3(static_cast<unsigned>((a.R + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
 spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
   const int64_t units = int64_t{a.N} * a.K;
   const int C = a.rows.C;
@@ -255,6 +291,53 @@ spec_status launch_diag(const sv::DiagArgs& a, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
+// Validation and argument block shared by the two verification entry points.
+spec_status prepare_verify(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                           const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k, spec_dtype dtype,
+                           int B, int K, int V, const int32_t* draft_ids, const float* temperature,
+                           float temperature_scalar, uint64_t seed, uint64_t offset, int32_t* accept_len,
+                           int32_t* emitted_ids, float* overlap, float* p_at_draft, float* q_at_draft,
+                           float* logz_target, float* logz_draft, void* workspace, size_t workspace_bytes,
+                           bool gumbel, sv::VerifyArgs* out, sv::GumbelBest** gbest) {
+  // ---- validation: synchronous, before anything touches the GPU ------------
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
+  if (!verify_sizes_ok(B, K, V, dtype)) return SPEC_EINVAL;
+  if (!target_logits || !draft_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
+  if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
+  const VerifyLayout L = verify_layout(B, K, V, dtype, gumbel);
+  if (!workspace) return SPEC_EWORKSPACE;
+  if (workspace_bytes < L.total) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  const size_t es = esize_of(dtype);
+  sv::VerifyArgs a{};
+  a.rows.tgt = target_logits; a.rows.tsb = t_stride_b; a.rows.tsk = t_stride_k; a.rows.tper = K + 1;
+  a.rows.drf = draft_logits; a.rows.dsb = d_stride_b; a.rows.dsk = d_stride_k; a.rows.dper = K;
+  a.rows.nb = B;
+  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, es) ? 1 : 0;
+  a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_b, d_stride_k, es) ? 1 : 0;
+  a.B = B; a.K = K;
+  a.ids = draft_ids;
+  a.seed = seed; a.offset = offset;
+  a.accept_len = accept_len; a.emitted = emitted_ids;
+  a.overlap = overlap; a.p_at = p_at_draft; a.q_at = q_at_draft;
+  a.logz_t = logz_target; a.logz_d = logz_draft;
+  char* ws = static_cast<char*>(workspace);
+  a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
+  a.norms = reinterpret_cast<sv::RowNorm*>(ws + L.norms);
+  a.decision = reinterpret_cast<int32_t*>(ws + L.decision);
+  a.pairs = reinterpret_cast<sv::PairStat*>(ws + L.pairs);
+  a.want_z = gumbel ? 0 : 1;
+  *gbest = gumbel ? reinterpret_cast<sv::GumbelBest*>(ws + L.gbest) : nullptr;
+  *out = a;
+  return SPEC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -284,6 +367,7 @@ size_t spec_tv_workspace_size(int N, int K, int V, spec_dtype dtype) {
   return tv_layout(N, K, V, dtype).total;
 }
 
+
 spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
                         const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
                         spec_dtype dtype, int B, int K, int V, const int32_t* draft_ids,
@@ -291,42 +375,75 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
                         uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
                         float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
                         void* workspace, size_t workspace_bytes, void* stream) {
-  // ---- validation: synchronous, before anything touches the GPU ------------
-  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
-  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
-  if (!verify_sizes_ok(B, K, V, dtype)) return SPEC_EINVAL;
-  if (!target_logits || !draft_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
-  if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
-  if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
-  const VerifyLayout L = verify_layout(B, K, V, dtype);
-  if (!workspace) return SPEC_EWORKSPACE;
-  if (workspace_bytes < L.total) return SPEC_EWORKSPACE;
-  if (!aligned16(workspace)) return SPEC_EINVAL;
-
-  const Geometry g = geometry(V, dtype);
-  const size_t es = esize_of(dtype);
-  sv::VerifyArgs a{};
-  a.rows.tgt = target_logits; a.rows.tsb = t_stride_b; a.rows.tsk = t_stride_k; a.rows.tper = K + 1;
-  a.rows.drf = draft_logits; a.rows.dsb = d_stride_b; a.rows.dsk = d_stride_k; a.rows.dper = K;
-  a.rows.nb = B;
-  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
-  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
-  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, es) ? 1 : 0;
-  a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_b, d_stride_k, es) ? 1 : 0;
-  a.B = B; a.K = K;
-  a.ids = draft_ids;
-  a.seed = seed; a.offset = offset;
-  a.accept_len = accept_len; a.emitted = emitted_ids;
-  a.overlap = overlap; a.p_at = p_at_draft; a.q_at = q_at_draft;
-  a.logz_t = logz_target; a.logz_d = logz_draft;
-  char* ws = static_cast<char*>(workspace);
-  a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
-  a.norms = reinterpret_cast<sv::RowNorm*>(ws + L.norms);
-  a.decision = reinterpret_cast<int32_t*>(ws + L.decision);
-  a.pairs = reinterpret_cast<sv::PairStat*>(ws + L.pairs);
+  sv::VerifyArgs a;
+  sv::GumbelBest* gb;
+  const spec_status st = prepare_verify(target_logits, t_stride_b, t_stride_k, draft_logits, d_stride_b, d_stride_k,
+                                        dtype, B, K, V, draft_ids, temperature, temperature_scalar, seed, offset,
+                                        accept_len, emitted_ids, overlap, p_at_draft, q_at_draft, logz_target,
+                                        logz_draft, workspace, workspace_bytes, false, &a, &gb);
+  if (st != SPEC_OK) return st;
   const int64_t rows = int64_t{B} * (2 * K + 1);
   hipStream_t s = static_cast<hipStream_t>(stream);
   return dtype == SPEC_BF16 ? launch_verify<BF16, kNtBf16>(a, rows, s) : launch_verify<F32, kNtF32>(a, rows, s);
+}
+
+size_t spec_verify_gumbel_workspace_size(int B, int K, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (!verify_sizes_ok(B, K, V, dtype)) return 0;
+  return verify_layout(B, K, V, dtype, true).total;
+}
+
+spec_status spec_verify_gumbel(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                               const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                               spec_dtype dtype, int B, int K, int V, const int32_t* draft_ids,
+                               const float* temperature, float temperature_scalar, uint64_t seed,
+                               uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
+                               float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  sv::VerifyArgs a;
+  sv::GumbelBest* gb;
+  const spec_status st = prepare_verify(target_logits, t_stride_b, t_stride_k, draft_logits, d_stride_b, d_stride_k,
+                                        dtype, B, K, V, draft_ids, temperature, temperature_scalar, seed, offset,
+                                        accept_len, emitted_ids, overlap, p_at_draft, q_at_draft, logz_target,
+                                        logz_draft, workspace, workspace_bytes, true, &a, &gb);
+  if (st != SPEC_OK) return st;
+  const int64_t rows = int64_t{B} * (2 * K + 1);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_verify_gumbel<BF16, kNtBf16>(a, gb, rows, s)
+                            : launch_verify_gumbel<F32, kNtF32>(a, gb, rows, s);
+}
+
+size_t spec_sample_gumbel_workspace_size(int R, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (!rows_ok(R, V, dtype)) return 0;
+  return align_up(static_cast<size_t>(R) * geometry(V, dtype).C * sizeof(sv::GumbelBest), 256);
+}
+
+spec_status spec_sample_gumbel(const void* logits, int64_t stride_r, spec_dtype dtype, int R, int V,
+                               const float* temperature, float temperature_scalar, uint64_t seed, uint64_t offset,
+                               int32_t* tokens, void* workspace, size_t workspace_bytes, void* stream) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (!rows_ok(R, V, dtype)) return SPEC_EINVAL;
+  if (!logits || !tokens || stride_r < 0) return SPEC_EINVAL;
+  if (!temperature && !(temperature_scalar >= 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
+  if (!workspace || workspace_bytes < spec_sample_gumbel_workspace_size(R, V, dtype)) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  sv::GumbelSampleArgs a{};
+  a.rows.tgt = logits; a.rows.tsb = stride_r; a.rows.tsk = 0; a.rows.tper = 1;
+  a.rows.drf = nullptr; a.rows.dsb = 0; a.rows.dsk = 0; a.rows.dper = 1;
+  a.rows.nb = R;
+  a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(logits, stride_r, 0, esize_of(dtype)) ? 1 : 0;
+  a.rows.vec_d = 0;
+  a.R = R;
+  a.seed = seed; a.offset = offset;
+  a.token = tokens;
+  a.best = reinterpret_cast<sv::GumbelBest*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_sample_gumbel<BF16, kNtBf16>(a, s) : launch_sample_gumbel<F32, kNtF32>(a, s);
 }
 
 spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,

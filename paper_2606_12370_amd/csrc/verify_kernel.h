@@ -41,6 +41,7 @@ struct VerifyArgs {
   RowNorm* norms;         // [rows]
   int32_t* decision;      // [B]: accept length n, or -1 for a row with a data error
   PairStat* pairs;        // [B*K][C]
+  int want_z;             // pair_pass also sums the residual mass of the first rejected step
 };
 
 __device__ __forceinline__ int target_row(const VerifyArgs& a, int b, int i) { return b * (a.K + 1) + i; }
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
     const int b = u / a.K, i = u % a.K;
     const int n = a.decision[b];
     if (n < 0) continue;  // data error: finish ignores this row's partials
-    const bool need_z = i == n;
+    const bool need_z = a.want_z && i == n;
     if (!need_z && a.overlap == nullptr) continue;  // no overlap requested: only the residual step is read again
     const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
     int bb;

@@ -254,3 +254,61 @@ def compare_diagnostics(gpu, ref, dtype, rows=None):
 
 
 DIAG_KEYS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")
+
+
+GUMBEL_EPS = 2e-6
+
+
+def compare_verify_gumbel(gpu, ref, dtype, rows=None):
+    """Gumbel-max verification: as compare_verify for the accept decisions,
+    overlaps and debug outputs; a different emitted token at the same
+    accept length is a boundary draw only if the oracle's score of the GPU's
+    token is within the float32 precision of the GPU's keys of the best
+    score: GUMBEL_EPS * (4 + sens_best + sens_gpu), sens = (p + q) / r being
+    how strongly the relative rounding of p and q moves log r."""
+    em_g = gpu["emitted"].cpu().numpy()
+    acc_g = gpu["accept_len"].cpu().numpy()
+    if rows is not None:
+        em_g, acc_g = em_g[rows], acc_g[rows]
+    em_fixed = em_g.copy()
+    boundary = 0
+    for r in np.nonzero(acc_g == ref["accept_len"])[0]:
+        n = int(acc_g[r])
+        if n < 0 or em_g[r, n] == ref["emitted"][r, n] or not np.array_equal(em_g[r, :n], ref["emitted"][r, :n]):
+            continue
+        g, o = int(em_g[r, n]), int(ref["emitted"][r, n])
+        assert 0 <= g < ref["gumbel_score"].shape[1], "row %d: gpu token %d out of range" % (r, g)
+        sc, sens = ref["gumbel_score"][r], ref["gumbel_sens"][r]
+        gap = sc[o] - sc[g]
+        lim = GUMBEL_EPS * (4 + sens[o] + sens[g])
+        assert gap <= lim, "row %d: gpu token %d (score %.9g), oracle %d (score %.9g), gap %.3e > %.3e" % (
+            r, g, sc[g], o, sc[o], gap, lim)
+        em_fixed[r, n] = o
+        boundary += 1
+    full = dict(gpu)
+    if rows is not None:
+        full = {k: (v[torch.as_tensor(rows, device=v.device)] if torch.is_tensor(v) else v) for k, v in gpu.items()}
+    full["emitted"] = torch.from_numpy(em_fixed)
+    ref2 = dict(ref)
+    ref2["resample_margin"] = np.full(len(ref["accept_len"]), np.inf)
+    out = compare_verify(full, ref2, dtype)
+    out["gumbel_boundary_rows"] = boundary
+    return out
+
+
+def compare_sample_gumbel(tokens, ref, rows=None):
+    """Gumbel-max sampler: tokens bit for bit, except where the oracle's score
+    of the GPU's token is within float32 precision of the best score."""
+    tok = tokens.cpu().numpy()
+    if rows is not None:
+        tok = tok[rows]
+    boundary = 0
+    for r in np.nonzero(tok != ref["token"])[0]:
+        g, o = int(tok[r]), int(ref["token"][r])
+        assert g >= 0 and o >= 0, "row %d: gpu %d, oracle %d" % (r, g, o)
+        sc = ref["score"][r]
+        gap = sc[o] - sc[g]
+        lim = 1e-6 * (4 + abs(sc[o]) + abs(sc[g]))
+        assert gap <= lim, "row %d: gpu %d, oracle %d, score gap %.3e > %.3e" % (r, g, o, gap, lim)
+        boundary += 1
+    return {"rows": int(len(tok)), "boundary_rows": boundary}

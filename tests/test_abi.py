@@ -36,7 +36,9 @@ def test_exports_every_declared_function(lib):
                            "spec_tv_loss_fwd_bwd", "spec_status_string", "spec_version",
                            "spec_verify_target_only_workspace_size", "spec_verify_target_only",
                            "spec_sample_workspace_size", "spec_sample",
-                           "spec_diagnostics_workspace_size", "spec_diagnostics"}
+                           "spec_diagnostics_workspace_size", "spec_diagnostics",
+                           "spec_verify_gumbel_workspace_size", "spec_verify_gumbel",
+                           "spec_sample_gumbel_workspace_size", "spec_sample_gumbel"}
     for name in protos:
         assert hasattr(lib, name), name
 
@@ -48,6 +50,9 @@ def test_ctypes_prototypes_match_header():
     assert len(protos["spec_verify_target_only"]) == len(binding.TO_ARGTYPES)
     assert len(protos["spec_sample"]) == len(binding.SAMPLE_ARGTYPES)
     assert len(protos["spec_diagnostics"]) == len(binding.DIAG_ARGTYPES)
+    assert len(protos["spec_verify_gumbel"]) == len(binding.VERIFY_ARGTYPES)
+    assert protos["spec_verify_gumbel"] == protos["spec_verify"]
+    assert len(protos["spec_sample_gumbel"]) == len(binding.SAMPLE_GUMBEL_ARGTYPES)
 
 
 def test_diag_columns_match_header():
@@ -88,6 +93,11 @@ def test_workspace_sizes(lib):
     assert lib.spec_sample_workspace_size(4, 0, 0) == 0
     assert lib.spec_diagnostics_workspace_size(256, 3, 151936, 1) > 0
     assert lib.spec_diagnostics_workspace_size(256, 0, 151936, 1) == 0
+    # Gumbel-max: the verify workspace plus one 16-byte best key per (batch row, chunk)
+    assert lib.spec_verify_gumbel_workspace_size(256, 3, 151936, 1) >= b + 256 * 10 * 16
+    assert lib.spec_verify_gumbel_workspace_size(256, 9, 151936, 1) == 0
+    assert lib.spec_sample_gumbel_workspace_size(768, 151936, 1) == 768 * 10 * 16
+    assert lib.spec_sample_gumbel_workspace_size(0, 151936, 1) == 0
 
 
 FAKE = 0x10000  # never dereferenced: every call below fails validation first
@@ -236,3 +246,42 @@ def call_diag(lib, **kw):
 ])
 def test_diagnostics_argument_errors(lib, kw, status):
     assert call_diag(lib, **kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), 2),
+    (dict(K=9), 2),
+    (dict(B=0), 1),
+    (dict(t=None), 1),
+    (dict(ids=None), 1),
+    (dict(temp_s=0.0), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=64), 4),
+])
+def test_verify_gumbel_argument_errors(lib, kw, status):
+    args = dict(t=FAKE, tsb=400, tsk=100, d=FAKE, dsb=300, dsk=100, dtype=1, B=4, K=3, V=100, ids=FAKE,
+                temp=None, temp_s=1.0, seed=0, off=0, acc=FAKE, em=FAKE, ov=None, p=None, q=None,
+                lzt=None, lzd=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    assert lib.spec_verify_gumbel(*[args[k] for k in ("t", "tsb", "tsk", "d", "dsb", "dsk", "dtype", "B", "K", "V",
+                                                      "ids", "temp", "temp_s", "seed", "off", "acc", "em", "ov", "p",
+                                                      "q", "lzt", "lzd", "ws", "wsb", "stream")]) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=5), 2),
+    (dict(R=0), 1),
+    (dict(V=0), 1),
+    (dict(z=None), 1),
+    (dict(tok=None), 1),
+    (dict(temp_s=-0.5), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=8), 4),
+    (dict(ws=FAKE + 4), 1),
+])
+def test_sample_gumbel_argument_errors(lib, kw, status):
+    args = dict(z=FAKE, sr=100, dtype=1, R=4, V=100, temp=None, temp_s=1.0, seed=0, off=0, tok=FAKE,
+                ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    assert lib.spec_sample_gumbel(*[args[k] for k in ("z", "sr", "dtype", "R", "V", "temp", "temp_s", "seed", "off",
+                                                      "tok", "ws", "wsb", "stream")]) == status
