@@ -20,6 +20,8 @@ variants Target-only verification (Sec. 2.2 Eq. target_only), the draft-stage
          alpha^TO, alpha^RS and its split, the App. E decision boundary).
 gumbel   Gumbel-max verification (App. G.2, Alg. rs_gumbel) and the
          Gumbel-max draft sampler.
+kl       CE, forward-KL and reverse-KL losses and gradients (Sec. 4.1 and its
+         footnote, Table grad_comparison, App. B, App. C).
 
 Every function is pinned by the ``-m "not gpu"`` tests against something
 other than itself (numpy's own Philox, scipy routines, closed forms,

@@ -1,0 +1,101 @@
+"""Pins of the CE / forward-KL / reverse-KL oracle against scipy's entropy,
+relative-entropy and xlogy routines, central finite differences of the
+losses, the identity CE = H(p) + KL(p||q), Pinsker's inequality (Sec. 4.3),
+and the q = p special case."""
+
+import numpy as np
+import pytest
+from scipy import special, stats
+
+from oracle.kl import KIND_CE, KIND_FORWARD, KIND_REVERSE, kl_ref, log_softmax_t
+from paper_2606_12370_amd import workloads as W
+
+KINDS = [KIND_FORWARD, KIND_CE, KIND_REVERSE]
+
+
+def _rows(seed, N=3, K=2, V=40, noise=1.0):
+    rng = np.random.default_rng(seed)
+    zt = rng.normal(0, 2, size=(N, K, V))
+    zd = zt + rng.normal(0, noise, size=(N, K, V))
+    return zt, zd
+
+
+def test_log_softmax_matches_scipy():
+    zt, _ = _rows(0)
+    for T in (0.7, 1.3):
+        np.testing.assert_allclose(log_softmax_t(zt, T), special.log_softmax(zt / T, axis=-1), rtol=1e-13)
+    # shift invariance with logits far outside exp's range
+    np.testing.assert_allclose(log_softmax_t(zt + 1000.0, 0.5), special.log_softmax(zt / 0.5, axis=-1), rtol=1e-9)
+
+
+@pytest.mark.parametrize("T", [1.0, 0.6])
+def test_losses_against_scipy(T):
+    zt, zd = _rows(1)
+    fk = kl_ref(zt, zd, T, KIND_FORWARD)["per_step"]
+    ce = kl_ref(zt, zd, T, KIND_CE)["per_step"]
+    rk = kl_ref(zt, zd, T, KIND_REVERSE)["per_step"]
+    for n in range(zt.shape[0]):
+        for k in range(zt.shape[1]):
+            p = special.softmax(zt[n, k] / T)
+            q = special.softmax(zd[n, k] / T)
+            np.testing.assert_allclose(fk[n, k], stats.entropy(p, q), rtol=1e-11)
+            np.testing.assert_allclose(fk[n, k], special.rel_entr(p, q).sum(), rtol=1e-11)
+            np.testing.assert_allclose(rk[n, k], stats.entropy(q, p), rtol=1e-11)
+            np.testing.assert_allclose(ce[n, k], -special.xlogy(p, q).sum(), rtol=1e-11)
+            np.testing.assert_allclose(ce[n, k], stats.entropy(p) + stats.entropy(p, q), rtol=1e-11)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("K,T", [(1, 1.0), (3, 0.7)])
+def test_gradient_matches_finite_differences(kind, K, T):
+    zt, zd = _rows(2, N=2, K=K, V=12)
+    scale = 1.7
+    out = kl_ref(zt, zd, T, kind, scale)
+    h = 1e-6
+    fd = np.zeros_like(zd)
+    for idx in np.ndindex(zd.shape):
+        zp = zd.copy(); zp[idx] += h
+        zm = zd.copy(); zm[idx] -= h
+        fd[idx] = (kl_ref(zt, zp, T, kind, scale)["loss"] - kl_ref(zt, zm, T, kind, scale)["loss"]) / (2 * h)
+    np.testing.assert_allclose(out["grad"], fd, rtol=1e-6, atol=1e-8)
+    # softmax is shift invariant: every gradient row sums to 0
+    np.testing.assert_allclose(out["grad"].sum(axis=-1), 0.0, atol=1e-13)
+
+
+def test_forward_and_ce_share_the_gradient_and_reduce_at_q_equals_p():
+    zt, zd = _rows(3)
+    a = kl_ref(zt, zd, 0.9, KIND_FORWARD)
+    b = kl_ref(zt, zd, 0.9, KIND_CE)
+    np.testing.assert_allclose(a["grad"], b["grad"], rtol=0, atol=0)
+    same = [kl_ref(zt, zt, 0.9, kind) for kind in KINDS]
+    np.testing.assert_allclose(same[0]["per_step"], 0.0, atol=1e-13)
+    np.testing.assert_allclose(same[2]["per_step"], 0.0, atol=1e-13)
+    H = np.array([[stats.entropy(special.softmax(zt[n, k] / 0.9)) for k in range(zt.shape[1])]
+                  for n in range(zt.shape[0])])
+    np.testing.assert_allclose(same[1]["per_step"], H, rtol=1e-12)
+    for s in same:
+        np.testing.assert_allclose(s["grad"], 0.0, atol=1e-15)
+
+
+def test_pinsker_bound():
+    """Sec. 4.3 (Eq. pinsker): d_TV(p, q) <= sqrt(KL(p||q) / 2)."""
+    zt, zd = _rows(4, N=50, K=1, V=30, noise=2.0)
+    kl = kl_ref(zt, zd, 1.0, KIND_FORWARD)["per_step"][:, 0]
+    p = special.softmax(zt[:, 0], axis=-1)
+    q = special.softmax(zd[:, 0], axis=-1)
+    tv = 0.5 * np.abs(p - q).sum(axis=-1)
+    assert np.all(tv <= np.sqrt(kl / 2) + 1e-15)
+
+
+def test_loss_reduction_and_zero_weights():
+    d = W.tv_inputs_numpy(5, 3, 64, W.F32, 6)
+    out = kl_ref(d["target"], d["draft"], 1.0, KIND_FORWARD, scale=0.5)
+    np.testing.assert_allclose(out["loss"], 0.5 * out["per_step"].mean(axis=1).sum(), rtol=1e-14)
+    # p_v = 0 contributes nothing to forward KL or CE; q_v = 0 nothing to reverse KL
+    zt = np.zeros((1, 1, 4)); zt[0, 0, 0] = -np.inf
+    zd = np.zeros((1, 1, 4)); zd[0, 0, 1] = -np.inf
+    f = kl_ref(zt, np.zeros((1, 1, 4)), 1.0, KIND_FORWARD)
+    r = kl_ref(np.zeros((1, 1, 4)), zd, 1.0, KIND_REVERSE)
+    assert np.isfinite(f["per_step"]).all() and np.isfinite(r["per_step"]).all()
+    assert np.all(np.isfinite(r["grad"]))
+    np.testing.assert_allclose(f["per_step"][0, 0], stats.entropy([0, 1 / 3, 1 / 3, 1 / 3], [0.25] * 4), rtol=1e-13)
