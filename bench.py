@@ -16,9 +16,10 @@ the same workload.  The fused TV-loss forward+backward on the training
 workload (N=16384 positions x 3 steps) is timed too and reported under
 `tv_loss`; target-only verification, the draft-stage sampler (the B*K draft
 rows) and the per-step diagnostics on the same batch under `target_only`,
-`sample` and `diagnostics`, and the Gumbel-max variants of verification and
-sampling under `verify_gumbel` and `sample_gumbel` (none of them part of
-`value`).
+`sample` and `diagnostics`, the Gumbel-max variants of verification and
+sampling under `verify_gumbel` and `sample_gumbel`, and the forward- and
+reverse-KL losses with gradients on the training workload under `kl_loss`
+(none of them part of `value`).
 """
 
 import argparse
@@ -206,6 +207,7 @@ def main():
     ap.add_argument("--no-variants", action="store_true",
                     help="skip target-only verification, the sampler and the diagnostics")
     ap.add_argument("--variant-steps", type=int, default=20)
+    ap.add_argument("--no-kl", action="store_true", help="skip the CE / KL loss legs")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
@@ -302,7 +304,8 @@ def main():
         log("generating TV inputs N=%d K=%d V=%d bf16" % (N, KT, VT))
         td = W.tv_inputs_torch(N, KT, VT, W.BF16, tcfg["seed"])
         grad = torch.empty((N, KT, VT), dtype=torch.float32, device=dev)
-        tws = binding.workspace(binding.tv_workspace_size(N, KT, VT, torch.bfloat16), dev)
+        tws = binding.workspace(max(binding.tv_workspace_size(N, KT, VT, torch.bfloat16),
+                                    binding.kl_workspace_size(N, KT, VT, torch.bfloat16)), dev)
         binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
         torch.cuda.synchronize()
         ev0.record(stream)
@@ -321,6 +324,22 @@ def main():
                          "frac": tv_ach / HBM_PEAK_GBS,
                          "traffic": measured_traffic("tv_bf16_n16384_k3_v151936", tv_bytes)},
         }
+        if not args.no_kl:
+            # the baselines the TV loss is compared against, on the same workload
+            result["kl_loss"] = {}
+            for kind in ("forward", "reverse"):
+                binding.kl_loss_fwd_bwd(td["target"], td["draft"], 1.0, kind, 1.0, ws=tws, grad_out=grad)
+                torch.cuda.synchronize()
+                ev0.record(stream)
+                for _ in range(args.tv_steps):
+                    binding.kl_loss_fwd_bwd(td["target"], td["draft"], 1.0, kind, 1.0, ws=tws, grad_out=grad)
+                ev1.record(stream)
+                torch.cuda.synchronize()
+                kl_ms = ev0.elapsed_time(ev1) / args.tv_steps
+                result["kl_loss"][kind] = {
+                    "workload": "tv_bf16_n16384_k3_v151936", "ms_per_call": kl_ms,
+                    "positions_per_s": N / (kl_ms * 1e-3),
+                    "roofline": hbm_roofline(tv_bytes, kl_ms, "kl_%s_bf16_n16384_k3_v151936" % kind)}
         del td, grad
         torch.cuda.empty_cache()
 

@@ -9,7 +9,9 @@
  * define the TV loss, its gradient and the end-to-end multi-step TV loss.
  * Sec. 2.2 (Eq. target_only) defines target-only verification, App. G.1 the
  * draft-stage sampler, Sec. 3 and App. E the acceptance diagnostics, App. G.2
- * (Alg. rs_gumbel) Gumbel-max verification and the Gumbel-max draft sampler.
+ * (Alg. rs_gumbel) Gumbel-max verification and the Gumbel-max draft sampler;
+ * Sec. 4.1 (footnote), Table grad_comparison, App. B and App. C the CE and KL
+ * objectives the TV loss is compared against.
  *
  * Conventions shared by every entry point
  *  - All tensor pointers are DEVICE pointers owned by the caller.  The
@@ -30,7 +32,8 @@
  *  - Each call is a short fixed sequence of kernel launches on `stream`
  *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a gradient,
  *    spec_verify_target_only: 2, spec_sample: 2, spec_diagnostics: 4,
- *    spec_verify_gumbel: 4, or 3 without overlaps, spec_sample_gumbel: 2); no
+ *    spec_verify_gumbel: 4, or 3 without overlaps, spec_sample_gumbel: 2,
+ *    spec_kl_loss_fwd_bwd: 5, or 6 for reverse KL with a gradient); no
  *    launch waits on another workgroup, so any number of resident
  *    workgroups is enough.
  *  - Entry points are thread-safe; each call is independent.
@@ -318,6 +321,41 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
                              const float* temperature, float temperature_scalar,
                              float* diag, int32_t* greedy_draft, int32_t* rs_preferred,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+typedef enum {
+  SPEC_KL_FORWARD = 0, /* sum_v p_v log(p_v / q_v)   (App. B)                     */
+  SPEC_KL_CE = 1,      /* -sum_v p_v log q_v        (= H(p) + forward KL)         */
+  SPEC_KL_REVERSE = 2  /* sum_v q_v log(q_v / p_v)   (App. C)                     */
+} spec_kl_kind;
+
+/* Bytes of workspace spec_kl_loss_fwd_bwd needs (0 on invalid sizes). */
+size_t spec_kl_workspace_size(int N, int K, int V, spec_dtype dtype);
+
+/*
+ * spec_kl_loss_fwd_bwd — the CE / forward-KL / reverse-KL objectives of the
+ * draft against the (detached) target, the baselines of the TV loss (Sec.
+ * 4.1 footnote, Table grad_comparison, App. B, App. C), and their gradients
+ * w.r.t. the draft logits.
+ *
+ * For position n and draft step k, p = softmax(target[n, k] / T),
+ * q = softmax(draft[n, k] / T), L_{n,k} by `kind` (terms with zero weight are 0):
+ *   forward KL / CE:  grad = scale * (1/K) * (1/T) * (q - p)
+ *   reverse KL:       grad = scale * (1/K) * (1/T) * q * (log q - log p - L_{n,k})
+ *   loss = scale * sum_n (1/K) sum_k L_{n,k}
+ * target_logits, draft_logits  [N, K, V], element strides (stride_n, stride_k)
+ * temperature    finite and > 0
+ * loss           [1] float32 out (device)
+ * per_step       [N, K] float32 out: L_{n,k} (may be NULL)
+ * grad_draft     [N, K, V] float32 out, contiguous; NULL = forward only
+ * NaN or infinite logits propagate into that position's loss and gradient.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= N, N*K < 2^31.
+ */
+spec_status spec_kl_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,
+                                 const void* draft_logits, int64_t d_stride_n, int64_t d_stride_k,
+                                 spec_dtype dtype, int N, int K, int V,
+                                 float temperature, spec_kl_kind kind, float scale,
+                                 float* loss, float* per_step, float* grad_draft,
+                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* spec_status_string(spec_status s);

@@ -43,6 +43,8 @@ TO_ARGTYPES = [_P, _I64, _I64, _I, _I, _I, _I, _P, _P, _F, _U64, _U64, _P, _P, _
 SAMPLE_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _P, _SZ, _P]
 SAMPLE_GUMBEL_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _SZ, _P]
 DIAG_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _P, _F, _P, _P, _P, _P, _SZ, _P]
+KL_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _SZ, _P]
+KL_KINDS = {"forward": 0, "ce": 1, "reverse": 2}
 DIAG_COLUMNS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")
 
 
@@ -97,6 +99,10 @@ def load_library():
         lib.spec_sample_gumbel_workspace_size.argtypes = [_I, _I, _I]
         lib.spec_sample_gumbel.restype = _I
         lib.spec_sample_gumbel.argtypes = SAMPLE_GUMBEL_ARGTYPES
+        lib.spec_kl_workspace_size.restype = _SZ
+        lib.spec_kl_workspace_size.argtypes = [_I, _I, _I, _I]
+        lib.spec_kl_loss_fwd_bwd.restype = _I
+        lib.spec_kl_loss_fwd_bwd.argtypes = KL_ARGTYPES
         _lib = lib
         return lib
 
@@ -125,6 +131,11 @@ def verify_gumbel_workspace_size(B, K, V, dtype=torch.bfloat16):
 def sample_gumbel_workspace_size(R, V, dtype=torch.bfloat16):
     code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
     return int(load_library().spec_sample_gumbel_workspace_size(R, V, code))
+
+
+def kl_workspace_size(N, K, V, dtype=torch.bfloat16):
+    code = SPEC_BF16 if dtype == torch.bfloat16 else SPEC_F32
+    return int(load_library().spec_kl_workspace_size(N, K, V, code))
 
 
 def verify_workspace_size(B, K, V, dtype=torch.bfloat16):
@@ -430,3 +441,40 @@ def sample_gumbel(logits, temperature=1.0, seed=0, offset=0, ws=None, out=None):
     if st != 0:
         raise SpecError("spec_sample_gumbel", st)
     return out
+
+
+def kl_loss_fwd_bwd(target_logits, draft_logits, temperature=1.0, kind="forward", scale=1.0, want_grad=True,
+                    want_per_step=True, ws=None, grad_out=None):
+    """CE / forward-KL / reverse-KL loss and gradient (spec_kl_loss_fwd_bwd).
+
+    target_logits, draft_logits [N, K, V] (bf16 or f32); kind in KL_KINDS.
+    Returns (loss [1], per_step [N, K] or None, grad [N, K, V] or None).
+    """
+    lib = load_library()
+    N, K, V = target_logits.shape
+    _check_rows(target_logits, "target_logits", (N, K, V))
+    _check_rows(draft_logits, "draft_logits", (N, K, V))
+    if draft_logits.dtype != target_logits.dtype:
+        raise TypeError("target and draft logits must share a dtype")
+    dev = target_logits.device
+    code = _dtype_code(target_logits)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    per_step = torch.empty((N, K), dtype=torch.float32, device=dev) if want_per_step else None
+    grad = None
+    if want_grad:
+        grad = grad_out if grad_out is not None else torch.empty((N, K, V), dtype=torch.float32, device=dev)
+        if not grad.is_contiguous() or tuple(grad.shape) != (N, K, V) or grad.dtype != torch.float32:
+            raise ValueError("grad_out must be a contiguous float32 [N, K, V] tensor")
+    need = int(lib.spec_kl_workspace_size(N, K, V, code))
+    if need == 0:
+        raise ValueError("unsupported KL shape N=%d K=%d V=%d" % (N, K, V))
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib.spec_kl_loss_fwd_bwd(
+        _ptr(target_logits), target_logits.stride(0), target_logits.stride(1),
+        _ptr(draft_logits), draft_logits.stride(0), draft_logits.stride(1),
+        code, N, K, V, float(temperature), KL_KINDS[kind] if isinstance(kind, str) else int(kind), float(scale),
+        _ptr(loss), _ptr(per_step), _ptr(grad), _ptr(ws), ws.numel(), _stream(dev))
+    if st != 0:
+        raise SpecError("spec_kl_loss_fwd_bwd", st)
+    return loss, per_step, grad

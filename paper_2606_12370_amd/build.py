@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libspecverify.so")
 ARCH = "gfx950"
 
 SOURCES = ["specverify.hip"]
-HEADERS = ["sv_device.h", "verify_kernel.h", "tv_kernel.h", "variants_kernel.h", "gumbel_kernel.h"]
+HEADERS = ["sv_device.h", "verify_kernel.h", "tv_kernel.h", "variants_kernel.h", "gumbel_kernel.h", "kl_kernel.h"]
 
 
 def hipcc():

@@ -13,6 +13,7 @@
 #include "specverify.h"
 #include "sv_device.h"
 #include "gumbel_kernel.h"
+#include "kl_kernel.h"
 #include "tv_kernel.h"
 #include "variants_kernel.h"
 #include "verify_kernel.h"
@@ -105,6 +106,23 @@ TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
   // indicator bits 1[q <= p] for the gradient pass: one 64-bit word per thread and chunk
   L.bits_stride = C * sv::kChunkWords * sizeof(uint64_t);
   L.bits = off; off = align_up(off + static_cast<size_t>(N) * K * L.bits_stride, 256);
+  L.total = off;
+  return L;
+}
+
+struct KlLayout {
+  size_t stats = 0, norms = 0, parts = 0, coef = 0, loss = 0, total = 0;
+};
+KlLayout kl_layout(int N, int K, int V, spec_dtype dt) {
+  KlLayout L;
+  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t rows = static_cast<size_t>(N) * 2 * K;
+  size_t off = 0;
+  L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
+  L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
+  L.parts = off; off = align_up(off + static_cast<size_t>(N) * K * C * sizeof(sv::KlPart), 256);
+  L.coef = off; off = align_up(off + static_cast<size_t>(N) * K * sizeof(float2), 256);
+  L.loss = off; off = align_up(off + static_cast<size_t>(N) * sizeof(double), 256);
   L.total = off;
   return L;
 }
@@ -250,6 +268,39 @@ spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
   }
   hipLaunchKernelGGL(sv::tv_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT, int KIND>
+spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
+  const int64_t units = int64_t{a.N} * a.K;
+  const int C = a.rows.C;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(2 * units * C)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), 2 * units * C);
+  hipLaunchKernelGGL(sv::row_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C,
+                     const_cast<sv::RowNorm*>(a.norms));
+  // the passes that may write the gradient read bf16 as 4-element vectors: one float4 store per lane
+  using G = typename GradElem<E>::type;
+  constexpr int NTG = kChunkElems / (sv::kThreads * G::EPV);
+  void (*kp)(sv::KlArgs, int64_t) = sv::kl_pass_kernel<G, NTG, kStep, KIND>;
+  hipLaunchKernelGGL(kp, dim3(grid_for(reinterpret_cast<const void*>(kp), units * C)), dim3(sv::kThreads), 0, s, a,
+                     units * C);
+  hipLaunchKernelGGL(sv::kl_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, a);
+  if (KIND == sv::kKlReverse && a.grad) {
+    void (*kg)(sv::KlArgs, int64_t) = sv::kl_grad_kernel<G, NTG, kStep>;
+    hipLaunchKernelGGL(kg, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a, units * C);
+  }
+  hipLaunchKernelGGL(sv::kl_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E, int NT>
+spec_status launch_kl_kind(const sv::KlArgs& a, hipStream_t s) {
+  if (a.kind == sv::kKlForward) return launch_kl<E, NT, sv::kKlForward>(a, s);
+  if (a.kind == sv::kKlCe) return launch_kl<E, NT, sv::kKlCe>(a, s);
+  return launch_kl<E, NT, sv::kKlReverse>(a, s);
 }
 
 template <class E, int NT>
@@ -604,6 +655,55 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
   a.pairs = reinterpret_cast<sv::DiagPair*>(ws + L.pairs);
   hipStream_t s = static_cast<hipStream_t>(stream);
   return dtype == SPEC_BF16 ? launch_diag<BF16, kNtBf16>(a, s) : launch_diag<F32, kNtF32>(a, s);
+}
+
+size_t spec_kl_workspace_size(int N, int K, int V, spec_dtype dtype) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
+  if (!tv_sizes_ok(N, K, V, dtype)) return 0;
+  return kl_layout(N, K, V, dtype).total;
+}
+
+spec_status spec_kl_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,
+                                 const void* draft_logits, int64_t d_stride_n, int64_t d_stride_k,
+                                 spec_dtype dtype, int N, int K, int V, float temperature, spec_kl_kind kind,
+                                 float scale, float* loss, float* per_step, float* grad_draft, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
+  if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
+  if (!tv_sizes_ok(N, K, V, dtype)) return SPEC_EINVAL;
+  if (!target_logits || !draft_logits || !loss) return SPEC_EINVAL;
+  if (t_stride_n < 0 || t_stride_k < 0 || d_stride_n < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!(temperature > 0.f && std::isfinite(temperature))) return SPEC_EINVAL;
+  if (kind != SPEC_KL_FORWARD && kind != SPEC_KL_CE && kind != SPEC_KL_REVERSE) return SPEC_EINVAL;
+  if (!std::isfinite(scale)) return SPEC_EINVAL;
+  const KlLayout L = kl_layout(N, K, V, dtype);
+  if (!workspace || workspace_bytes < L.total) return SPEC_EWORKSPACE;
+  if (!aligned16(workspace)) return SPEC_EINVAL;
+
+  const Geometry g = geometry(V, dtype);
+  const size_t es = esize_of(dtype);
+  sv::KlArgs a{};
+  a.rows.tgt = target_logits; a.rows.tsb = t_stride_n; a.rows.tsk = t_stride_k; a.rows.tper = K;
+  a.rows.drf = draft_logits; a.rows.dsb = d_stride_n; a.rows.dsk = d_stride_k; a.rows.dper = K;
+  a.rows.nb = N;
+  a.rows.temp = nullptr; a.rows.temp_scalar = temperature;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_n, t_stride_k, es) ? 1 : 0;
+  a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_n, d_stride_k, es) ? 1 : 0;
+  a.N = N; a.K = K;
+  a.kind = static_cast<int>(kind);
+  a.scale = static_cast<double>(scale);
+  a.inv_t = 1.0f / temperature;
+  a.loss = loss; a.per_step = per_step; a.grad = grad_draft;
+  char* ws = static_cast<char*>(workspace);
+  a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
+  a.norms = reinterpret_cast<const sv::RowNorm*>(ws + L.norms);
+  a.parts = reinterpret_cast<sv::KlPart*>(ws + L.parts);
+  a.coef = reinterpret_cast<float2*>(ws + L.coef);
+  a.loss_pos = reinterpret_cast<double*>(ws + L.loss);
+  a.vec_g = (grad_draft && aligned16(grad_draft) && (V % 4 == 0)) ? 1 : 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_kl_kind<BF16, kNtBf16>(a, s) : launch_kl_kind<F32, kNtF32>(a, s);
 }
 
 }  // extern "C"

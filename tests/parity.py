@@ -312,3 +312,38 @@ def compare_sample_gumbel(tokens, ref, rows=None):
         assert gap <= lim, "row %d: gpu %d, oracle %d, score gap %.3e > %.3e" % (r, g, o, gap, lim)
         boundary += 1
     return {"rows": int(len(tok)), "boundary_rows": boundary}
+
+
+KL_ABS = 1e-6
+
+
+def compare_kl(loss_g, ps_g, grad_g, ref, dtype, positions=None, loss_exact=True):
+    """CE / KL losses: per-step values and the total within tol * |L| + KL_ABS
+    (the absolute term covers the float32 rounding of the log-ratios, about
+    1e-7 of the log partition functions, which no longer cancels when the two
+    distributions nearly coincide); the gradient norm-wise per (position,
+    step) row within tol."""
+    tol = TOL[dtype]
+    out = {}
+    if ps_g is not None:
+        ps = ps_g.cpu().numpy().astype(np.float64)
+        if positions is not None:
+            ps = ps[positions]
+        e = np.abs(ps - ref["per_step"]) - tol * np.abs(ref["per_step"])
+        assert np.all(e <= KL_ABS), "per-step loss error beyond tolerance: %.3e" % e.max()
+        out["max_rel_per_step"] = float((np.abs(ps - ref["per_step"]) / np.maximum(np.abs(ref["per_step"]), 1e-30)).max())
+    if loss_exact:
+        lg = float(loss_g.cpu().numpy()[0])
+        assert abs(lg - ref["loss"]) <= tol * abs(ref["loss"]) + KL_ABS * ref["per_step"].size, (lg, ref["loss"])
+        out["rel_loss"] = abs(lg - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
+    if grad_g is not None:
+        g = grad_g
+        if positions is not None:
+            g = g[torch.as_tensor(positions, device=g.device)]
+        g = g.cpu().numpy().astype(np.float64)
+        gr = ref["grad"]
+        scale = np.maximum(np.abs(gr).max(axis=-1), 1e-300)
+        worst = float((np.abs(g - gr).max(axis=-1) / scale).max())
+        assert worst <= tol, "gradient norm-wise relative error %.3e" % worst
+        out["max_normwise_grad"] = worst
+    return out

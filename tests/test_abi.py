@@ -38,7 +38,8 @@ def test_exports_every_declared_function(lib):
                            "spec_sample_workspace_size", "spec_sample",
                            "spec_diagnostics_workspace_size", "spec_diagnostics",
                            "spec_verify_gumbel_workspace_size", "spec_verify_gumbel",
-                           "spec_sample_gumbel_workspace_size", "spec_sample_gumbel"}
+                           "spec_sample_gumbel_workspace_size", "spec_sample_gumbel",
+                           "spec_kl_workspace_size", "spec_kl_loss_fwd_bwd"}
     for name in protos:
         assert hasattr(lib, name), name
 
@@ -53,6 +54,7 @@ def test_ctypes_prototypes_match_header():
     assert len(protos["spec_verify_gumbel"]) == len(binding.VERIFY_ARGTYPES)
     assert protos["spec_verify_gumbel"] == protos["spec_verify"]
     assert len(protos["spec_sample_gumbel"]) == len(binding.SAMPLE_GUMBEL_ARGTYPES)
+    assert len(protos["spec_kl_loss_fwd_bwd"]) == len(binding.KL_ARGTYPES)
 
 
 def test_diag_columns_match_header():
@@ -98,6 +100,8 @@ def test_workspace_sizes(lib):
     assert lib.spec_verify_gumbel_workspace_size(256, 9, 151936, 1) == 0
     assert lib.spec_sample_gumbel_workspace_size(768, 151936, 1) == 768 * 10 * 16
     assert lib.spec_sample_gumbel_workspace_size(0, 151936, 1) == 0
+    assert lib.spec_kl_workspace_size(16384, 3, 151936, 1) > 0
+    assert lib.spec_kl_workspace_size(16384, 9, 151936, 1) == 0
 
 
 FAKE = 0x10000  # never dereferenced: every call below fails validation first
@@ -285,3 +289,28 @@ def test_sample_gumbel_argument_errors(lib, kw, status):
     args.update(kw)
     assert lib.spec_sample_gumbel(*[args[k] for k in ("z", "sr", "dtype", "R", "V", "temp", "temp_s", "seed", "off",
                                                       "tok", "ws", "wsb", "stream")]) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=3), 2),
+    (dict(K=9), 2),
+    (dict(N=0), 1),
+    (dict(V=-5), 1),
+    (dict(t=None), 1),
+    (dict(loss=None), 1),
+    (dict(T=0.0), 1),
+    (dict(T=float("inf")), 1),
+    (dict(kind=3), 1),
+    (dict(kind=-1), 1),
+    (dict(scale=float("nan")), 1),
+    (dict(dsk=-1), 1),
+    (dict(ws=None), 4),
+    (dict(wsb=100), 4),
+])
+def test_kl_argument_errors(lib, kw, status):
+    args = dict(t=FAKE, tsn=300, tsk=100, d=FAKE, dsn=300, dsk=100, dtype=1, N=4, K=3, V=100, T=1.0, kind=0,
+                scale=1.0, loss=FAKE, ps=None, grad=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    assert lib.spec_kl_loss_fwd_bwd(*[args[k] for k in ("t", "tsn", "tsk", "d", "dsn", "dsk", "dtype", "N", "K", "V",
+                                                        "T", "kind", "scale", "loss", "ps", "grad", "ws", "wsb",
+                                                        "stream")]) == status

@@ -1,0 +1,99 @@
+"""GPU parity of spec_kl_loss_fwd_bwd (CE, forward KL, reverse KL and their
+gradients) against the float64 oracle, through the C ABI."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.kl import KIND_CE, KIND_FORWARD, KIND_REVERSE, kl_ref
+from paper_2606_12370_amd import binding
+from paper_2606_12370_amd import workloads as W
+from tests.parity import compare_kl, device_inputs, host_logits
+
+pytestmark = pytest.mark.gpu
+KINDS = {"forward": KIND_FORWARD, "ce": KIND_CE, "reverse": KIND_REVERSE}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    binding.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def run_case(d, kind, T=1.0, scale=1.0, want_grad=True):
+    tgt, drf = device_inputs(d)
+    loss, ps, grad = binding.kl_loss_fwd_bwd(tgt, drf, T, kind, scale, want_grad=want_grad)
+    torch.cuda.synchronize()
+    ref = kl_ref(W.to_float64(d["target"], d["dtype"]), W.to_float64(d["draft"], d["dtype"]), float(np.float32(T)),
+                 KINDS[kind], float(np.float32(scale)))
+    return loss, ps, grad, ref
+
+
+@pytest.mark.parametrize("kind", ["forward", "ce", "reverse"])
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("T", [1.0, 0.7])
+def test_small_all_kinds(kind, dtype, T):
+    d = W.tv_inputs_numpy(4, 3, 5000, dtype, 3)
+    loss, ps, grad, ref = run_case(d, kind, T, scale=0.5)
+    print(kind, dtype, T, compare_kl(loss, ps, grad, ref, dtype))
+
+
+@pytest.mark.parametrize("kind", ["forward", "reverse"])
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("N,K,V", [(3, 1, 1), (2, 2, 7), (3, 3, 1023), (2, 8, 8197), (5, 2, 20480 + 3),
+                                   (1, 1, 256 * 8192 + 8195)])
+def test_ragged(kind, dtype, N, K, V):
+    d = W.tv_inputs_numpy(N, K, V, dtype, 13 + V)
+    loss, ps, grad, ref = run_case(d, kind)
+    print(kind, dtype, N, K, V, compare_kl(loss, ps, grad, ref, dtype))
+
+
+@pytest.mark.parametrize("noise", [0.05, 0.3])
+def test_nearly_equal_distributions(noise):
+    """Small KL: the self-normalised sums keep it accurate."""
+    d = W.tv_inputs_numpy(4, 2, 60000, W.F32, 21, noise=noise)
+    for kind in ("forward", "reverse", "ce"):
+        loss, ps, grad, ref = run_case(d, kind)
+        rep = compare_kl(loss, ps, grad, ref, W.F32)
+        print(kind, noise, rep, "min KL", float(ref["per_step"].min()))
+
+
+def test_forward_only_q_equals_p_and_determinism():
+    d = W.tv_inputs_numpy(6, 3, 30000, W.BF16, 4)
+    loss, ps, grad, ref = run_case(d, "ce", want_grad=False)
+    assert grad is None
+    compare_kl(loss, ps, None, ref, W.BF16)
+    d = W.tv_inputs_numpy(3, 2, 30000, W.F32, 5, q_equals_p=True)
+    for kind in ("forward", "reverse"):
+        loss, ps, grad, ref = run_case(d, kind)
+        assert float(ps.abs().max()) < 1e-6
+        assert float(grad.abs().max()) < 1e-7
+    tgt, drf = device_inputs(W.tv_inputs_numpy(8, 3, 40000, W.BF16, 6))
+    a = binding.kl_loss_fwd_bwd(tgt, drf, 0.9, "reverse", 0.25)
+    b = binding.kl_loss_fwd_bwd(tgt, drf, 0.9, "reverse", 0.25)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_training_workload_sampled_positions():
+    """N=16384 positions x 3 steps x V=151936 (bf16), forward KL (CE's
+    gradient): sampled positions against the oracle, the total loss against
+    the float64 sum of the kernel's own per-step values."""
+    cfg = W.CONFIGS["tv_bf16_n16384_k3_v151936"]
+    d = W.tv_inputs_torch(cfg["N"], cfg["K"], cfg["V"], cfg["dtype"], cfg["seed"])
+    for kind in ("forward", "reverse"):
+        loss, ps, grad = binding.kl_loss_fwd_bwd(d["target"], d["draft"], 1.0, kind, 1.0)
+        torch.cuda.synchronize()
+        pos = np.sort(np.random.default_rng(cfg["seed"]).choice(cfg["N"], size=4, replace=False))
+        pi = torch.as_tensor(pos, device="cuda")
+        ref = kl_ref(host_logits(d["target"][pi], W.BF16), host_logits(d["draft"][pi], W.BF16), 1.0, KINDS[kind])
+        rep = compare_kl(loss, ps, grad, ref, W.BF16, positions=pos, loss_exact=False)
+        total = ps.cpu().numpy().astype(np.float64).mean(axis=1).sum()
+        lg = float(loss.cpu().numpy()[0])
+        assert abs(lg - total) <= 1e-5 * abs(total)
+        print(kind, "training workload", rep, "loss", lg)
+        del grad
+        torch.cuda.empty_cache()
