@@ -28,6 +28,11 @@ using sv::F32;
 constexpr int kNtBf16 = 8;
 constexpr int kNtF32 = 16;
 constexpr int kStep = 4;
+// Multinomial verification streams longer tasks (32768 elements: 16 bf16 or
+// 32 fp32 tiles) and keeps statistics per sub-chunk of kStep tiles, which is
+// what its finish re-reads.
+constexpr int kTaskBf16 = 16;
+constexpr int kTaskF32 = 32;
 constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
 static_assert(kNtF32 * sv::kThreads * sv::F32::EPV == kChunkElems, "chunk geometry");
@@ -55,10 +60,13 @@ Geometry geometry(int V, spec_dtype dt) {
   return g;
 }
 
+// Sub-chunks of kStep tiles per row (the statistics granularity of multinomial verification).
+int sub_chunks(int V, spec_dtype dt) { return (geometry(V, dt).ntiles + kStep - 1) / kStep; }
+
 bool verify_sizes_ok(int B, int K, int V, spec_dtype dt) {
   if (B < 1 || K < 1 || K > SPEC_MAX_K || V < 1) return false;
   const int64_t rows = static_cast<int64_t>(B) * (2 * K + 1);
-  return rows * geometry(V, dt).C < (int64_t{1} << 31);
+  return rows * sub_chunks(V, dt) < (int64_t{1} << 31);
 }
 
 bool tv_sizes_ok(int N, int K, int V, spec_dtype dt) {
@@ -76,7 +84,7 @@ struct VerifyLayout {
 };
 VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt, bool gumbel = false) {
   VerifyLayout L;
-  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t C = static_cast<size_t>(gumbel ? geometry(V, dt).C : sub_chunks(V, dt));
   const size_t rows = static_cast<size_t>(B) * (2 * K + 1);
   size_t off = 0;
   L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
@@ -195,20 +203,22 @@ unsigned grid_for(const void* kernel, int64_t tasks) {
   return static_cast<unsigned>((r > 0 && r < tasks) ? r : tasks);
 }
 
-template <class E, int NT>
+template <class E, int NTT>
 spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) {
-  const int C = a.rows.C;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  // tasks of NTT tiles; statistics and pair sums per sub-chunk of kStep tiles
+  const int ct = (a.rows.ntiles + NTT - 1) / NTT;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int, int64_t) = sv::row_stats_sub_kernel<E, NTT, kStep>;
   // one workgroup per task: measured faster for this first, purely streaming pass
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(rows * C)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), rows * C);
+  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(rows * ct)), dim3(sv::kThreads), 0, s, a.rows,
+                     const_cast<sv::RowStat*>(a.stats), ct, rows * ct);
   hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
-  void (*pp)(sv::VerifyArgs, int64_t) = sv::pair_pass_kernel<E, NT, kStep>;
-  const int64_t pairs = int64_t{a.B} * a.K * C;
-  hipLaunchKernelGGL(pp, dim3(grid_for(reinterpret_cast<const void*>(pp), pairs)), dim3(sv::kThreads), 0, s, a,
+  void (*pp)(sv::VerifyArgs, int, int64_t) = sv::pair_pass_sub_kernel<E, NTT, kStep>;
+  const int64_t pairs = int64_t{a.B} * a.K * ct;
+  hipLaunchKernelGGL(pp, dim3(grid_for(reinterpret_cast<const void*>(pp), pairs)), dim3(sv::kThreads), 0, s, a, ct,
                      pairs);
-  hipLaunchKernelGGL((sv::finish_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s,
-                     a);
+  // the finish inverts the CDF inside one sub-chunk (kStep tiles, one load step)
+  hipLaunchKernelGGL((sv::finish_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
+                     s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
@@ -369,7 +379,7 @@ spec_status prepare_verify(const void* target_logits, int64_t t_stride_b, int64_
   a.rows.drf = draft_logits; a.rows.dsb = d_stride_b; a.rows.dsk = d_stride_k; a.rows.dper = K;
   a.rows.nb = B;
   a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
-  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = gumbel ? g.C : sub_chunks(V, dtype);
   a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, es) ? 1 : 0;
   a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_b, d_stride_k, es) ? 1 : 0;
   a.B = B; a.K = K;
@@ -435,7 +445,7 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
   if (st != SPEC_OK) return st;
   const int64_t rows = int64_t{B} * (2 * K + 1);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_verify<BF16, kNtBf16>(a, rows, s) : launch_verify<F32, kNtF32>(a, rows, s);
+  return dtype == SPEC_BF16 ? launch_verify<BF16, kTaskBf16>(a, rows, s) : launch_verify<F32, kTaskF32>(a, rows, s);
 }
 
 size_t spec_verify_gumbel_workspace_size(int B, int K, int V, spec_dtype dtype) {

@@ -425,4 +425,74 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat
   }
 }
 
+// Statistics at sub-chunk granularity: a task streams NT tiles of a row (a
+// long contiguous read per workgroup) and reports the statistics of each of
+// its NT/S sub-chunks of S tiles, one sub-chunk per load step, so that later
+// passes can select and re-read a short sub-chunk.  stats[r * Cs + c * NB + j]
+// holds sub-chunk j of task c of row r (Cs sub-chunks per row).
+template <class E, int NT, int S>
+__global__ __launch_bounds__(kThreads) void row_stats_sub_kernel(RowsDesc d, RowStat* __restrict__ stats, int ct,
+                                                                 int64_t ntasks) {
+  constexpr int EPV = E::EPV;
+  constexpr int NB = NT / S;
+  static_assert(NT % S == 0, "a task holds whole sub-chunks");
+  __shared__ RedLds<NB> red;
+  const int Cs = d.C;
+  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
+    const int r = static_cast<int>(t / ct), c = static_cast<int>(t - static_cast<int64_t>(t / ct) * ct);
+    int b;
+    bool aligned;
+    const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+    const float T = temperature_of(d, b);
+    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+    const int tile0 = c * NT;
+    const int nt = min(NT, d.ntiles - tile0);
+    float ref[NB], dsum[NB];
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) {
+      ref[jb] = -INFINITY;
+      dsum[jb] = 0.f;
+      if (jb * S >= nt) continue;
+      float x[S][EPV];
+      load_tiles<E, S>(row, tile0 + jb * S, d.V, aligned, x);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < S; ++j)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[j][k]);
+      if (mx != -INFINITY) {
+        const float rr = mx * s;
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < S; ++j)
+#pragma unroll
+          for (int k = 0; k < EPV; ++k) acc += __builtin_amdgcn_exp2f(fmaf(x[j][k], s, -rr));
+        ref[jb] = rr;
+        dsum[jb] = acc;
+      }
+    }
+    float m[NB];
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) m[jb] = ref[jb];
+    wg_max<NB>(m, red);
+    double dd[NB];
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) {
+      if (dsum[jb] != dsum[jb]) dd[jb] = dsum[jb];  // NaN propagates (data error)
+      else if (ref[jb] == -INFINITY) dd[jb] = 0.0;
+      else dd[jb] = static_cast<double>(dsum[jb]) * static_cast<double>(__builtin_amdgcn_exp2f(ref[jb] - m[jb]));
+    }
+    wg_sum<NB>(dd, red);
+    if (threadIdx.x == 0) {
+#pragma unroll
+      for (int jb = 0; jb < NB; ++jb) {
+        if (jb * S >= nt) break;
+        RowStat o;
+        o.m = m[jb]; o.pad = 0.f; o.D = dd[jb];
+        stats[static_cast<int64_t>(r) * Cs + c * NB + jb] = o;
+      }
+    }
+  }
+}
+
 }  // namespace sv

@@ -211,6 +211,98 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
   }
 }
 
+// The pair pass at sub-chunk granularity (pairs as row_stats_sub_kernel
+// lays out the statistics): a task streams NT tiles of a (target, draft)
+// pair and reports the overlap (and, at the first rejected step, the
+// residual mass) of each of its NT/S sub-chunks.
+template <class E, int NT, int S>
+__global__ __launch_bounds__(kThreads) void pair_pass_sub_kernel(VerifyArgs a, int ct, int64_t ntasks) {
+  constexpr int EPV = E::EPV;
+  constexpr int NB = NT / S;
+  __shared__ RedLds<2 * NB> red2;
+  __shared__ RedLds<NB> red1;
+  const RowsDesc& d = a.rows;
+  const int Cs = d.C;
+  // persistent: the grid is sized to what the device holds at once and
+  // strides over the (pair, task) items
+  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
+    const int u = static_cast<int>(t / ct), c = static_cast<int>(t - static_cast<int64_t>(t / ct) * ct);
+    const int b = u / a.K, i = u % a.K;
+    const int n = a.decision[b];
+    if (n < 0) continue;  // data error: finish ignores this row's partials
+    const bool need_z = a.want_z && i == n;
+    if (!need_z && a.overlap == nullptr) continue;  // no overlap requested: only the residual step is read again
+    const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
+    int bb;
+    bool al_t, al_d;
+    const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
+    const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
+    const float s = scale_of(temperature_of(d, b));
+    const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
+    const int tile0 = c * NT;
+    const int nt_tiles = min(NT, d.ntiles - tile0);
+    float al[NB], zr[NB];
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) {
+      al[jb] = 0.f;
+      zr[jb] = 0.f;
+      if (jb * S >= nt_tiles) continue;
+      float xt[S][EPV], xd[S][EPV];
+      load_tiles<E, S>(rt, tile0 + jb * S, d.V, al_t, xt);
+      load_tiles<E, S>(rd, tile0 + jb * S, d.V, al_d, xd);
+      if (need_z) {
+#pragma unroll
+        for (int j = 0; j < S; ++j)
+#pragma unroll
+          for (int k = 0; k < EPV; ++k) {
+            const float p = prob(xt[j][k], s, nt.M, nt.invD);
+            const float mn = fminf(p, prob(xd[j][k], s, nd.M, nd.invD));
+            al[jb] += mn;
+            zr[jb] += p - mn;
+          }
+      } else {
+#pragma unroll
+        for (int j = 0; j < S; ++j)
+#pragma unroll
+          for (int k = 0; k < EPV; ++k) al[jb] += min_prob(xt[j][k], xd[j][k], s, nt, nd);
+      }
+    }
+    PairStat* out = a.pairs + static_cast<int64_t>(u) * Cs + c * NB;
+    if (need_z) {
+      double v[2 * NB];
+#pragma unroll
+      for (int jb = 0; jb < NB; ++jb) {
+        v[jb] = static_cast<double>(al[jb]);
+        v[NB + jb] = static_cast<double>(zr[jb]);
+      }
+      wg_sum<2 * NB>(v, red2);
+      if (threadIdx.x == 0) {
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+          if (jb * S >= nt_tiles) break;
+          PairStat o;
+          o.alpha = v[jb]; o.Z = v[NB + jb];
+          out[jb] = o;
+        }
+      }
+    } else {
+      double v[NB];
+#pragma unroll
+      for (int jb = 0; jb < NB; ++jb) v[jb] = static_cast<double>(al[jb]);
+      wg_sum<NB>(v, red1);
+      if (threadIdx.x == 0) {
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+          if (jb * S >= nt_tiles) break;
+          PairStat o;
+          o.alpha = v[jb]; o.Z = 0.0;
+          out[jb] = o;
+        }
+      }
+    }
+  }
+}
+
 // Residual (or target) mass of the EPV elements of one thread's vector;
 // element `excl` (-1: none) has mass 0.
 template <class E>
