@@ -208,6 +208,7 @@ def main():
                     help="skip target-only verification, the sampler and the diagnostics")
     ap.add_argument("--variant-steps", type=int, default=20)
     ap.add_argument("--no-kl", action="store_true", help="skip the CE / KL loss legs")
+    ap.add_argument("--no-tv-loss", action="store_true", help="skip the TV loss leg (keeps the KL legs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
@@ -306,24 +307,25 @@ def main():
         grad = torch.empty((N, KT, VT), dtype=torch.float32, device=dev)
         tws = binding.workspace(max(binding.tv_workspace_size(N, KT, VT, torch.bfloat16),
                                     binding.kl_workspace_size(N, KT, VT, torch.bfloat16)), dev)
-        binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
-        torch.cuda.synchronize()
-        ev0.record(stream)
-        for _ in range(args.tv_steps):
-            binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        tv_ms = ev0.elapsed_time(ev1) / args.tv_steps
         # both logit tensors read once, the float32 gradient written once
         tv_bytes = N * KT * VT * (2 + 2 + 4) + N * KT * 4 + 4
-        tv_ach = tv_bytes / (tv_ms * 1e-3) / 1e9
-        result["tv_loss"] = {
-            "workload": "tv_bf16_n16384_k3_v151936", "mode": "prod", "ms_per_call": tv_ms,
-            "positions_per_s": N / (tv_ms * 1e-3),
-            "roofline": {"bound": "hbm", "achieved": tv_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": tv_ach / HBM_PEAK_GBS,
-                         "traffic": measured_traffic("tv_bf16_n16384_k3_v151936", tv_bytes)},
-        }
+        if not args.no_tv_loss:
+            binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            for _ in range(args.tv_steps):
+                binding.tv_loss_fwd_bwd(td["target"], td["draft"], 1.0, "prod", 1.0, ws=tws, grad_out=grad)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            tv_ms = ev0.elapsed_time(ev1) / args.tv_steps
+            tv_ach = tv_bytes / (tv_ms * 1e-3) / 1e9
+            result["tv_loss"] = {
+                "workload": "tv_bf16_n16384_k3_v151936", "mode": "prod", "ms_per_call": tv_ms,
+                "positions_per_s": N / (tv_ms * 1e-3),
+                "roofline": {"bound": "hbm", "achieved": tv_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": tv_ach / HBM_PEAK_GBS,
+                             "traffic": measured_traffic("tv_bf16_n16384_k3_v151936", tv_bytes)},
+            }
         if not args.no_kl:
             # the baselines the TV loss is compared against, on the same workload
             result["kl_loss"] = {}

@@ -452,7 +452,12 @@ __global__ __launch_bounds__(kThreads) void row_stats_sub_kernel(RowsDesc d, Row
     for (int jb = 0; jb < NB; ++jb) {
       ref[jb] = -INFINITY;
       dsum[jb] = 0.f;
-      if (jb * S >= nt) continue;
+    }
+    // one load step per sub-chunk; "break" (not "continue") keeps the next
+    // step's loads behind this step's work instead of all hoisted up front
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) {
+      if (jb * S >= nt) break;
       float x[S][EPV];
       load_tiles<E, S>(row, tile0 + jb * S, d.V, aligned, x);
       float mx = -INFINITY;

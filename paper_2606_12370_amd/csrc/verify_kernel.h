@@ -246,7 +246,10 @@ __global__ __launch_bounds__(kThreads) void pair_pass_sub_kernel(VerifyArgs a, i
     for (int jb = 0; jb < NB; ++jb) {
       al[jb] = 0.f;
       zr[jb] = 0.f;
-      if (jb * S >= nt_tiles) continue;
+    }
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) {
+      if (jb * S >= nt_tiles) break;
       float xt[S][EPV], xd[S][EPV];
       load_tiles<E, S>(rt, tile0 + jb * S, d.V, al_t, xt);
       load_tiles<E, S>(rd, tile0 + jb * S, d.V, al_d, xd);

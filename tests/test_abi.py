@@ -95,8 +95,12 @@ def test_workspace_sizes(lib):
     assert lib.spec_sample_workspace_size(4, 0, 0) == 0
     assert lib.spec_diagnostics_workspace_size(256, 3, 151936, 1) > 0
     assert lib.spec_diagnostics_workspace_size(256, 0, 151936, 1) == 0
-    # Gumbel-max: the verify workspace plus one 16-byte best key per (batch row, chunk)
-    assert lib.spec_verify_gumbel_workspace_size(256, 3, 151936, 1) >= b + 256 * 10 * 16
+    # multinomial verification keeps statistics per 8192-element sub-chunk (19 per bf16 row
+    # at V=151936); Gumbel-max verification per 16384-element chunk (10 per row) plus one
+    # 16-byte best key per (batch row, chunk)
+    assert b >= 256 * 7 * 19 * 16 + 256 * 3 * 19 * 16
+    g = lib.spec_verify_gumbel_workspace_size(256, 3, 151936, 1)
+    assert 256 * 7 * 10 * 16 + 256 * 3 * 10 * 16 + 256 * 10 * 16 <= g < b
     assert lib.spec_verify_gumbel_workspace_size(256, 9, 151936, 1) == 0
     assert lib.spec_sample_gumbel_workspace_size(768, 151936, 1) == 768 * 10 * 16
     assert lib.spec_sample_gumbel_workspace_size(0, 151936, 1) == 0
