@@ -56,13 +56,36 @@ struct DecideShared {
   int n;
 };
 
+// The draft token of step i and its target and draft logits, gathered by
+// lane i before the normalisers are known (the loads overlap the combine).
+struct DraftGather {
+  int x;
+  float zt, zd;
+};
+
+template <class E>
+__device__ __forceinline__ DraftGather gather_draft(const VerifyArgs& a, int b, int i) {
+  const RowsDesc& d = a.rows;
+  DraftGather g;
+  g.x = a.ids[static_cast<int64_t>(b) * a.K + i];
+  g.zt = 0.f;
+  g.zd = 0.f;
+  if (g.x >= 0 && g.x < d.V) {
+    int bb;
+    bool al;
+    g.zt = E::one(row_of<E>(d, target_row(a, b, i), &bb, &al) + g.x);
+    g.zd = E::one(row_of<E>(d, draft_row(a, b, i), &bb, &al) + g.x);
+  }
+  return g;
+}
+
 // Accept tests and every per-row output except the overlaps and emitted[n],
 // for batch row b whose 2K+1 row normalisers are in sh.nrm (`fail` forces a
-// row error).  Whole workgroup; returns the accept length n, or -1 for a row
-// with a data error (then every output of the row has been written).
+// row error); lane i < K holds step i's gathered token and logits.  Whole
+// workgroup; returns the accept length n, or -1 for a row with a data error
+// (then every output of the row has been written).
 template <class E>
-__device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& sh) {
-  using raw = typename E::raw;
+__device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& sh, const DraftGather& gx) {
   const RowsDesc& d = a.rows;
   const int K = a.K, V = d.V;
   const int tid = threadIdx.x;
@@ -72,7 +95,7 @@ __device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& s
   // accept tests in float64: u q(x) < p(x), no division; one lane per step
   if (tid < K) {
     const int i = tid;
-    const int x = a.ids[static_cast<int64_t>(b) * K + i];
+    const int x = gx.x;
     const RowNorm& nt = sh.nrm[i];
     const RowNorm& nd = sh.nrm[K + 1 + i];
     int ok = 0, bad = 1;
@@ -80,12 +103,8 @@ __device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& s
     if (x >= 0 && x < V) {
       bad = 0;
       if (t_ok && norm_ok(nt) && norm_ok(nd)) {
-        int bb;
-        bool al;
-        const raw* rt = row_of<E>(d, target_row(a, b, i), &bb, &al);
-        const raw* rd = row_of<E>(d, draft_row(a, b, i), &bb, &al);
-        p = exp2(static_cast<double>(E::one(rt + x)) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
-        q = exp2(static_cast<double>(E::one(rd + x)) * static_cast<double>(s) - static_cast<double>(nd.M)) / nd.D;
+        p = exp2(static_cast<double>(gx.zt) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
+        q = exp2(static_cast<double>(gx.zd) * static_cast<double>(s) - static_cast<double>(nd.M)) / nd.D;
         const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(i), a.offset, 0ull,
                                            a.seed, 0ull);
         ok = (u24(g.w[0]) * q < p) ? 1 : 0;
@@ -134,6 +153,8 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
   const int K = a.K, C = d.C;
   const int b = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  DraftGather gx{0, 0.f, 0.f};
+  if (static_cast<int>(threadIdx.x) < K) gx = gather_draft<E>(a, b, threadIdx.x);
   // row j < K+1: target row j; row K+1+i: draft row i (one wave per row)
   for (int j = wave; j < 2 * K + 1; j += kWaves) {
     const int r = j <= K ? target_row(a, b, j) : draft_row(a, b, j - K - 1);
@@ -147,7 +168,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
     }
   }
   __syncthreads();
-  const int n = decide_row<E>(a, b, false, sh);
+  const int n = decide_row<E>(a, b, false, sh, gx);
   if (threadIdx.x == 0) a.decision[b] = n;
 }
 
@@ -371,7 +392,8 @@ struct SampleShared {
 template <class E, int NT, int S>
 __device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
                                            bool al_d, bool residual, int excl, int c, int V, int ntiles, float s,
-                                           const RowNorm& nt, const RowNorm& nd, float (&tsum)[NT]) {
+                                           const RowNorm& nt, const RowNorm& nd, float (&tsum)[NT],
+                                           float (*keep)[S][E::EPV] = nullptr) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   const int tile0 = c * NT;
@@ -396,6 +418,7 @@ __device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t,
         float m = residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
         if (j0 + j == ex_tile && k == ex_k) m = 0.f;
         tsum[j0 + j] += m;
+        if (keep) (*keep)[j][k] = m;
       }
   }
   return nt_tiles;
@@ -415,7 +438,10 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
   const int tid = threadIdx.x;
   const int tile0 = cstar * NT;
   float tsum[NT];
-  const int nt_tiles = tile_masses<E, NT, S>(rt, al_t, rd, al_d, residual, excl, cstar, V, ntiles, s, nt, nd, tsum);
+  // a chunk of one load step keeps its element masses for the final scan
+  float keep[S][EPV];
+  const int nt_tiles = tile_masses<E, NT, S>(rt, al_t, rd, al_d, residual, excl, cstar, V, ntiles, s, nt, nd, tsum,
+                                             NT == S ? &keep : nullptr);
   double W[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) W[j] = (j < nt_tiles) ? static_cast<double>(tsum[j]) : 0.0;
@@ -450,7 +476,15 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
   if (tid == tstar) {
     const int v0 = (tile0 + jstar) * TILE + tid * EPV;
     float r[EPV];
-    vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+    if constexpr (NT == S) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+        if (j == jstar)
+#pragma unroll
+          for (int k = 0; k < EPV; ++k) r[k] = keep[j][k];
+    } else {
+      vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+    }
     const double tl = t_in - excl_sum;
     float cumf = 0.f;
     int kstar = -1, klast = -1;
