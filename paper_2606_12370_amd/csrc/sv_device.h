@@ -324,6 +324,37 @@ __device__ __forceinline__ void combine_row(const RowStat* __restrict__ st, int 
   *D = wave_sum(d);
 }
 
+// combine_row for two rows at once (one wave), both rows' loads issued before
+// either reduction; the sums run in combine_row's order, so each row gets the
+// same bits as combine_row would give it.
+__device__ __forceinline__ void combine_two_rows(const RowStat* __restrict__ s1, const RowStat* __restrict__ s2,
+                                                 int C, float* M1, double* D1, float* M2, double* D2) {
+  const int lane = threadIdx.x & 63;
+  if (C > 64) {
+    combine_row(s1, C, M1, D1);
+    combine_row(s2, C, M2, D2);
+    return;
+  }
+  RowStat a, b;
+  a.m = -INFINITY; a.D = 0.0; b.m = -INFINITY; b.D = 0.0;
+  if (lane < C) {
+    a = s1[lane];
+    b = s2[lane];
+  }
+  const float m1 = wave_max(a.m), m2 = wave_max(b.m);
+  double d1 = 0.0, d2 = 0.0;
+  if (lane < C) {
+    if (a.D != a.D) d1 += a.D;
+    else if (a.m != -INFINITY) d1 += a.D * static_cast<double>(__builtin_amdgcn_exp2f(a.m - m1));
+    if (b.D != b.D) d2 += b.D;
+    else if (b.m != -INFINITY) d2 += b.D * static_cast<double>(__builtin_amdgcn_exp2f(b.m - m2));
+  }
+  *M1 = m1;
+  *D1 = wave_sum(d1);
+  *M2 = m2;
+  *D2 = wave_sum(d2);
+}
+
 // A row's combined normaliser: p_v = 2^(z_v s - M) / D.
 struct RowNorm {
   float M;      // log2 units; +inf / NaN / -inf mark a bad row

@@ -123,26 +123,29 @@ __device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& s
       if (n == K && !sh.acc[i]) n = i;  // the first rejection ends the chain
     }
     a.accept_len[b] = err ? -1 : n;
-    int32_t* em = a.emitted + static_cast<int64_t>(b) * (K + 1);
-    const int32_t* xb = a.ids + static_cast<int64_t>(b) * K;
-    for (int j = 0; j <= K; ++j)
-      if (err || j != n) em[j] = (!err && j < n) ? xb[j] : -1;  // emitted[n] is written with the sampled token
-    for (int i = 0; i < K; ++i) {
-      const int64_t o = static_cast<int64_t>(b) * K + i;
-      const RowNorm& nd = sh.nrm[K + 1 + i];
-      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(sh.px[i]);
-      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(sh.qx[i]);
-      if (a.logz_d) a.logz_d[o] = err ? NAN : static_cast<float>((static_cast<double>(nd.M) + log2(nd.D)) * kLn2D);
-      if (a.overlap && err) a.overlap[o] = NAN;
-    }
-    if (a.logz_t)
-      for (int i = 0; i <= K; ++i)
-        a.logz_t[static_cast<int64_t>(b) * (K + 1) + i] =
-            err ? NAN : static_cast<float>((static_cast<double>(sh.nrm[i].M) + log2(sh.nrm[i].D)) * kLn2D);
     sh.n = err ? -1 : n;
   }
   __syncthreads();
-  return sh.n;
+  // the per-step outputs, one lane each (the float64 log2 of the normalisers in parallel)
+  const int n = sh.n;
+  const bool err = n < 0;
+  if (tid <= K) {
+    const int j = tid;
+    const int64_t ob = static_cast<int64_t>(b) * (K + 1) + j;
+    // emitted[n] is written with the sampled token
+    if (err || j != n) a.emitted[ob] = (!err && j < n) ? a.ids[static_cast<int64_t>(b) * K + j] : -1;
+    if (a.logz_t)
+      a.logz_t[ob] = err ? NAN : static_cast<float>((static_cast<double>(sh.nrm[j].M) + log2(sh.nrm[j].D)) * kLn2D);
+    if (j < K) {
+      const int64_t o = static_cast<int64_t>(b) * K + j;
+      const RowNorm& nd = sh.nrm[K + 1 + j];
+      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(sh.px[j]);
+      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(sh.qx[j]);
+      if (a.logz_d) a.logz_d[o] = err ? NAN : static_cast<float>((static_cast<double>(nd.M) + log2(nd.D)) * kLn2D);
+      if (a.overlap && err) a.overlap[o] = NAN;
+    }
+  }
+  return n;
 }
 
 // Row normalisers and accept decisions, one workgroup per batch row.
@@ -155,16 +158,26 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   DraftGather gx{0, 0.f, 0.f};
   if (static_cast<int>(threadIdx.x) < K) gx = gather_draft<E>(a, b, threadIdx.x);
-  // row j < K+1: target row j; row K+1+i: draft row i (one wave per row)
-  for (int j = wave; j < 2 * K + 1; j += kWaves) {
-    const int r = j <= K ? target_row(a, b, j) : draft_row(a, b, j - K - 1);
-    float M;
-    double D;
-    combine_row(a.stats + static_cast<int64_t>(r) * C, C, &M, &D);
+  // row j < K+1: target row j; row K+1+i: draft row i (one wave per row, the
+  // rows of a wave combined together so that their loads are in flight at once)
+  const int R = 2 * K + 1;
+  for (int j = wave; j < R; j += 2 * kWaves) {
+    const int j2 = j + kWaves;
+    const int r1 = j <= K ? target_row(a, b, j) : draft_row(a, b, j - K - 1);
+    const int r2 = j2 < R ? (j2 <= K ? target_row(a, b, j2) : draft_row(a, b, j2 - K - 1)) : r1;
+    float M1, M2;
+    double D1, D2;
+    combine_two_rows(a.stats + static_cast<int64_t>(r1) * C, a.stats + static_cast<int64_t>(r2) * C, C, &M1, &D1,
+                     &M2, &D2);
     if (lane == 0) {
-      const RowNorm nm = make_norm(M, D);
-      sh.nrm[j] = nm;
-      a.norms[r] = nm;
+      const RowNorm n1 = make_norm(M1, D1);
+      sh.nrm[j] = n1;
+      a.norms[r1] = n1;
+      if (j2 < R) {
+        const RowNorm n2 = make_norm(M2, D2);
+        sh.nrm[j2] = n2;
+        a.norms[r2] = n2;
+      }
     }
   }
   __syncthreads();
