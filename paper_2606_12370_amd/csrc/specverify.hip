@@ -265,8 +265,8 @@ spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
                      dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C,
                      const_cast<sv::RowNorm*>(a.norms));
   void (*tp)(sv::TvArgs, int64_t) = sv::tv_pair_kernel<E, NT, kStep>;
-  hipLaunchKernelGGL(tp, dim3(grid_for(reinterpret_cast<const void*>(tp), units * C)), dim3(sv::kThreads), 0, s, a,
-                     units * C);
+  // one workgroup per task (measured faster than a resident grid: 5.6 against 6.0 ms at N=16384, K=3, V=151936)
+  hipLaunchKernelGGL(tp, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a, units * C);
   hipLaunchKernelGGL(sv::tv_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
   // the gradient pass reads bf16 as 4-element vectors: one coalesced float4 store per lane

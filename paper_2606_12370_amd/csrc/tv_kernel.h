@@ -16,8 +16,9 @@
 //                 with A1 = scale g_k (1 - S_k) / T, A0 = -scale g_k S_k / T,
 //                 written once (skipped for a forward-only call).
 //   6 tv_loss     one workgroup adds the N position losses in a fixed order.
-// The indicator 1[q <= p] is evaluated by the same code on the same bits in
-// launches 3 and 5, so S and the gradient always agree on it.
+// The indicator 1[q <= p] is decided once, in launch 3, on log2 q <= log2 p
+// (float32), and stored as bits that launch 5 reads, so S and the gradient
+// always agree on it.
 #pragma once
 
 #include "sv_device.h"
@@ -109,7 +110,7 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
   __shared__ RedLds<4> red;
   const RowsDesc& d = a.rows;
   const int C = d.C;
-  // persistent: strides over the (position step, chunk) tasks
+  // grid-stride over the (position step, chunk) tasks (launched one workgroup per task)
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
     const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
     const int n = u / a.K, k = u % a.K;
@@ -136,11 +137,14 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
         uint32_t m = 0;
 #pragma unroll
         for (int kk = 0; kk < EPV; ++kk) {
-          const float p = prob(xt[j][kk], s, nt.M, nt.invD);
-          const float q = prob(xd[j][kk], s, nd.M, nd.invD);
-          al += fminf(p, q);
-          const bool le = q <= p;
-          sq += le ? q : 0.f;
+          // log2 p and log2 q; min(p, q) is one exponential, and it is q
+          // itself wherever q <= p, so it also carries the S term
+          const float lp = fmaf(xt[j][kk], s, -nt.M) - nt.L;
+          const float lq = fmaf(xd[j][kk], s, -nd.M) - nd.L;
+          const float mn = __builtin_amdgcn_exp2f(fminf(lp, lq));
+          al += mn;
+          const bool le = lq <= lp;
+          sq += le ? mn : 0.f;
           m |= le ? (1u << kk) : 0u;
         }
         mbits |= static_cast<uint64_t>(m) << ((j0 + j) * EPV);
