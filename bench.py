@@ -17,9 +17,10 @@ workload (N=16384 positions x 3 steps) is timed too and reported under
 `tv_loss`; target-only verification, the draft-stage sampler (the B*K draft
 rows) and the per-step diagnostics on the same batch under `target_only`,
 `sample` and `diagnostics`, the Gumbel-max variants of verification and
-sampling under `verify_gumbel` and `sample_gumbel`, and the forward- and
-reverse-KL losses with gradients on the training workload under `kl_loss`
-(none of them part of `value`).
+sampling under `verify_gumbel` and `sample_gumbel`, the forward- and
+reverse-KL losses with gradients on the training workload under `kl_loss`,
+and spec_verify without overlaps (`verify_serving`) and on the B=64 and
+B=1024 / V=262144 batches (none of them part of `value`).
 """
 
 import argparse
@@ -114,7 +115,7 @@ def timed(torch, stream, fn, steps):
 def hbm_roofline(nbytes, ms, key):
     achieved = nbytes / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(key, nbytes)}
+            "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(key, nbytes) if key else None}
 
 
 def bench_variants(torch, binding, copies, stream, steps, B, K, V):
@@ -183,6 +184,52 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
     return out
 
 
+def verify_bytes(B, K, V, esize=2):
+    """Algorithmic bytes of one spec_verify call: logits read once, ids and
+    per-row temperatures in, accept lengths, emitted ids and overlaps out."""
+    return B * (2 * K + 1) * V * esize + B * K * 4 + B * 4 + B * (K + 1) * 4 + B * 4 + B * K * 4
+
+
+def bench_verify_context(torch, binding, W, copies, stream, steps):
+    """spec_verify beside the headline: the same batch without overlaps
+    (serving: only the first rejected step's pair is read again), and the
+    rollout (B=64) and large (B=1024, V=262144, per-row temperature) batches.
+    Reported next to `value`, not in it."""
+    out = {}
+    cfg = W.CONFIGS["verify_bf16_b256_k3_v151936"]
+    B, K, V = cfg["B"], cfg["K"], cfg["V"]
+    o = {"accept_len": torch.empty(B, dtype=torch.int32, device="cuda"),
+         "emitted": torch.empty((B, K + 1), dtype=torch.int32, device="cuda")}
+
+    def serving(it):
+        c = copies[it % len(copies)]
+        binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, want_overlap=False, out=o)
+
+    ms = timed(torch, stream, serving, steps)
+    nbytes = verify_bytes(B, K, V) - B * K * 4
+    out["verify_serving"] = {"workload": "verify_bf16_b256_k3_v151936 without overlaps", "ms_per_call": ms,
+                             "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
+                             "roofline": hbm_roofline(nbytes, ms, None)}
+    for key in ("rollout_bf16_b64_k3_v151936", "large_bf16_b1024_k3_v262144"):
+        c2 = W.CONFIGS[key]
+        B2, K2, V2 = c2["B"], c2["K"], c2["V"]
+        cps = [W.verify_inputs_torch(B2, K2, V2, W.BF16, c2["gen"], c2["seed"] + 100 * i) for i in range(2)]
+        o2 = {"accept_len": torch.empty(B2, dtype=torch.int32, device="cuda"),
+              "emitted": torch.empty((B2, K2 + 1), dtype=torch.int32, device="cuda"),
+              "overlap": torch.empty((B2, K2), dtype=torch.float32, device="cuda")}
+
+        def step2(it):
+            c = cps[it % len(cps)]
+            binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=o2)
+
+        ms = timed(torch, stream, step2, steps)
+        out["verify_" + key] = {"ms_per_call": ms, "verified_draft_tokens_per_s": B2 * K2 / (ms * 1e-3),
+                                "roofline": hbm_roofline(verify_bytes(B2, K2, V2), ms, None)}
+        del cps
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_calibration(torch, dev, gib=1, reps=3):
     """A plain device-to-device copy of known size, for scaling the FETCH_SIZE
     and WRITE_SIZE counters of the other kernels in the same profile."""
@@ -207,6 +254,8 @@ def main():
     ap.add_argument("--no-variants", action="store_true",
                     help="skip target-only verification, the sampler and the diagnostics")
     ap.add_argument("--variant-steps", type=int, default=20)
+    ap.add_argument("--no-context", action="store_true",
+                    help="skip spec_verify without overlaps and on the B=64 / B=1024 batches")
     ap.add_argument("--no-kl", action="store_true", help="skip the CE / KL loss legs")
     ap.add_argument("--no-tv-loss", action="store_true", help="skip the TV loss leg (keeps the KL legs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -279,7 +328,7 @@ def main():
         acc = outs[0]["accept_len"].float()
         assert float(acc.min()) >= 0
         # logits read once, plus ids and per-row temperatures in, all outputs out
-        algo_bytes = B * (2 * K + 1) * V * 2 + B * K * 4 + B * 4 + B * (K + 1) * 4 + B * 4 + B * K * 4
+        algo_bytes = verify_bytes(B, K, V)
         achieved = algo_bytes / (ms_per_step * 1e-3) / 1e9
         result.update({
             "value": B * K / (ms_per_step * 1e-3),
@@ -292,6 +341,9 @@ def main():
             "wall_s_timed_region": wall,
         })
         del outs
+        if not args.no_context:
+            log("timing spec_verify without overlaps and on the B=64 and B=1024 batches")
+            result.update(bench_verify_context(torch, binding, W, copies, stream, args.variant_steps))
     if not args.no_variants:
         log("timing target-only verification, the sampler and the diagnostics")
         result.update(bench_variants(torch, binding, copies, stream, args.variant_steps, B, K, V))
