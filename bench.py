@@ -245,8 +245,10 @@ def copy_calibration(torch, dev, gib=1, reps=3):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    # the GPU takes some tens of milliseconds of sustained load to reach its
+    # clocks: 300 untimed calls (about 55 ms) put the timed ones at steady state
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tv", action="store_true")
     ap.add_argument("--tv-steps", type=int, default=3)

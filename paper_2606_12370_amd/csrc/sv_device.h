@@ -139,15 +139,52 @@ __device__ __forceinline__ double u24(uint64_t w) {
 // ---------------------------------------------------------------------------
 // wave64 and workgroup reductions / scans.  All reductions run in a fixed
 // order so results are bitwise reproducible.
+//
+// The max and sum reductions use DPP lane permutations inside each row of 16
+// lanes (a butterfly: swap neighbours, swap pairs, mirror the half row,
+// mirror the row; a commutative step gives every lane of the row the same
+// bits) and then combine the four rows' results, read from lanes 0, 16, 32
+// and 48, in a fixed order.  No LDS traffic is involved.
+namespace dpp {
+constexpr int kXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kHalfMirror = 0x141;  // row_half_mirror: lane i <- 7 - i within 8
+constexpr int kMirror = 0x140;      // row_mirror: lane i <- 15 - i within 16
+template <int CTRL>
+__device__ __forceinline__ float mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+template <int CTRL>
+__device__ __forceinline__ double mov(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(b), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(b >> 32), CTRL, 0xf, 0xf, false);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+}
+__device__ __forceinline__ float lane(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ double lane(double v, int l) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), l);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), l);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+}
+}  // namespace dpp
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp::mov<dpp::kXor1>(v));
+  v = fmaxf(v, dpp::mov<dpp::kXor2>(v));
+  v = fmaxf(v, dpp::mov<dpp::kHalfMirror>(v));
+  v = fmaxf(v, dpp::mov<dpp::kMirror>(v));
+  return fmaxf(fmaxf(dpp::lane(v, 0), dpp::lane(v, 16)), fmaxf(dpp::lane(v, 32), dpp::lane(v, 48)));
 }
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp::mov<dpp::kXor1>(v);
+  v += dpp::mov<dpp::kXor2>(v);
+  v += dpp::mov<dpp::kHalfMirror>(v);
+  v += dpp::mov<dpp::kMirror>(v);
+  return (dpp::lane(v, 0) + dpp::lane(v, 16)) + (dpp::lane(v, 32) + dpp::lane(v, 48));
 }
 __device__ __forceinline__ int wave_min_int(int v) {
 #pragma unroll
