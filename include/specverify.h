@@ -32,7 +32,7 @@
  *  - Each call is a short fixed sequence of kernel launches on `stream`
  *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a gradient,
  *    spec_verify_target_only: 2, spec_sample: 2, spec_diagnostics: 4,
- *    spec_verify_gumbel: 4, or 3 without overlaps, spec_sample_gumbel: 2,
+ *    spec_verify_gumbel: 5, or 4 without overlaps, spec_sample_gumbel: 2,
  *    spec_kl_loss_fwd_bwd: 5, or 6 for reverse KL with a gradient); no
  *    launch waits on another workgroup, so any number of resident
  *    workgroups is enough.
