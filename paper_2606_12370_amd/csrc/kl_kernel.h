@@ -92,6 +92,8 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
 #pragma unroll
       for (int j = 0; j < S; ++j) {
         float gv[EPV];
+        // the EPV elements of one vector are summed in float32, vectors in float64
+        float ve = 0.f, vf = 0.f, vw = 0.f;
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
           const float tt = fmaf(xt[j][k], s, -nt.M);
@@ -102,11 +104,14 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
           if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
           else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
           else term = f > 0.f ? f * (uu - tt) : 0.f;
-          se += static_cast<double>(e);
-          sf += static_cast<double>(f);
-          w += static_cast<double>(term);
+          ve += e;
+          vf += f;
+          vw += term;
           gv[k] = gcoef * (f * nd.invD - e * nt.invD);  // (q - p) scale / (K T)
         }
+        se += static_cast<double>(ve);
+        sf += static_cast<double>(vf);
+        w += static_cast<double>(vw);
         if (write_grad)
           store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }

@@ -294,7 +294,8 @@ spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
   using G = typename GradElem<E>::type;
   constexpr int NTG = kChunkElems / (sv::kThreads * G::EPV);
   void (*kp)(sv::KlArgs, int64_t) = sv::kl_pass_kernel<G, NTG, kStep, KIND>;
-  hipLaunchKernelGGL(kp, dim3(grid_for(reinterpret_cast<const void*>(kp), units * C)), dim3(sv::kThreads), 0, s, a,
+  // one workgroup per task (measured faster than a resident grid: reverse KL 22.8 -> 21.2 ms per call)
+  hipLaunchKernelGGL(kp, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a,
                      units * C);
   hipLaunchKernelGGL(sv::kl_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
