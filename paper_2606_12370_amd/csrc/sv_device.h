@@ -471,8 +471,7 @@ __device__ __forceinline__ bool temperature_ok(float T) { return T > 0.f && T < 
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat* __restrict__ stats, int64_t ntasks) {
   __shared__ RedLds<4> red;
-  // persistent: the grid is sized to what the device holds at once and
-  // strides over the (row, chunk) tasks
+  // grid-stride over the (row, chunk) tasks (launched one workgroup per task)
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
     const int r = static_cast<int>(t / d.C), c = static_cast<int>(t - static_cast<int64_t>(t / d.C) * d.C);
     int b;

@@ -200,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void tv_grad_kernel(TvArgs a, int64_t nta
   constexpr int TILE = kThreads * EPV;
   const RowsDesc& d = a.rows;
   const int C = d.C, K = a.K, V = d.V;
-  // persistent: strides over the (position step, chunk) tasks
+  // grid-stride over the (position step, chunk) tasks (launched one workgroup per task)
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
     const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
     const int n = u / K, k = u % K;

@@ -193,8 +193,7 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
   __shared__ RedLds<4> red;
   const RowsDesc& d = a.rows;
   const int C = d.C;
-  // persistent: the grid is sized to what the device holds at once and
-  // strides over the (pair, chunk) tasks
+  // grid-stride over the (pair, chunk) tasks (launched one workgroup per task)
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
     const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
     const int b = u / a.K, i = u % a.K;
