@@ -17,7 +17,10 @@
 //     row), diag_pair (per pair chunk), diag_finish (one wave per step).
 #pragma once
 
+#include <cfloat>
+
 #include "sv_device.h"
+
 #include "verify_kernel.h"
 
 namespace sv {
@@ -328,7 +331,6 @@ __global__ __launch_bounds__(kThreads) void diag_stats_kernel(RowsDesc d, DiagSt
     const int tile0 = c * NT;
     const int nt = min(NT, d.ntiles - tile0);
     float ref = -INFINITY, dsum = 0.f, esum = 0.f, zmax = -INFINITY;
-    int arg = 0x7fffffff;
 #pragma unroll
     for (int j0 = 0; j0 < NT; j0 += S) {
       if (j0 >= nt) break;
@@ -338,14 +340,8 @@ __global__ __launch_bounds__(kThreads) void diag_stats_kernel(RowsDesc d, DiagSt
 #pragma unroll
       for (int j = 0; j < S; ++j)
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          mx = fmaxf(mx, x[j][k]);
-          // ascending index order: a strict ">" keeps the first index of the maximum
-          if (x[j][k] > zmax) {
-            zmax = x[j][k];
-            arg = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV + k;
-          }
-        }
+        for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[j][k]);
+      zmax = fmaxf(zmax, mx);
       if (mx != -INFINITY) {
         const float rr = mx * s;
         float acc = 0.f, acce = 0.f;
@@ -356,7 +352,8 @@ __global__ __launch_bounds__(kThreads) void diag_stats_kernel(RowsDesc d, DiagSt
             const float tv = fmaf(x[j][k], s, -rr);
             const float e = __builtin_amdgcn_exp2f(tv);
             acc += e;
-            acce += (e != 0.f) ? e * tv : 0.f;
+            // e * tv, with a masked token's -inf exponent clamped so that 0 * tv stays 0
+            acce = fmaf(e, fmaxf(tv, -FLT_MAX), acce);
           }
         if (ref == -INFINITY) {
           ref = rr; dsum = acc; esum = acce;
@@ -384,7 +381,23 @@ __global__ __launch_bounds__(kThreads) void diag_stats_kernel(RowsDesc d, DiagSt
       d4[1] = f * (static_cast<double>(esum) + sh * static_cast<double>(dsum));
     }
     wg_sum<4>(d4, red);
-    const int a1 = wg_min_int((zmax == m4[1]) ? arg : 0x7fffffff, red1);
+    // first index of the chunk's largest logit: only the threads that hold it
+    // look through their elements again (ascending, so the first equal one)
+    int arg = 0x7fffffff;
+    if (zmax == m4[1] && zmax != -INFINITY) {
+#pragma unroll
+      for (int j0 = 0; j0 < NT; j0 += S) {
+        if (j0 >= nt || arg != 0x7fffffff) break;
+        float x[S][EPV];
+        load_tiles<E, S>(row, tile0 + j0, d.V, aligned, x);  // one load step, from L2
+#pragma unroll
+        for (int j = S - 1; j >= 0; --j)
+#pragma unroll
+          for (int k = EPV - 1; k >= 0; --k)
+            if (x[j][k] == zmax) arg = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV + k;
+      }
+    }
+    const int a1 = wg_min_int(arg, red1);
     if (threadIdx.x == 0) {
       DiagStat o;
       o.m = m4[0]; o.zmax = m4[1]; o.arg = a1; o.pad = 0; o.D = d4[0]; o.Em = d4[1];
