@@ -79,6 +79,11 @@ bool rows_ok(int64_t rows, int V, spec_dtype dt) {
   return rows >= 1 && V >= 1 && rows * geometry(V, dt).C < (int64_t{1} << 31);
 }
 
+// Sizes for the entry points that keep statistics per sub-chunk of kStep tiles.
+bool rows_sub_ok(int64_t rows, int V, spec_dtype dt) {
+  return rows >= 1 && V >= 1 && rows * sub_chunks(V, dt) < (int64_t{1} << 31);
+}
+
 struct VerifyLayout {
   size_t stats = 0, norms = 0, decision = 0, pairs = 0, gbest = 0, total = 0;
 };
@@ -140,14 +145,14 @@ struct ToLayout {
 };
 ToLayout to_layout(int B, int K, int V, spec_dtype dt) {
   ToLayout L;
-  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t C = static_cast<size_t>(sub_chunks(V, dt));
   L.stats = 0;
   L.total = align_up(static_cast<size_t>(B) * (K + 1) * C * sizeof(sv::RowStat), 256);
   return L;
 }
 
 size_t sample_ws(int R, int V, spec_dtype dt) {
-  return align_up(static_cast<size_t>(R) * geometry(V, dt).C * sizeof(sv::RowStat), 256);
+  return align_up(static_cast<size_t>(R) * sub_chunks(V, dt) * sizeof(sv::RowStat), 256);
 }
 
 struct DiagLayout {
@@ -314,25 +319,31 @@ spec_status launch_kl_kind(const sv::KlArgs& a, hipStream_t s) {
   return launch_kl<E, NT, sv::kKlReverse>(a, s);
 }
 
-template <class E, int NT>
+// Target-only verification and the sampler stream tasks of NTT tiles with
+// statistics per sub-chunk of kStep tiles (as multinomial verification
+// does), so that their per-row launch reads one sub-chunk again, in one load
+// step.
+template <class E, int NTT>
 spec_status launch_to(const sv::ToArgs& a, hipStream_t s) {
-  const int64_t tasks = int64_t{a.B} * (a.K + 1) * a.rows.C;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  const int ct = (a.rows.ntiles + NTT - 1) / NTT;
+  const int64_t tasks = int64_t{a.B} * (a.K + 1) * ct;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int, int64_t) = sv::row_stats_sub_kernel<E, NTT, kStep>;
   hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), tasks);
-  hipLaunchKernelGGL((sv::to_verify_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
+                     const_cast<sv::RowStat*>(a.stats), ct, tasks);
+  hipLaunchKernelGGL((sv::to_verify_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
                      s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
-template <class E, int NT>
+template <class E, int NTT>
 spec_status launch_sample(const sv::SampleArgs& a, hipStream_t s) {
-  const int64_t tasks = int64_t{a.R} * a.rows.C;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
+  const int ct = (a.rows.ntiles + NTT - 1) / NTT;
+  const int64_t tasks = int64_t{a.R} * ct;
+  void (*rs)(sv::RowsDesc, sv::RowStat*, int, int64_t) = sv::row_stats_sub_kernel<E, NTT, kStep>;
   hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), tasks);
-  hipLaunchKernelGGL((sv::sample_kernel<E, NT, kStep>), dim3(static_cast<unsigned>(a.R)), dim3(sv::kThreads), 0, s,
-                     a);
+                     const_cast<sv::RowStat*>(a.stats), ct, tasks);
+  hipLaunchKernelGGL((sv::sample_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.R)), dim3(sv::kThreads), 0,
+                     s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
@@ -556,7 +567,7 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
 
 size_t spec_verify_target_only_workspace_size(int B, int K, int V, spec_dtype dtype) {
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
-  if (B < 1 || K < 1 || K > SPEC_MAX_K || !rows_ok(int64_t{B} * (K + 1), V, dtype)) return 0;
+  if (B < 1 || K < 1 || K > SPEC_MAX_K || !rows_sub_ok(int64_t{B} * (K + 1), V, dtype)) return 0;
   return to_layout(B, K, V, dtype).total;
 }
 
@@ -567,7 +578,7 @@ spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_
                                     float* logz_target, void* workspace, size_t workspace_bytes, void* stream) {
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
   if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
-  if (B < 1 || K < 1 || !rows_ok(int64_t{B} * (K + 1), V, dtype)) return SPEC_EINVAL;
+  if (B < 1 || K < 1 || !rows_sub_ok(int64_t{B} * (K + 1), V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
   if (t_stride_b < 0 || t_stride_k < 0) return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
@@ -581,7 +592,7 @@ spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_
   a.rows.drf = nullptr; a.rows.dsb = 0; a.rows.dsk = 0; a.rows.dper = 1;
   a.rows.nb = B;
   a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
-  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = sub_chunks(V, dtype);
   a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, esize_of(dtype)) ? 1 : 0;
   a.rows.vec_d = 0;
   a.B = B; a.K = K;
@@ -590,12 +601,12 @@ spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_
   a.accept_len = accept_len; a.emitted = emitted_ids; a.p_at = p_at_draft; a.logz_t = logz_target;
   a.stats = reinterpret_cast<const sv::RowStat*>(static_cast<char*>(workspace) + L.stats);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_to<BF16, kNtBf16>(a, s) : launch_to<F32, kNtF32>(a, s);
+  return dtype == SPEC_BF16 ? launch_to<BF16, kTaskBf16>(a, s) : launch_to<F32, kTaskF32>(a, s);
 }
 
 size_t spec_sample_workspace_size(int R, int V, spec_dtype dtype) {
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
-  if (!rows_ok(R, V, dtype)) return 0;
+  if (!rows_sub_ok(R, V, dtype)) return 0;
   return sample_ws(R, V, dtype);
 }
 
@@ -603,7 +614,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
                         const float* temperature, float temperature_scalar, uint64_t seed, uint64_t offset,
                         int32_t* tokens, float* logz, void* workspace, size_t workspace_bytes, void* stream) {
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
-  if (!rows_ok(R, V, dtype)) return SPEC_EINVAL;
+  if (!rows_sub_ok(R, V, dtype)) return SPEC_EINVAL;
   if (!logits || !tokens || stride_r < 0) return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar >= 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
   if (!workspace || workspace_bytes < sample_ws(R, V, dtype)) return SPEC_EWORKSPACE;
@@ -615,7 +626,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
   a.rows.drf = nullptr; a.rows.dsb = 0; a.rows.dsk = 0; a.rows.dper = 1;
   a.rows.nb = R;
   a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
-  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = sub_chunks(V, dtype);
   a.rows.vec_t = rows_vec_aligned(logits, stride_r, 0, esize_of(dtype)) ? 1 : 0;
   a.rows.vec_d = 0;
   a.R = R;
@@ -623,7 +634,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
   a.token = tokens; a.logz = logz;
   a.stats = reinterpret_cast<const sv::RowStat*>(workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_sample<BF16, kNtBf16>(a, s) : launch_sample<F32, kNtF32>(a, s);
+  return dtype == SPEC_BF16 ? launch_sample<BF16, kTaskBf16>(a, s) : launch_sample<F32, kTaskF32>(a, s);
 }
 
 size_t spec_diagnostics_workspace_size(int B, int K, int V, spec_dtype dtype) {

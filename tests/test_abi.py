@@ -86,11 +86,12 @@ def test_workspace_sizes(lib):
     assert 0 < a < b and a % 256 == 0
     assert lib.spec_tv_workspace_size(16384, 3, 151936, 1) > 0
     assert lib.spec_tv_workspace_size(16384, 0, 151936, 1) == 0
-    # target-only: statistics of the K+1 target rows only
+    # target-only: statistics of the K+1 target rows only, one 16-byte record
+    # per 8192-element sub-chunk (19 per bf16 row of 151936)
     to = lib.spec_verify_target_only_workspace_size(256, 3, 151936, 1)
-    assert to == 256 * 4 * 10 * 16
+    assert to == 256 * 4 * 19 * 16
     assert lib.spec_verify_target_only_workspace_size(256, 9, 151936, 1) == 0
-    assert lib.spec_sample_workspace_size(768, 151936, 1) == 768 * 10 * 16
+    assert lib.spec_sample_workspace_size(768, 151936, 1) == 768 * 19 * 16
     assert lib.spec_sample_workspace_size(0, 151936, 1) == 0
     assert lib.spec_sample_workspace_size(4, 0, 0) == 0
     assert lib.spec_diagnostics_workspace_size(256, 3, 151936, 1) > 0
