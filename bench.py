@@ -334,10 +334,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 in, f32 math",
+        "dtype": "f32",
         "data": "synthetic (seeded rollout-shaped logits generated on the GPU)",
-        "config": {"workload": "verify_bf16_b256_k3_v151936", "B": B, "K": K, "V": V,
-                   "temperature": "per row, 1.0", "input_copies": 2},
+        "config": {"workload": "verify_bf16_b256_k3_v151936", "B": B, "K": K, "V": V, "logits": "bf16",
+                   "arithmetic": "float32 per element, float64 sums", "temperature": "per row, 1.0",
+                   "input_copies": 2},
     }
 
     if not args.no_verify or not args.no_variants:
