@@ -6,8 +6,6 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
-#include <map>
-#include <mutex>
 #include <utility>
 
 #include "specverify.h"
@@ -28,11 +26,13 @@ using sv::F32;
 constexpr int kNtBf16 = 8;
 constexpr int kNtF32 = 16;
 constexpr int kStep = 4;
-// Multinomial verification streams longer tasks (32768 elements: 16 bf16 or
-// 32 fp32 tiles) and keeps statistics per sub-chunk of kStep tiles, which is
-// what its finish re-reads.
-constexpr int kTaskBf16 = 16;
-constexpr int kTaskF32 = 32;
+// Multinomial verification, target-only verification and the sampler keep
+// statistics per sub-chunk of kStep tiles (8192 bf16 or 4096 fp32 elements),
+// which is what their per-row launches read again; one wave streams one
+// sub-chunk, kStatVec (statistics) or kPairVec (pair pass) vectors per lane
+// at a time.
+constexpr int kStatVec = 8;
+constexpr int kPairVec = 4;
 constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
 static_assert(kNtF32 * sv::kThreads * sv::F32::EPV == kChunkElems, "chunk geometry");
@@ -177,50 +177,29 @@ bool rows_vec_aligned(const void* base, int64_t s0, int64_t s1, size_t esize) {
          ((s1 * static_cast<int64_t>(esize)) % 16 == 0);
 }
 
-// Workgroups of `kernel` (256 threads, static LDS only) the current device
-// holds at once, queried once per (device, kernel).  The pair pass of
-// multinomial verification is launched with min(tasks, this) workgroups
-// striding over its tasks, which measured faster for it (173 against 174 µs
-// per call); every streaming kernel is written grid-stride, and the others
-// run one workgroup per task, which measured faster for them.
-// Returns 0 if the runtime cannot tell (the caller then launches one
-// workgroup per task).
-int64_t resident_blocks(const void* kernel) {
-  static std::mutex mu;
-  static std::map<std::pair<int, const void*>, int64_t> cache;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  std::lock_guard<std::mutex> g(mu);
-  const auto key = std::make_pair(dev, kernel);
-  const auto it = cache.find(key);
-  if (it != cache.end()) return it->second;
-  int cus = 0, per_cu = 0;
-  int64_t n = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, sv::kThreads, 0) == hipSuccess)
-    n = int64_t{cus} * per_cu;
-  cache[key] = n;
-  return n;
+// Statistics per sub-chunk of every row, one wave per sub-chunk and four
+// waves per workgroup (one workgroup per four sub-chunks measured faster
+// than a resident grid for this purely streaming pass).
+template <class E>
+void launch_stats_wave(const sv::RowsDesc& d, sv::RowStat* stats, int64_t rows, hipStream_t s) {
+  const int64_t nsub = rows * d.C;
+  hipLaunchKernelGGL((sv::row_stats_wave_kernel<E, kStep, kStatVec>),
+                     dim3(static_cast<unsigned>((nsub + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s, d,
+                     stats, nsub);
 }
 
-unsigned grid_for(const void* kernel, int64_t tasks) {
-  const int64_t r = resident_blocks(kernel);
-  return static_cast<unsigned>((r > 0 && r < tasks) ? r : tasks);
-}
-
-template <class E, int NTT>
+template <class E>
 spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) {
-  // tasks of NTT tiles; statistics and pair sums per sub-chunk of kStep tiles
-  const int ct = (a.rows.ntiles + NTT - 1) / NTT;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int, int64_t) = sv::row_stats_sub_kernel<E, NTT, kStep>;
-  // one workgroup per task: measured faster for this first, purely streaming pass
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(rows * ct)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), ct, rows * ct);
+  // statistics and pair sums per sub-chunk of kStep tiles, one wave per sub-chunk
+  launch_stats_wave<E>(a.rows, const_cast<sv::RowStat*>(a.stats), rows, s);
   hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
-  void (*pp)(sv::VerifyArgs, int, int64_t) = sv::pair_pass_sub_kernel<E, NTT, kStep>;
-  const int64_t pairs = int64_t{a.B} * a.K * ct;
-  hipLaunchKernelGGL(pp, dim3(grid_for(reinterpret_cast<const void*>(pp), pairs)), dim3(sv::kThreads), 0, s, a, ct,
-                     pairs);
+  // one workgroup per four (pair, sub-chunk) items: measured faster than a
+  // grid of what the device holds at once striding over them (73.6 against
+  // 75.0 us at B=256, K=3, V=151936 bf16)
+  const int64_t items = int64_t{a.B} * a.K * a.rows.C;
+  hipLaunchKernelGGL((sv::pair_pass_wave_kernel<E, kStep, kPairVec>),
+                     dim3(static_cast<unsigned>((items + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s, a,
+                     items);
   // the finish inverts the CDF inside one sub-chunk (kStep tiles, one load step)
   hipLaunchKernelGGL((sv::finish_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
                      s, a);
@@ -319,29 +298,20 @@ spec_status launch_kl_kind(const sv::KlArgs& a, hipStream_t s) {
   return launch_kl<E, NT, sv::kKlReverse>(a, s);
 }
 
-// Target-only verification and the sampler stream tasks of NTT tiles with
-// statistics per sub-chunk of kStep tiles (as multinomial verification
-// does), so that their per-row launch reads one sub-chunk again, in one load
-// step.
-template <class E, int NTT>
+// Target-only verification and the sampler keep statistics per sub-chunk
+// of kStep tiles (as multinomial verification does), so that their per-row
+// launch reads one sub-chunk again, in one load step.
+template <class E>
 spec_status launch_to(const sv::ToArgs& a, hipStream_t s) {
-  const int ct = (a.rows.ntiles + NTT - 1) / NTT;
-  const int64_t tasks = int64_t{a.B} * (a.K + 1) * ct;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int, int64_t) = sv::row_stats_sub_kernel<E, NTT, kStep>;
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), ct, tasks);
+  launch_stats_wave<E>(a.rows, const_cast<sv::RowStat*>(a.stats), int64_t{a.B} * (a.K + 1), s);
   hipLaunchKernelGGL((sv::to_verify_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
                      s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
-template <class E, int NTT>
+template <class E>
 spec_status launch_sample(const sv::SampleArgs& a, hipStream_t s) {
-  const int ct = (a.rows.ntiles + NTT - 1) / NTT;
-  const int64_t tasks = int64_t{a.R} * ct;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int, int64_t) = sv::row_stats_sub_kernel<E, NTT, kStep>;
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(tasks)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), ct, tasks);
+  launch_stats_wave<E>(a.rows, const_cast<sv::RowStat*>(a.stats), int64_t{a.R}, s);
   hipLaunchKernelGGL((sv::sample_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.R)), dim3(sv::kThreads), 0,
                      s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
@@ -457,7 +427,7 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
   if (st != SPEC_OK) return st;
   const int64_t rows = int64_t{B} * (2 * K + 1);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_verify<BF16, kTaskBf16>(a, rows, s) : launch_verify<F32, kTaskF32>(a, rows, s);
+  return dtype == SPEC_BF16 ? launch_verify<BF16>(a, rows, s) : launch_verify<F32>(a, rows, s);
 }
 
 size_t spec_verify_gumbel_workspace_size(int B, int K, int V, spec_dtype dtype) {
@@ -601,7 +571,7 @@ spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_
   a.accept_len = accept_len; a.emitted = emitted_ids; a.p_at = p_at_draft; a.logz_t = logz_target;
   a.stats = reinterpret_cast<const sv::RowStat*>(static_cast<char*>(workspace) + L.stats);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_to<BF16, kTaskBf16>(a, s) : launch_to<F32, kTaskF32>(a, s);
+  return dtype == SPEC_BF16 ? launch_to<BF16>(a, s) : launch_to<F32>(a, s);
 }
 
 size_t spec_sample_workspace_size(int R, int V, spec_dtype dtype) {
@@ -634,7 +604,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
   a.token = tokens; a.logz = logz;
   a.stats = reinterpret_cast<const sv::RowStat*>(workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_sample<BF16, kTaskBf16>(a, s) : launch_sample<F32, kTaskF32>(a, s);
+  return dtype == SPEC_BF16 ? launch_sample<BF16>(a, s) : launch_sample<F32>(a, s);
 }
 
 size_t spec_diagnostics_workspace_size(int B, int K, int V, spec_dtype dtype) {

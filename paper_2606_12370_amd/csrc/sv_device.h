@@ -65,30 +65,29 @@ struct F32 {
   static __device__ __forceinline__ float one(const raw* p) { return *p; }
 };
 
-// Load S tiles (tile0 .. tile0+S-1) of a row: x[j][k] receives element
-// (tile0 + j) * 256 * EPV + t * EPV + k of the row, t = threadIdx.x.  Elements
-// at or beyond V are -inf (probability 0).  With `aligned` (row base 16-byte
-// aligned) every full vector is one vector load, all issued back to back; a
-// vector past V is read from the row start and discarded (no branch around
-// the load); the one vector that straddles V (V not a multiple of EPV) is
-// completed element by element.  Unaligned rows are read element by element.
-template <class E, int S>
-__device__ __forceinline__ void load_tiles(const typename E::raw* __restrict__ row, int tile0, int V, bool aligned,
-                                           float (&x)[S][E::EPV]) {
+// Load S vectors of a span read by W lanes together: x[j][k] receives element
+// e0 + j * W * EPV + idx * EPV + k of the row (idx: this lane's index among
+// the W).  Elements at or beyond V are -inf (probability 0).  With `aligned`
+// (row base 16-byte aligned) every full vector is one vector load, all issued
+// back to back; a vector past V is read from the row start and discarded (no
+// branch around the load); the one vector that straddles V (V not a multiple
+// of EPV) is completed element by element.  Unaligned rows are read element
+// by element.
+template <class E, int S, int W>
+__device__ __forceinline__ void load_span(const typename E::raw* __restrict__ row, int e0, int idx, int V,
+                                          bool aligned, float (&x)[S][E::EPV]) {
   constexpr int EPV = E::EPV;
-  constexpr int TILE = 256 * EPV;
-  const int t = threadIdx.x;
   if (aligned) {
     typename E::vec w[S];
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      const int v0 = (tile0 + j) * TILE + t * EPV;
+      const int v0 = e0 + j * W * EPV + idx * EPV;
       const int off = (v0 + EPV <= V) ? v0 : 0;
       w[j] = __builtin_nontemporal_load(reinterpret_cast<const typename E::vec*>(row + off));
     }
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      const int v0 = (tile0 + j) * TILE + t * EPV;
+      const int v0 = e0 + j * W * EPV + idx * EPV;
       E::widen(w[j], x[j]);
       if (v0 + EPV > V) {
 #pragma unroll
@@ -98,11 +97,20 @@ __device__ __forceinline__ void load_tiles(const typename E::raw* __restrict__ r
   } else {
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      const int v0 = (tile0 + j) * TILE + t * EPV;
+      const int v0 = e0 + j * W * EPV + idx * EPV;
 #pragma unroll
       for (int k = 0; k < EPV; ++k) x[j][k] = (v0 + k < V) ? E::one(row + v0 + k) : -INFINITY;
     }
   }
+}
+
+// Load S tiles (tile0 .. tile0+S-1) of a row, a tile being one vector of each
+// of the workgroup's 256 threads: x[j][k] receives element
+// (tile0 + j) * 256 * EPV + t * EPV + k of the row, t = threadIdx.x.
+template <class E, int S>
+__device__ __forceinline__ void load_tiles(const typename E::raw* __restrict__ row, int tile0, int V, bool aligned,
+                                           float (&x)[S][E::EPV]) {
+  load_span<E, S, 256>(row, tile0 * 256 * E::EPV, static_cast<int>(threadIdx.x), V, aligned, x);
 }
 
 // ---------------------------------------------------------------------------
@@ -492,78 +500,65 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat
   }
 }
 
-// Statistics at sub-chunk granularity: a task streams NT tiles of a row (a
-// long contiguous read per workgroup) and reports the statistics of each of
-// its NT/S sub-chunks of S tiles, one sub-chunk per load step, so that later
-// passes can select and re-read a short sub-chunk.  stats[r * Cs + c * NB + j]
-// holds sub-chunk j of task c of row r (Cs sub-chunks per row).
-template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void row_stats_sub_kernel(RowsDesc d, RowStat* __restrict__ stats, int ct,
-                                                                 int64_t ntasks) {
+// Statistics at sub-chunk granularity, one wave per sub-chunk: sub-chunk
+// g = blockIdx.x * kWaves + wave of the rows' C sub-chunks each (row g / C,
+// sub-chunk g % C) covers the ST tiles of 256 vectors from tile (g % C) * ST,
+// i.e. ST * 4 vectors of the wave's 64 lanes.  The wave streams them S vectors
+// per lane at a time, keeping a per-lane running reference (the largest
+// z * s so far) and the exp2 sum rescaled to it, then takes one wave maximum
+// and one float64 wave sum: no LDS and no barrier.  stats[g] = stats[r * C + j]
+// holds (m, D) of sub-chunk j of row r: m the largest z * s of the
+// sub-chunk (-inf if it has none), D = sum 2^(z s - m).
+template <class E, int ST, int S>
+__global__ __launch_bounds__(kThreads) void row_stats_wave_kernel(RowsDesc d, RowStat* __restrict__ stats,
+                                                                  int64_t nsub) {
   constexpr int EPV = E::EPV;
-  constexpr int NB = NT / S;
-  static_assert(NT % S == 0, "a task holds whole sub-chunks");
-  __shared__ RedLds<NB> red;
-  const int Cs = d.C;
-  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int r = static_cast<int>(t / ct), c = static_cast<int>(t - static_cast<int64_t>(t / ct) * ct);
-    int b;
-    bool aligned;
-    const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
-    const float T = temperature_of(d, b);
-    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-    const int tile0 = c * NT;
-    const int nt = min(NT, d.ntiles - tile0);
-    float ref[NB], dsum[NB];
+  constexpr int WV = ST * (kThreads / 64);  // wave vectors per sub-chunk
+  static_assert(WV % S == 0, "whole load steps per sub-chunk");
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  if (g >= nsub) return;  // the whole wave leaves: nothing below synchronises the workgroup
+  const int C = d.C;
+  const int r = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
+  int b;
+  bool aligned;
+  const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+  const float T = temperature_of(d, b);
+  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+  const int e0 = j * WV * 64 * EPV;
+  float ref = -INFINITY, acc = 0.f;
 #pragma unroll
-    for (int jb = 0; jb < NB; ++jb) {
-      ref[jb] = -INFINITY;
-      dsum[jb] = 0.f;
+  for (int st = 0; st < WV / S; ++st) {
+    const int es = e0 + st * S * 64 * EPV;
+    if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+    float x[S][EPV];
+    load_span<E, S, 64>(row, es, lane, d.V, aligned, x);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[i][k]);
+    const float nr = fmaxf(ref, mx * s);
+    if (nr != -INFINITY) {
+      float a2 = ref == -INFINITY ? 0.f : acc * __builtin_amdgcn_exp2f(ref - nr);
+#pragma unroll
+      for (int i = 0; i < S; ++i)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) a2 += __builtin_amdgcn_exp2f(fmaf(x[i][k], s, -nr));
+      acc = a2;
+      ref = nr;
     }
-    // one load step per sub-chunk; "break" (not "continue") keeps the next
-    // step's loads behind this step's work instead of all hoisted up front
-#pragma unroll
-    for (int jb = 0; jb < NB; ++jb) {
-      if (jb * S >= nt) break;
-      float x[S][EPV];
-      load_tiles<E, S>(row, tile0 + jb * S, d.V, aligned, x);
-      float mx = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < S; ++j)
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[j][k]);
-      if (mx != -INFINITY) {
-        const float rr = mx * s;
-        float acc = 0.f;
-#pragma unroll
-        for (int j = 0; j < S; ++j)
-#pragma unroll
-          for (int k = 0; k < EPV; ++k) acc += __builtin_amdgcn_exp2f(fmaf(x[j][k], s, -rr));
-        ref[jb] = rr;
-        dsum[jb] = acc;
-      }
-    }
-    float m[NB];
-#pragma unroll
-    for (int jb = 0; jb < NB; ++jb) m[jb] = ref[jb];
-    wg_max<NB>(m, red);
-    double dd[NB];
-#pragma unroll
-    for (int jb = 0; jb < NB; ++jb) {
-      if (dsum[jb] != dsum[jb]) dd[jb] = dsum[jb];  // NaN propagates (data error)
-      else if (ref[jb] == -INFINITY) dd[jb] = 0.0;
-      else dd[jb] = static_cast<double>(dsum[jb]) * static_cast<double>(__builtin_amdgcn_exp2f(ref[jb] - m[jb]));
-    }
-    wg_sum<NB>(dd, red);
-    if (threadIdx.x == 0) {
-#pragma unroll
-      for (int jb = 0; jb < NB; ++jb) {
-        if (jb * S >= nt) break;
-        RowStat o;
-        o.m = m[jb]; o.pad = 0.f; o.D = dd[jb];
-        stats[static_cast<int64_t>(r) * Cs + c * NB + jb] = o;
-      }
-    }
+  }
+  const float m = wave_max(ref);
+  double dd;
+  if (acc != acc) dd = acc;  // NaN propagates (data error)
+  else if (ref == -INFINITY) dd = 0.0;
+  else dd = static_cast<double>(acc) * static_cast<double>(__builtin_amdgcn_exp2f(ref - m));
+  dd = wave_sum(dd);
+  if (lane == 0) {
+    RowStat o;
+    o.m = m; o.pad = 0.f; o.D = dd;
+    stats[g] = o;
   }
 }
 

@@ -2,21 +2,22 @@
 // Eq. reject_sample; App. G.1, Alg. rs_multinomial) in four launches that
 // never wait on each other inside a launch:
 //
-//   1 row_stats   (sv_device.h) every target and draft row, split into
-//                 chunks of NT tiles: per-chunk (max reference, exp2 sum).
+//   1 row_stats   (sv_device.h) every target and draft row, one wave per
+//                 sub-chunk: per-sub-chunk (max reference, exp2 sum).
 //   2 decide      one workgroup per batch row: each row's normaliser from its
 //                 chunk statistics; the K accept tests in parallel lanes
 //                 (float64, u q(x) < p(x) with the two gathered logits and
 //                 Philox uniforms); accept length; every output except the
 //                 overlaps and the resampled token.
-//   3 pair_pass   every (target row i, draft row i) pair, chunk by chunk:
+//   3 pair_pass   every (target row i, draft row i) pair, one wave per
+//                 sub-chunk:
 //                 overlap sum min(p, q); for the row's first rejected step
 //                 also the residual mass sum max(0, p - q).  Bonus rows are
 //                 not read again, and without an overlap output only the
 //                 first rejected step's pair is.
 //   4 finish      one workgroup per batch row: overlaps; the chunk whose
 //                 cumulative residual (or bonus) mass crosses u' Z, found
-//                 from the per-chunk masses; only that chunk is read again
+//                 from the per-sub-chunk masses; only that one is read again
 //                 to invert the CDF inside it (tile sums, thread scan,
 //                 element scan).
 #pragma once
@@ -244,22 +245,23 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
   }
 }
 
-// The pair pass at sub-chunk granularity (pairs as row_stats_sub_kernel
-// lays out the statistics): a task streams NT tiles of a (target, draft)
-// pair and reports the overlap (and, at the first rejected step, the
-// residual mass) of each of its NT/S sub-chunks.
-template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void pair_pass_sub_kernel(VerifyArgs a, int ct, int64_t ntasks) {
+// Pass 2 with one wave per (pair, sub-chunk) item: item g = u * C + j is
+// sub-chunk j (ST tiles of 256 vectors, i.e. ST * 4 vectors of the wave's 64
+// lanes) of draft pair u = b * K + i.  The wave sums the overlap (and, for the
+// row's first rejected step, the residual mass) S vectors per lane at a time,
+// then one float64 wave sum per quantity: no LDS and no barrier.  Written
+// grid-stride over groups of kWaves items (launched one workgroup per group).
+template <class E, int ST, int S>
+__global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, int64_t nitems) {
   constexpr int EPV = E::EPV;
-  constexpr int NB = NT / S;
-  __shared__ RedLds<2 * NB> red2;
-  __shared__ RedLds<NB> red1;
+  constexpr int WV = ST * (kThreads / 64);
+  static_assert(WV % S == 0, "whole load steps per sub-chunk");
   const RowsDesc& d = a.rows;
-  const int Cs = d.C;
-  // persistent: the grid is sized to what the device holds at once and
-  // strides over the (pair, task) items
-  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int u = static_cast<int>(t / ct), c = static_cast<int>(t - static_cast<int64_t>(t / ct) * ct);
+  const int C = d.C;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave; g < nitems;
+       g += static_cast<int64_t>(gridDim.x) * kWaves) {
+    const int u = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
     const int b = u / a.K, i = u % a.K;
     const int n = a.decision[b];
     if (n < 0) continue;  // data error: finish ignores this row's partials
@@ -272,70 +274,36 @@ __global__ __launch_bounds__(kThreads) void pair_pass_sub_kernel(VerifyArgs a, i
     const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
     const float s = scale_of(temperature_of(d, b));
     const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-    const int tile0 = c * NT;
-    const int nt_tiles = min(NT, d.ntiles - tile0);
-    float al[NB], zr[NB];
+    const int e0 = j * WV * 64 * EPV;
+    float al = 0.f, zr = 0.f;
 #pragma unroll
-    for (int jb = 0; jb < NB; ++jb) {
-      al[jb] = 0.f;
-      zr[jb] = 0.f;
-    }
-#pragma unroll
-    for (int jb = 0; jb < NB; ++jb) {
-      if (jb * S >= nt_tiles) break;
+    for (int st = 0; st < WV / S; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
       float xt[S][EPV], xd[S][EPV];
-      load_tiles<E, S>(rt, tile0 + jb * S, d.V, al_t, xt);
-      load_tiles<E, S>(rd, tile0 + jb * S, d.V, al_d, xd);
+      load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
+      load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
       if (need_z) {
 #pragma unroll
-        for (int j = 0; j < S; ++j)
+        for (int q = 0; q < S; ++q)
 #pragma unroll
           for (int k = 0; k < EPV; ++k) {
-            const float p = prob(xt[j][k], s, nt.M, nt.invD);
-            const float mn = fminf(p, prob(xd[j][k], s, nd.M, nd.invD));
-            al[jb] += mn;
-            zr[jb] += p - mn;
+            const float p = prob(xt[q][k], s, nt.M, nt.invD);
+            const float mn = fminf(p, prob(xd[q][k], s, nd.M, nd.invD));
+            al += mn;
+            zr += p - mn;
           }
       } else {
 #pragma unroll
-        for (int j = 0; j < S; ++j)
+        for (int q = 0; q < S; ++q)
 #pragma unroll
-          for (int k = 0; k < EPV; ++k) al[jb] += min_prob(xt[j][k], xd[j][k], s, nt, nd);
+          for (int k = 0; k < EPV; ++k) al += min_prob(xt[q][k], xd[q][k], s, nt, nd);
       }
     }
-    PairStat* out = a.pairs + static_cast<int64_t>(u) * Cs + c * NB;
-    if (need_z) {
-      double v[2 * NB];
-#pragma unroll
-      for (int jb = 0; jb < NB; ++jb) {
-        v[jb] = static_cast<double>(al[jb]);
-        v[NB + jb] = static_cast<double>(zr[jb]);
-      }
-      wg_sum<2 * NB>(v, red2);
-      if (threadIdx.x == 0) {
-#pragma unroll
-        for (int jb = 0; jb < NB; ++jb) {
-          if (jb * S >= nt_tiles) break;
-          PairStat o;
-          o.alpha = v[jb]; o.Z = v[NB + jb];
-          out[jb] = o;
-        }
-      }
-    } else {
-      double v[NB];
-#pragma unroll
-      for (int jb = 0; jb < NB; ++jb) v[jb] = static_cast<double>(al[jb]);
-      wg_sum<NB>(v, red1);
-      if (threadIdx.x == 0) {
-#pragma unroll
-        for (int jb = 0; jb < NB; ++jb) {
-          if (jb * S >= nt_tiles) break;
-          PairStat o;
-          o.alpha = v[jb]; o.Z = 0.0;
-          out[jb] = o;
-        }
-      }
-    }
+    PairStat o;
+    o.alpha = wave_sum(static_cast<double>(al));
+    o.Z = need_z ? wave_sum(static_cast<double>(zr)) : 0.0;
+    if (lane == 0) a.pairs[g] = o;
   }
 }
 
