@@ -11,7 +11,8 @@ step from the previous one.
 Prints ONE JSON line.  `value` = verified draft tokens/s = B*K / step time.
 `roofline` relates the algorithmic bytes of one call (the logits it must
 read once, ids and outputs) to the call time measured with HIP events on the
-launch stream.  `cpu_baseline` times the float64 CPU oracle on a bounded
+launch stream; `ms_per_call_distribution` gives p10 / median / p90 of single
+calls from a separate pass with an event between calls.  `cpu_baseline` times the float64 CPU oracle on a bounded
 sample of rows of the same workload, and `parity` compares the oracle's
 pass over every row of that batch with the library's outputs for it.  The fused TV-loss forward+backward on the training
 workload (N=16384 positions x 3 steps) is timed too and reported under
@@ -139,6 +140,16 @@ def parity_summary(gpu_out, ref_chunks, K, boundary=1e-6):
             "against": "float64 CPU oracle, seed 0, offset 0, every row of the batch"}
 
 
+def quantile(sorted_vals, q):
+    """Linear-interpolation quantile of an ascending list."""
+    if not sorted_vals:
+        return None
+    x = q * (len(sorted_vals) - 1)
+    i = int(x)
+    j = min(i + 1, len(sorted_vals) - 1)
+    return sorted_vals[i] + (sorted_vals[j] - sorted_vals[i]) * (x - i)
+
+
 def timed(torch, stream, fn, steps):
     """Mean milliseconds of fn(it) over `steps` calls, HIP events on `stream`."""
     fn(0)
@@ -254,7 +265,10 @@ def bench_verify_context(torch, binding, W, copies, stream, steps):
     for key in ("rollout_bf16_b64_k3_v151936", "large_bf16_b1024_k3_v262144"):
         c2 = W.CONFIGS[key]
         B2, K2, V2 = c2["B"], c2["K"], c2["V"]
-        cps = [W.verify_inputs_torch(B2, K2, V2, W.BF16, c2["gen"], c2["seed"] + 100 * i) for i in range(2)]
+        # enough copies that the 256 MB Infinity Cache cannot hold the inputs of
+        # the previous calls (4 x 136 MB for B=64; 2 x 3.8 GB for B=1024)
+        ncp = 4 if B2 * (2 * K2 + 1) * V2 * 2 < (512 << 20) else 2
+        cps = [W.verify_inputs_torch(B2, K2, V2, W.BF16, c2["gen"], c2["seed"] + 100 * i) for i in range(ncp)]
         o2 = {"accept_len": torch.empty(B2, dtype=torch.int32, device="cuda"),
               "emitted": torch.empty((B2, K2 + 1), dtype=torch.int32, device="cuda"),
               "overlap": torch.empty((B2, K2), dtype=torch.float32, device="cuda")}
@@ -264,7 +278,8 @@ def bench_verify_context(torch, binding, W, copies, stream, steps):
             binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=o2)
 
         ms = timed(torch, stream, step2, steps)
-        out["verify_" + key] = {"ms_per_call": ms, "verified_draft_tokens_per_s": B2 * K2 / (ms * 1e-3),
+        out["verify_" + key] = {"ms_per_call": ms, "input_copies": ncp,
+                                "verified_draft_tokens_per_s": B2 * K2 / (ms * 1e-3),
                                 "roofline": hbm_roofline(verify_bytes(B2, K2, V2), ms, None)}
         del cps
     torch.cuda.empty_cache()
@@ -384,6 +399,17 @@ def main():
             "mean_accept_len": float(acc.mean()),
             "wall_s_timed_region": wall,
         })
+        # per-call distribution, from a separate pass with an event between calls
+        n_dist = min(args.steps, 100)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_dist + 1)]
+        evs[0].record(stream)
+        for it in range(n_dist):
+            step(it)
+            evs[it + 1].record(stream)
+        torch.cuda.synchronize()
+        per_call = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(n_dist))
+        result["ms_per_call_distribution"] = {"calls": n_dist, "p10": quantile(per_call, 0.10),
+                                              "median": quantile(per_call, 0.50), "p90": quantile(per_call, 0.90)}
         del outs
         if not args.no_context:
             log("timing spec_verify without overlaps and on the B=64 and B=1024 batches")

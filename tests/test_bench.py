@@ -1,6 +1,7 @@
 """bench.py's host logic, on the CPU: the one-GPU refusal, the parity
 summary's classification of rows, the algorithmic byte count of the
-headline call and the counter-traffic lookup tied to the kernel sources."""
+headline call, the quantiles of the per-call distribution and the
+counter-traffic lookup tied to the kernel sources."""
 
 import json
 import os
@@ -67,3 +68,18 @@ def test_traffic_is_reported_only_for_the_profiled_sources(tmp_path, monkeypatch
     assert bench.measured_traffic("missing", 0) is None
     assert bench.hbm_roofline(8e9, 1.0, None)["traffic"] is None
     assert bench.hbm_roofline(8e9, 1.0, None)["frac"] == pytest.approx(1.0)
+
+
+def test_quantiles_of_the_per_call_distribution():
+    vals = sorted([4.0, 1.0, 3.0, 2.0, 5.0])
+    assert bench.quantile(vals, 0.5) == 3.0
+    assert bench.quantile(vals, 0.0) == 1.0 and bench.quantile(vals, 1.0) == 5.0
+    assert bench.quantile(vals, 0.1) == pytest.approx(1.4)  # linear between the first two
+    assert bench.quantile(vals, 0.9) == pytest.approx(4.6)
+    assert bench.quantile([7.0], 0.9) == 7.0
+    assert bench.quantile([], 0.5) is None
+    # agrees with numpy's default (linear) quantile
+    rng = np.random.default_rng(3)
+    x = sorted(rng.random(101).tolist())
+    for q in (0.1, 0.5, 0.9):
+        assert bench.quantile(x, q) == pytest.approx(float(np.quantile(x, q)))
