@@ -26,13 +26,14 @@ using sv::F32;
 constexpr int kNtBf16 = 8;
 constexpr int kNtF32 = 16;
 constexpr int kStep = 4;
-// Multinomial verification, target-only verification and the sampler keep
-// statistics per sub-chunk of kStep tiles (8192 bf16 or 4096 fp32 elements),
-// which is what their per-row launches read again; one wave streams one
-// sub-chunk, kStatVec (statistics) or kPairVec (pair pass) vectors per lane
-// at a time.
+// Multinomial verification, target-only verification, the sampler and the
+// diagnostics keep statistics per sub-chunk of kStep tiles (8192 bf16 or 4096
+// fp32 elements), which is what their per-row launches read again; one wave
+// streams one sub-chunk, kStatVec (statistics), kPairVec (verification pair
+// pass) or kDiagPairVec (diagnostics pair pass) vectors per lane at a time.
 constexpr int kStatVec = 8;
 constexpr int kPairVec = 4;
+constexpr int kDiagPairVec = 2;
 constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
 static_assert(kNtF32 * sv::kThreads * sv::F32::EPV == kChunkElems, "chunk geometry");
@@ -160,7 +161,7 @@ struct DiagLayout {
 };
 DiagLayout diag_layout(int B, int K, int V, spec_dtype dt) {
   DiagLayout L;
-  const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t C = static_cast<size_t>(sub_chunks(V, dt));
   const size_t rows = static_cast<size_t>(B) * 2 * K;
   size_t off = 0;
   L.stats = off; off = align_up(off + rows * C * sizeof(sv::DiagStat), 256);
@@ -317,18 +318,21 @@ spec_status launch_sample(const sv::SampleArgs& a, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
 }
 
-template <class E, int NT>
+// Diagnostics per sub-chunk of kStep tiles, one wave per sub-chunk in both
+// streaming passes.
+template <class E>
 spec_status launch_diag(const sv::DiagArgs& a, hipStream_t s) {
   const int C = a.rows.C;
   const int64_t units = int64_t{a.B} * a.K;
-  void (*ds)(sv::RowsDesc, sv::DiagStat*, int64_t) = sv::diag_stats_kernel<E, NT, kStep>;
-  hipLaunchKernelGGL(ds, dim3(static_cast<unsigned>(2 * units * C)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::DiagStat*>(a.stats), 2 * units * C);
+  const int64_t nsub = 2 * units * C;
+  hipLaunchKernelGGL((sv::diag_stats_wave_kernel<E, kStep, kStatVec>),
+                     dim3(static_cast<unsigned>((nsub + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s,
+                     a.rows, const_cast<sv::DiagStat*>(a.stats), nsub);
   hipLaunchKernelGGL(sv::diag_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C, a.norms, a.info);
-  void (*dp)(sv::DiagArgs, int64_t) = sv::diag_pair_kernel<E, NT, kStep>;
-  hipLaunchKernelGGL(dp, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a,
-                     units * C);
+  hipLaunchKernelGGL((sv::diag_pair_wave_kernel<E, kStep, kDiagPairVec>),
+                     dim3(static_cast<unsigned>((units * C + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0,
+                     s, a, units * C);
   hipLaunchKernelGGL((sv::diag_finish_kernel<E>), dim3(static_cast<unsigned>((units + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
@@ -609,7 +613,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
 
 size_t spec_diagnostics_workspace_size(int B, int K, int V, spec_dtype dtype) {
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return 0;
-  if (B < 1 || K < 1 || K > SPEC_MAX_K || !rows_ok(int64_t{B} * 2 * K, V, dtype)) return 0;
+  if (B < 1 || K < 1 || K > SPEC_MAX_K || !rows_sub_ok(int64_t{B} * 2 * K, V, dtype)) return 0;
   return diag_layout(B, K, V, dtype).total;
 }
 
@@ -620,7 +624,7 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
                              void* stream) {
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
   if (K > SPEC_MAX_K) return SPEC_EUNSUPPORTED;
-  if (B < 1 || K < 1 || !rows_ok(int64_t{B} * 2 * K, V, dtype)) return SPEC_EINVAL;
+  if (B < 1 || K < 1 || !rows_sub_ok(int64_t{B} * 2 * K, V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_logits || !diag) return SPEC_EINVAL;
   if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
@@ -635,7 +639,7 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
   a.rows.drf = draft_logits; a.rows.dsb = d_stride_b; a.rows.dsk = d_stride_k; a.rows.dper = K;
   a.rows.nb = B;
   a.rows.temp = temperature; a.rows.temp_scalar = temperature_scalar;
-  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = g.C;
+  a.rows.V = V; a.rows.ntiles = g.ntiles; a.rows.C = sub_chunks(V, dtype);
   a.rows.vec_t = rows_vec_aligned(target_logits, t_stride_b, t_stride_k, es) ? 1 : 0;
   a.rows.vec_d = rows_vec_aligned(draft_logits, d_stride_b, d_stride_k, es) ? 1 : 0;
   a.B = B; a.K = K;
@@ -646,7 +650,7 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
   a.info = reinterpret_cast<sv::DiagRow*>(ws + L.info);
   a.pairs = reinterpret_cast<sv::DiagPair*>(ws + L.pairs);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_diag<BF16, kNtBf16>(a, s) : launch_diag<F32, kNtF32>(a, s);
+  return dtype == SPEC_BF16 ? launch_diag<BF16>(a, s) : launch_diag<F32>(a, s);
 }
 
 size_t spec_kl_workspace_size(int N, int K, int V, spec_dtype dtype) {

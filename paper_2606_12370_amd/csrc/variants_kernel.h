@@ -12,9 +12,10 @@
 //   per-step diagnostics (Sec. 3; App. E): entropies of p_i and q_i, max p_i,
 //     the greedy draft token and alpha^TO = p_i(argmax q_i), alpha^RS =
 //     sum min(p_i, q_i) split into sum_{p>q} q and sum_{q>=p} p.  Four
-//     launches: diag_stats (per chunk: max reference, exp2 sum, the entropy
-//     moment, largest logit and its first index), diag_norm (one wave per
-//     row), diag_pair (per pair chunk), diag_finish (one wave per step).
+//     launches: diag_stats (one wave per sub-chunk: max reference, exp2 sum,
+//     the entropy moment, largest logit and its first index), diag_norm (one
+//     wave per row), diag_pair (one wave per pair sub-chunk), diag_finish
+//     (one wave per step).
 #pragma once
 
 #include <cfloat>
@@ -277,12 +278,12 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(SampleArgs a) {
 // ---------------------------------------------------------------------------
 // per-step diagnostics
 
-// One chunk of one row.  With a_v = z_v s (log2 units) and the reference m:
+// One sub-chunk of one row.  With a_v = z_v s (log2 units) and the reference m:
 // D = sum 2^(a_v - m), Em = sum 2^(a_v - m) (a_v - m), so that over a whole
 // row with reference M the entropy in nats is ln2 (log2 D - Em / D).
 struct DiagStat {
-  float m;     // largest thread reference (log2 units), -inf: chunk without mass
-  float zmax;  // largest logit of the chunk
+  float m;     // largest lane reference (log2 units), -inf: sub-chunk without mass
+  float zmax;  // largest logit of the sub-chunk
   int arg;     // its first index
   int pad;
   double D;
@@ -295,7 +296,7 @@ struct DiagRow {   // one row, combined
   int arg;
 };
 
-struct DiagPair {  // one chunk of a (target, draft) pair
+struct DiagPair {  // one sub-chunk of a (target, draft) pair
   double gt;       // sum over p > q of q
   double ge;       // sum over q >= p of p
 };
@@ -314,95 +315,159 @@ struct DiagArgs {
   DiagPair* pairs;        // [BK][C]
 };
 
-template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void diag_stats_kernel(RowsDesc d, DiagStat* __restrict__ stats,
-                                                              int64_t ntasks) {
+// Per-sub-chunk diagnostics statistics, one wave per sub-chunk: sub-chunk
+// g = blockIdx.x * kWaves + wave of the rows' C sub-chunks each (row g / C,
+// sub-chunk g % C) covers ST tiles of 256 vectors, i.e. ST * 4 vectors of the
+// wave's 64 lanes, streamed S vectors per lane at a time.  Per lane: a running
+// reference r (the largest z * s so far), D = sum 2^(z s - r) and the entropy
+// moment E = sum 2^(z s - r) (z s - r), both rescaled when r grows, and the
+// largest logit with the load step where it first appears.  Then one wave
+// maximum of r and of the largest logit, float64 wave sums of the rescaled D
+// and E, and the first index of the largest logit from the lanes that hold it
+// (each reads that one load step again, from cache): no LDS, no barrier.
+template <class E, int ST, int S>
+__global__ __launch_bounds__(kThreads) void diag_stats_wave_kernel(RowsDesc d, DiagStat* __restrict__ stats,
+                                                                   int64_t nsub) {
   constexpr int EPV = E::EPV;
-  constexpr int TILE = kThreads * EPV;
-  __shared__ RedLds<4> red;
-  __shared__ RedLds<1> red1;
-  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int r = static_cast<int>(t / d.C), c = static_cast<int>(t - static_cast<int64_t>(t / d.C) * d.C);
-    int b;
-    bool aligned;
-    const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
-    const float T = temperature_of(d, b);
-    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-    const int tile0 = c * NT;
-    const int nt = min(NT, d.ntiles - tile0);
-    float ref = -INFINITY, dsum = 0.f, esum = 0.f, zmax = -INFINITY;
+  constexpr int WV = ST * (kThreads / 64);
+  static_assert(WV % S == 0, "whole load steps per sub-chunk");
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  if (g >= nsub) return;  // the whole wave leaves: nothing below synchronises the workgroup
+  const int C = d.C;
+  const int r = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
+  int b;
+  bool aligned;
+  const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+  const float T = temperature_of(d, b);
+  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+  const int e0 = j * WV * 64 * EPV;
+  float ref = -INFINITY, dsum = 0.f, esum = 0.f, zmax = -INFINITY;
+  int zstep = -1;
 #pragma unroll
-    for (int j0 = 0; j0 < NT; j0 += S) {
-      if (j0 >= nt) break;
-      float x[S][EPV];
-      load_tiles<E, S>(row, tile0 + j0, d.V, aligned, x);
-      float mx = -INFINITY;
+  for (int st = 0; st < WV / S; ++st) {
+    const int es = e0 + st * S * 64 * EPV;
+    if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+    float x[S][EPV];
+    load_span<E, S, 64>(row, es, lane, d.V, aligned, x);
+    float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < S; ++j)
+    for (int i = 0; i < S; ++i)
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[j][k]);
-      zmax = fmaxf(zmax, mx);
-      if (mx != -INFINITY) {
-        const float rr = mx * s;
-        float acc = 0.f, acce = 0.f;
+      for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[i][k]);
+    if (mx > zmax) { zmax = mx; zstep = st; }
+    const float nr = fmaxf(ref, mx * s);
+    if (nr != -INFINITY) {
+      float acc = 0.f, acce = 0.f;
 #pragma unroll
-        for (int j = 0; j < S; ++j)
+      for (int i = 0; i < S; ++i)
 #pragma unroll
-          for (int k = 0; k < EPV; ++k) {
-            const float tv = fmaf(x[j][k], s, -rr);
-            const float e = __builtin_amdgcn_exp2f(tv);
-            acc += e;
-            // e * tv, with a masked token's -inf exponent clamped so that 0 * tv stays 0
-            acce = fmaf(e, fmaxf(tv, -FLT_MAX), acce);
-          }
-        if (ref == -INFINITY) {
-          ref = rr; dsum = acc; esum = acce;
-        } else if (rr > ref) {
-          const float f = __builtin_amdgcn_exp2f(ref - rr);
-          esum = f * (esum + (ref - rr) * dsum) + acce;
-          dsum = dsum * f + acc;
-          ref = rr;
-        } else {
-          const float f = __builtin_amdgcn_exp2f(rr - ref);
-          dsum += acc * f;
-          esum += f * (acce + (rr - ref) * acc);
+        for (int k = 0; k < EPV; ++k) {
+          const float tv = fmaf(x[i][k], s, -nr);
+          const float e = __builtin_amdgcn_exp2f(tv);
+          acc += e;
+          // e * tv, with a masked token's -inf exponent clamped so that 0 * tv stays 0
+          acce = fmaf(e, fmaxf(tv, -FLT_MAX), acce);
         }
+      if (ref == -INFINITY) {
+        dsum = acc; esum = acce;
+      } else {  // nr >= ref: bring the running sums to the new reference
+        const float sh = ref - nr;
+        const float f = __builtin_amdgcn_exp2f(sh);
+        esum = f * (esum + sh * dsum) + acce;
+        dsum = dsum * f + acc;
       }
+      ref = nr;
     }
-    float m4[4] = {ref, zmax, -INFINITY, -INFINITY};
-    wg_max<4>(m4, red);
-    double d4[4] = {0.0, 0.0, 0.0, 0.0};
-    if (dsum != dsum || esum != esum) {
-      d4[0] = NAN;  // data error propagates
-    } else if (ref != -INFINITY) {
-      const double f = static_cast<double>(__builtin_amdgcn_exp2f(ref - m4[0]));
-      const double sh = static_cast<double>(ref) - static_cast<double>(m4[0]);
-      d4[0] = static_cast<double>(dsum) * f;
-      d4[1] = f * (static_cast<double>(esum) + sh * static_cast<double>(dsum));
-    }
-    wg_sum<4>(d4, red);
-    // first index of the chunk's largest logit: only the threads that hold it
-    // look through their elements again (ascending, so the first equal one)
-    int arg = 0x7fffffff;
-    if (zmax == m4[1] && zmax != -INFINITY) {
+  }
+  const float m = wave_max(ref);
+  const float zm = wave_max(zmax);
+  double dd = 0.0, de = 0.0;
+  if (dsum != dsum || esum != esum) {
+    dd = NAN;  // data error propagates
+  } else if (ref != -INFINITY) {
+    const double f = static_cast<double>(__builtin_amdgcn_exp2f(ref - m));
+    const double sh = static_cast<double>(ref) - static_cast<double>(m);
+    dd = static_cast<double>(dsum) * f;
+    de = f * (static_cast<double>(esum) + sh * static_cast<double>(dsum));
+  }
+  dd = wave_sum(dd);
+  de = wave_sum(de);
+  // first index of the sub-chunk's largest logit: the lanes that hold it scan
+  // the load step where it first appears, ascending
+  int arg = 0x7fffffff;
+  if (zmax == zm && zm != -INFINITY) {
 #pragma unroll
-      for (int j0 = 0; j0 < NT; j0 += S) {
-        if (j0 >= nt || arg != 0x7fffffff) break;
+    for (int st = 0; st < WV / S; ++st)
+      if (st == zstep) {
+        const int es = e0 + st * S * 64 * EPV;
         float x[S][EPV];
-        load_tiles<E, S>(row, tile0 + j0, d.V, aligned, x);  // one load step, from L2
+        load_span<E, S, 64>(row, es, lane, d.V, aligned, x);
 #pragma unroll
-        for (int j = S - 1; j >= 0; --j)
+        for (int i = S - 1; i >= 0; --i)
 #pragma unroll
           for (int k = EPV - 1; k >= 0; --k)
-            if (x[j][k] == zmax) arg = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV + k;
+            if (x[i][k] == zm) arg = es + i * 64 * EPV + lane * EPV + k;
       }
-    }
-    const int a1 = wg_min_int(arg, red1);
-    if (threadIdx.x == 0) {
-      DiagStat o;
-      o.m = m4[0]; o.zmax = m4[1]; o.arg = a1; o.pad = 0; o.D = d4[0]; o.Em = d4[1];
-      stats[t] = o;
-    }
+  }
+  arg = wave_min_int(arg);
+  if (lane == 0) {
+    DiagStat o;
+    o.m = m; o.zmax = zm; o.arg = arg; o.pad = 0; o.D = dd; o.Em = de;
+    stats[g] = o;
+  }
+}
+
+// Split overlap sums, one wave per (pair, sub-chunk) item: item g = u * C + j
+// is sub-chunk j of pair u (target row u, draft row B*K + u of the
+// diagnostics row layout); gt = sum over p > q of q, ge = sum over q >= p of
+// p, S vectors of each row per lane per load step, then float64 wave sums.
+// One exponential per element pair: with x = log2 p and y = log2 q,
+// 2^min(x, y) is q where x > y and p elsewhere, so x > y routes it.
+template <class E, int ST, int S>
+__global__ __launch_bounds__(kThreads) void diag_pair_wave_kernel(DiagArgs a, int64_t nitems) {
+  constexpr int EPV = E::EPV;
+  constexpr int WV = ST * (kThreads / 64);
+  static_assert(WV % S == 0, "whole load steps per sub-chunk");
+  const RowsDesc& d = a.rows;
+  const int C = d.C, BK = a.B * a.K;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  if (g >= nitems) return;  // the whole wave leaves: nothing below synchronises the workgroup
+  const int u = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
+  int b;
+  bool al_t, al_d;
+  const typename E::raw* rt = row_of<E>(d, u, &b, &al_t);
+  const typename E::raw* rd = row_of<E>(d, BK + u, &b, &al_d);
+  const float T = temperature_of(d, b);
+  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+  const RowNorm nt = a.norms[u], nd = a.norms[BK + u];
+  const int e0 = j * WV * 64 * EPV;
+  float gt = 0.f, ge = 0.f;
+#pragma unroll
+  for (int st = 0; st < WV / S; ++st) {
+    const int es = e0 + st * S * 64 * EPV;
+    if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+    float xt[S][EPV], xd[S][EPV];
+    load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
+    load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) {
+        const float lp = fmaf(xt[i][k], s, -nt.M) - nt.L;
+        const float lq = fmaf(xd[i][k], s, -nd.M) - nd.L;
+        const float mn = __builtin_amdgcn_exp2f(fminf(lp, lq));
+        if (lp > lq) gt += mn;
+        else ge += mn;
+      }
+  }
+  const double vgt = wave_sum(static_cast<double>(gt));
+  const double vge = wave_sum(static_cast<double>(ge));
+  if (lane == 0) {
+    DiagPair o;
+    o.gt = vgt; o.ge = vge;
+    a.pairs[g] = o;
   }
 }
 
@@ -443,51 +508,6 @@ __global__ __launch_bounds__(kThreads) void diag_norm_kernel(const DiagStat* __r
     o.zmax = zm;
     o.arg = arg;
     info[r] = o;
-  }
-}
-
-// Second read of each (target, draft) pair chunk: the overlap split by the larger side.
-template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void diag_pair_kernel(DiagArgs a, int64_t ntasks) {
-  constexpr int EPV = E::EPV;
-  __shared__ RedLds<4> red;
-  const RowsDesc& d = a.rows;
-  const int C = d.C, BK = a.B * a.K;
-  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
-    int b;
-    bool al_t, al_d;
-    const typename E::raw* rt = row_of<E>(d, u, &b, &al_t);
-    const typename E::raw* rd = row_of<E>(d, BK + u, &b, &al_d);
-    const float T = temperature_of(d, b);
-    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-    const RowNorm nt = a.norms[u], nd = a.norms[BK + u];
-    const int tile0 = c * NT;
-    const int nt_tiles = min(NT, d.ntiles - tile0);
-    float gt = 0.f, ge = 0.f;
-#pragma unroll
-    for (int j0 = 0; j0 < NT; j0 += S) {
-      if (j0 >= nt_tiles) break;
-      float xt[S][EPV], xd[S][EPV];
-      load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
-      load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
-#pragma unroll
-      for (int j = 0; j < S; ++j)
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          const float p = prob(xt[j][k], s, nt.M, nt.invD);
-          const float q = prob(xd[j][k], s, nd.M, nd.invD);
-          if (p > q) gt += q;
-          else ge += p;
-        }
-    }
-    double v[4] = {static_cast<double>(gt), static_cast<double>(ge), 0.0, 0.0};
-    wg_sum<4>(v, red);
-    if (threadIdx.x == 0) {
-      DiagPair o;
-      o.gt = v[0]; o.ge = v[1];
-      a.pairs[t] = o;
-    }
   }
 }
 
