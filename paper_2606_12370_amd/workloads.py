@@ -125,6 +125,47 @@ def verify_inputs_numpy(B, K, V, dtype, gen, seed, shared_target=False, q_equals
     return dict(target=tgt, draft=drf, ids=ids, temperature=T, dtype=dtype, B=B, K=K, V=V)
 
 
+def masked_verify_inputs_numpy(B, K, V, dtype, seed):
+    """Rollout-shaped verify inputs with -inf masks (masked tokens, p = 0),
+    one of five patterns per batch row (b % 5):
+      0  target rows masked on [0, 5000), draft rows on [8192, 16384);
+      1  the same random support of 50 tokens in target and draft;
+      2  random supports of 200 tokens, target and draft sharing half;
+      3  draft rows masked beyond the first 3000 tokens;
+      4  target rows masked on every other 512-token block.
+    Draft ids are drawn from the masked draft distribution.  V >= 16384."""
+    d = verify_inputs_numpy(B, K, V, dtype, "rollout_t", seed)
+    tgt = to_float64(d["target"], dtype).astype(np.float32)
+    drf = to_float64(d["draft"], dtype).astype(np.float32)
+    rng = np.random.default_rng(seed + 11)
+    for b in range(B):
+        pat = b % 5
+        if pat == 0:
+            tgt[b, :, :5000] = -np.inf
+            drf[b, :, 8192:16384] = -np.inf
+        elif pat == 1:
+            keep = rng.choice(V, size=50, replace=False)
+            m = np.ones(V, bool); m[keep] = False
+            tgt[b, :, m] = -np.inf
+            drf[b, :, m] = -np.inf
+        elif pat == 2:
+            both = rng.choice(V, size=300, replace=False)
+            mt = np.ones(V, bool); mt[both[:200]] = False
+            md = np.ones(V, bool); md[both[100:]] = False
+            tgt[b, :, mt] = -np.inf
+            drf[b, :, md] = -np.inf
+        elif pat == 3:
+            drf[b, :, 3000:] = -np.inf
+        else:
+            blocks = (np.arange(V) // 512) % 2 == 1
+            tgt[b, :, blocks] = -np.inf
+    d["target"] = _store(tgt, dtype)
+    d["draft"] = _store(drf, dtype)
+    id_rng = np.random.default_rng(seed + 13)
+    d["ids"] = _gumbel_ids(id_rng, to_float64(d["draft"], dtype), d["temperature"].astype(np.float64)[:, None, None])
+    return d
+
+
 def greedy_ids(draft, dtype):
     """The draft's greedy tokens (first index of each row's largest stored
     logit), the draft choice target-only verification assumes."""

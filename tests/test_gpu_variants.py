@@ -166,6 +166,23 @@ def run_sample(z, T, dtype, seed=0, offset=0, rows_view=None):
 
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_target_only_masked_vocabularies(dtype):
+    d = W.masked_verify_inputs_numpy(15, 3, 20000, dtype, 43)
+    out, ref = run_to(d, W.greedy_ids(d["draft"], dtype), seed=5, offset=2)
+    compare_target_only(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_sample_masked_vocabularies(dtype):
+    d = W.masked_verify_inputs_numpy(15, 2, 20000, dtype, 44)
+    z = W.to_float64(d["draft"], dtype).astype(np.float32).reshape(-1, 20000)
+    T = np.repeat(d["temperature"], 2).astype(np.float32)
+    T[::7] = 0.0  # greedy rows
+    out, ref = run_sample(z, T, dtype, seed=6, offset=3)
+    compare_sample(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("R,V", [(40, 1024), (9, 20000), (17, 2049), (5, 7), (4, 1), (6, 65536 + 24),
                                  (2, 256 * 8192 + 8195)])
 def test_sample_ragged(dtype, R, V):
@@ -272,6 +289,35 @@ def test_diagnostics_controls_and_errors():
     g = out["greedy_draft"].cpu().numpy()
     assert g[0, 0] == 123 and g[1, 0] == 700
     assert list(out["rs_preferred"].cpu().numpy()[2:, 0]) == [-1, -1, -1]
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_diagnostics_greedy_ties_inside_a_subchunk(dtype):
+    """Ties of the draft's largest logit inside one 8192-element (bf16) or
+    4096-element (fp32) sub-chunk: in one lane at two load steps, in several
+    lanes and vectors of one step, at the last element of a sub-chunk against
+    the next sub-chunk, and at every 37th element.  The greedy token is the
+    first index among the ties."""
+    V = 20000
+    ties = [[4100, 1030, 517, 3000], [9000, 8191], [6000, 4096, 4097], [2055, 2047, 5000], list(range(0, V, 37))]
+    z = np.random.default_rng(5).normal(0.0, 1.0, (len(ties), 1, V)).astype(np.float32)
+    zd = np.random.default_rng(6).normal(0.0, 1.0, (len(ties), 1, V)).astype(np.float32)
+    for r, pos in enumerate(ties):
+        zd[r, 0, pos] = 8.0
+    d = dict(target=W.f32_to_bf16_bits(z) if dtype == W.BF16 else z,
+             draft=W.f32_to_bf16_bits(zd) if dtype == W.BF16 else zd,
+             temperature=np.ones(len(ties), np.float32), dtype=dtype)
+    out, ref = run_diag(d)
+    compare_diagnostics(out, ref, dtype)
+    assert list(out["greedy_draft"].cpu().numpy()[:, 0]) == [min(p) for p in ties]
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_diagnostics_masked_vocabularies(dtype):
+    d = W.masked_verify_inputs_numpy(15, 3, 20000, dtype, 45)
+    d["target"] = np.ascontiguousarray(d["target"][:, :3])  # rows i < K
+    out, ref = run_diag(d)
+    compare_diagnostics(out, ref, dtype)
 
 
 def test_diagnostics_benchmark_batch_sampled_rows():

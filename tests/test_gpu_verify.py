@@ -126,6 +126,17 @@ def test_row_data_errors(dtype):
 
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_masked_vocabularies(dtype):
+    """-inf masks (masked tokens, p = 0) that empty whole load steps and
+    sub-chunks, sparse supports shared or half-shared by target and draft,
+    and block masks: every row is valid and must match the oracle."""
+    d = W.masked_verify_inputs_numpy(15, 3, 20000, dtype, 41)
+    out, ref = run_numpy_case(d, seed=3, offset=1)
+    assert not ref["row_error"].any()
+    compare_verify(out, ref, dtype)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 def test_unaligned_strided_views(dtype):
     """Rows that are not 16-byte aligned and non-contiguous batch strides take
     the element-wise load path; results must not change."""
