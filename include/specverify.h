@@ -53,6 +53,9 @@ extern "C" {
 
 #define SPEC_VERSION 1
 #define SPEC_MAX_K 8 /* largest number of draft steps K */
+/* largest vocabulary V (2^31 - 2^16): element indices are 32-bit and run one
+ * 16384-element chunk past V where a row's last chunk is rounded up */
+#define SPEC_MAX_V 2147418112
 
 typedef enum { SPEC_F32 = 0, SPEC_BF16 = 1 } spec_dtype;
 
@@ -112,7 +115,7 @@ size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
  * outside [0, V), a per-row temperature that is not finite and > 0) do not
  * fail the call: that row gets accept_len = -1, emitted = -1 and NaN in every
  * float output.  -inf logits are legal (probability 0).
- * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= B, B*(K+1) < 2^31.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V <= SPEC_MAX_V, 1 <= B, B*(K+1) < 2^31.
  */
 spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
                         const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
@@ -149,7 +152,7 @@ size_t spec_tv_workspace_size(int N, int K, int V, spec_dtype dtype);
  * grad_draft     [N, K, V] float32 out, contiguous; NULL = forward only
  * NaN or infinite logits propagate as NaN into that position's loss and
  * gradient (no per-position status).
- * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= N, N*K < 2^31.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V <= SPEC_MAX_V, 1 <= N, N*K < 2^31.
  */
 spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,
                                  const void* draft_logits, int64_t d_stride_n, int64_t d_stride_k,
@@ -200,7 +203,7 @@ size_t spec_sample_gumbel_workspace_size(int R, int V, spec_dtype dtype);
  * logits [R, V] with row stride stride_r; temperature [R] or NULL (scalar,
  * finite, >= 0); tokens [R] int32 out.  Row data errors (NaN or +inf
  * logits, all -inf, a negative or non-finite per-row temperature) give -1.
- * Limits: 1 <= R, 1 <= V < 2^31.
+ * Limits: 1 <= R, 1 <= V <= SPEC_MAX_V.
  */
 spec_status spec_sample_gumbel(const void* logits, int64_t stride_r, spec_dtype dtype, int R, int V,
                                const float* temperature, float temperature_scalar,
@@ -235,7 +238,7 @@ size_t spec_verify_target_only_workspace_size(int B, int K, int V, spec_dtype dt
  * logz_target    [B, K+1] float32 out: natural-log partition function of z/T (may be NULL)
  * workspace      device memory of at least spec_verify_target_only_workspace_size bytes
  * Row data errors behave as in spec_verify (accept_len = -1, emitted = -1, NaN).
- * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= B.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V <= SPEC_MAX_V, 1 <= B.
  */
 spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
                                     spec_dtype dtype, int B, int K, int V,
@@ -269,7 +272,7 @@ size_t spec_sample_workspace_size(int R, int V, spec_dtype dtype);
  * workspace    device memory of at least spec_sample_workspace_size bytes
  * Row data errors (NaN or +inf logits, all -inf, a per-row temperature that
  * is negative or not finite) give tokens[r] = -1 and logz[r] = NaN.
- * Limits: 1 <= R, 1 <= V < 2^31.
+ * Limits: 1 <= R, 1 <= V <= SPEC_MAX_V.
  */
 spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, int R, int V,
                         const float* temperature, float temperature_scalar,
@@ -313,7 +316,7 @@ size_t spec_diagnostics_workspace_size(int B, int K, int V, spec_dtype dtype);
  * workspace      device memory of at least spec_diagnostics_workspace_size bytes
  * Row data errors (as in spec_verify, without draft ids) give NaN in every
  * column, greedy_draft = -1 and rs_preferred = -1.
- * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= B.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V <= SPEC_MAX_V, 1 <= B.
  */
 spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
                              const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
@@ -348,7 +351,7 @@ size_t spec_kl_workspace_size(int N, int K, int V, spec_dtype dtype);
  * per_step       [N, K] float32 out: L_{n,k} (may be NULL)
  * grad_draft     [N, K, V] float32 out, contiguous; NULL = forward only
  * NaN or infinite logits propagate into that position's loss and gradient.
- * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V < 2^31, 1 <= N, N*K < 2^31.
+ * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V <= SPEC_MAX_V, 1 <= N, N*K < 2^31.
  */
 spec_status spec_kl_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, int64_t t_stride_k,
                                  const void* draft_logits, int64_t d_stride_n, int64_t d_stride_k,

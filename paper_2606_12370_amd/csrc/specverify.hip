@@ -64,25 +64,30 @@ Geometry geometry(int V, spec_dtype dt) {
 // Sub-chunks of kStep tiles per row (the statistics granularity of multinomial verification).
 int sub_chunks(int V, spec_dtype dt) { return (geometry(V, dt).ntiles + kStep - 1) / kStep; }
 
+// Largest vocabulary: element indices are 32-bit and run up to one chunk
+// (16384 elements) past V where a row's last chunk is rounded up.
+constexpr int64_t kMaxV = SPEC_MAX_V;
+static_assert(kMaxV + kChunkElems < (int64_t{1} << 31), "element indices fit in int");
+
 bool verify_sizes_ok(int B, int K, int V, spec_dtype dt) {
-  if (B < 1 || K < 1 || K > SPEC_MAX_K || V < 1) return false;
+  if (B < 1 || K < 1 || K > SPEC_MAX_K || V < 1 || V > kMaxV) return false;
   const int64_t rows = static_cast<int64_t>(B) * (2 * K + 1);
   return rows * sub_chunks(V, dt) < (int64_t{1} << 31);
 }
 
 bool tv_sizes_ok(int N, int K, int V, spec_dtype dt) {
-  if (N < 1 || K < 1 || K > SPEC_MAX_K || V < 1) return false;
+  if (N < 1 || K < 1 || K > SPEC_MAX_K || V < 1 || V > kMaxV) return false;
   const int64_t rows = static_cast<int64_t>(N) * 2 * K;
   return rows * geometry(V, dt).C < (int64_t{1} << 31);
 }
 
 bool rows_ok(int64_t rows, int V, spec_dtype dt) {
-  return rows >= 1 && V >= 1 && rows * geometry(V, dt).C < (int64_t{1} << 31);
+  return rows >= 1 && V >= 1 && V <= kMaxV && rows * geometry(V, dt).C < (int64_t{1} << 31);
 }
 
 // Sizes for the entry points that keep statistics per sub-chunk of kStep tiles.
 bool rows_sub_ok(int64_t rows, int V, spec_dtype dt) {
-  return rows >= 1 && V >= 1 && rows * sub_chunks(V, dt) < (int64_t{1} << 31);
+  return rows >= 1 && V >= 1 && V <= kMaxV && rows * sub_chunks(V, dt) < (int64_t{1} << 31);
 }
 
 struct VerifyLayout {

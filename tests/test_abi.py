@@ -109,6 +109,20 @@ def test_workspace_sizes(lib):
     assert lib.spec_kl_workspace_size(16384, 9, 151936, 1) == 0
 
 
+def test_vocabulary_limit(lib):
+    """V up to SPEC_MAX_V = 2^31 - 2^16 is accepted (element indices, 32-bit,
+    run one 16384-element chunk past V); one more is rejected everywhere."""
+    max_v = int(re.search(r"#define SPEC_MAX_V (\d+)", open(HEADER).read()).group(1))
+    assert max_v == (1 << 31) - (1 << 16)
+    for V, ok in ((max_v, True), (max_v + 1, False)):
+        for dt in (0, 1):
+            sizes = [lib.spec_verify_workspace_size(1, 1, V, dt), lib.spec_tv_workspace_size(1, 1, V, dt),
+                     lib.spec_verify_gumbel_workspace_size(1, 1, V, dt), lib.spec_sample_gumbel_workspace_size(1, V, dt),
+                     lib.spec_verify_target_only_workspace_size(1, 1, V, dt), lib.spec_sample_workspace_size(1, V, dt),
+                     lib.spec_diagnostics_workspace_size(1, 1, V, dt), lib.spec_kl_workspace_size(1, 1, V, dt)]
+            assert all((x > 0) == ok for x in sizes), (V, dt, sizes)
+
+
 FAKE = 0x10000  # never dereferenced: every call below fails validation first
 
 
@@ -142,6 +156,7 @@ def call_verify(lib, **kw):
     (dict(ws=None), 4),
     (dict(wsb=64), 4),
     (dict(ws=FAKE + 4), 1),
+    (dict(V=(1 << 31) - (1 << 16) + 1, tsk=1 << 31, tsb=1 << 33, dsk=1 << 31, dsb=1 << 33), 1),
 ])
 def test_verify_argument_errors(lib, kw, status):
     assert call_verify(lib, **kw) == status
@@ -170,6 +185,7 @@ def call_tv(lib, **kw):
     (dict(tsk=-1), 1),
     (dict(ws=None), 4),
     (dict(wsb=100), 4),
+    (dict(V=(1 << 31) - (1 << 16) + 1, tsk=1 << 31, tsn=1 << 33, dsk=1 << 31, dsn=1 << 33), 1),
 ])
 def test_tv_argument_errors(lib, kw, status):
     assert call_tv(lib, **kw) == status
