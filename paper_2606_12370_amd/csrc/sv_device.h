@@ -121,6 +121,19 @@ __device__ __forceinline__ void load_tiles(const typename E::raw* __restrict__ r
 struct Philox4x64 {
   uint64_t w[4];
 };
+// Full 128-bit product a * m as (hi, lo), schoolbook over 32-bit halves: four
+// 32 x 32 -> 64-bit partial products; a partial plus the 32-bit carries added
+// to it stays below 2^64 ((2^32 - 1)^2 + 2 (2^32 - 1) = 2^64 - 1), so both
+// halves come from four multiply-adds and one add.
+__device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t m, uint64_t* lo, uint64_t* hi) {
+  const uint64_t a0 = static_cast<uint32_t>(a), a1 = a >> 32;
+  const uint64_t m0 = static_cast<uint32_t>(m), m1 = m >> 32;
+  const uint64_t p00 = a0 * m0;
+  const uint64_t p01 = a0 * m1 + (p00 >> 32);
+  const uint64_t p10 = a1 * m0 + static_cast<uint32_t>(p01);
+  *hi = a1 * m1 + (p01 >> 32) + (p10 >> 32);
+  *lo = (p10 << 32) | static_cast<uint32_t>(p00);
+}
 
 __device__ inline Philox4x64 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                            uint64_t k0, uint64_t k1) {
@@ -129,8 +142,9 @@ __device__ inline Philox4x64 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r > 0) { k0 += W0; k1 += W1; }
-    const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
-    const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+    uint64_t lo0, hi0, lo1, hi1;
+    mulhilo64(c0, M0, &lo0, &hi0);
+    mulhilo64(c2, M1, &lo1, &hi1);
     const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
     c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
   }

@@ -42,7 +42,7 @@ struct TvArgs {
   TvPair* pairs;         // [N K][C]
   float2* coef;          // [N K]: (A1, A0)
   double* loss_pos;      // [N]
-  uint8_t* bits;         // [N K][bits_stride]: bit (v % 8) of byte v / 8 = 1[q_v <= p_v]; NULL without gradient
+  uint8_t* bits;         // [N K][bits_stride]: 1[q <= p] per element, one 64-bit word per (chunk, tv_pair thread); NULL without gradient
   int64_t bits_stride;   // bytes per (position, step)
   int vec_g;
 };
