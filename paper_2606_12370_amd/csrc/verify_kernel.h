@@ -443,54 +443,81 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
 #pragma unroll
   for (int j = 0; j < NT; ++j)
     if (j == jstar) w = tsum[j];
-  double incl;
-  const double excl_sum = wg_scan(static_cast<double>(w), red1, &incl);
-  int tstar = kThreads;
-  if (!clamp) tstar = wg_min_int((incl > t_in && excl_sum <= t_in && w > 0.f) ? tid : kThreads, red1);
-  if (tstar == kThreads) {
-    clamp = true;
-    tstar = -wg_min_int((w > 0.f) ? -tid : 1, red1);
-  }
+  // the wave holding the target from the wave totals (one exchange through
+  // LDS), then a prefix scan inside that wave only; its winning lane scans its
+  // elements and writes the token
+  const int wave = tid >> 6, lane = tid & 63;
+  const double wt = wave_sum(static_cast<double>(w));
+  if (lane == 0) red1.d[wave][0] = wt;
   if (tid == 0) sh.token = -1;
   __syncthreads();
-  if (tid == tstar) {
-    const int v0 = (tile0 + jstar) * TILE + tid * EPV;
-    float r[EPV];
-    if constexpr (NT == S) {
+  int twave = -1, tlast = -1;
+  double tbase = 0.0, base = 0.0;
 #pragma unroll
-      for (int j = 0; j < NT; ++j)
-        if (j == jstar)
-#pragma unroll
-          for (int k = 0; k < EPV; ++k) r[k] = keep[j][k];
-    } else {
-      vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+  for (int w2 = 0; w2 < kWaves; ++w2) {
+    const double tw = red1.d[w2][0];
+    if (tw > 0.0) tlast = w2;
+    if (!clamp && twave < 0 && tw > 0.0 && base + tw > t_in) { twave = w2; tbase = base; }
+    base += tw;
+  }
+  if (twave < 0) { clamp = true; twave = tlast; }  // rounding: the last wave with mass
+  if (wave == twave) {
+    const double incl = tbase + wave_incl_scan(static_cast<double>(w));
+    const double excl_sum = incl - static_cast<double>(w);
+    const uint64_t hit = clamp ? 0ull : __ballot(incl > t_in && excl_sum <= t_in && w > 0.f);
+    bool lclamp = clamp;
+    int lstar;
+    if (hit) {
+      lstar = __ffsll(static_cast<long long>(hit)) - 1;
+    } else {  // rounding inside the wave: its last lane with mass
+      lclamp = true;
+      const uint64_t pos = __ballot(w > 0.f);
+      lstar = pos ? 63 - __clzll(pos) : -1;
     }
-    const double tl = t_in - excl_sum;
-    float cumf = 0.f;
-    int kstar = -1, klast = -1;
+    if (lane == lstar) {
+      const int v0 = (tile0 + jstar) * TILE + tid * EPV;
+      float r[EPV];
+      if constexpr (NT == S) {
 #pragma unroll
-    for (int k = 0; k < EPV; ++k) {
-      cumf += r[k];
-      if (r[k] > 0.f) klast = k;
-      if (kstar < 0 && !clamp && r[k] > 0.f && static_cast<double>(cumf) > tl) kstar = k;
+        for (int j = 0; j < NT; ++j)
+          if (j == jstar)
+#pragma unroll
+            for (int k = 0; k < EPV; ++k) r[k] = keep[j][k];
+      } else {
+        vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+      }
+      const double tl = t_in - excl_sum;
+      float cumf = 0.f;
+      int kstar = -1, klast = -1;
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) {
+        cumf += r[k];
+        if (r[k] > 0.f) klast = k;
+        if (kstar < 0 && !lclamp && r[k] > 0.f && static_cast<double>(cumf) > tl) kstar = k;
+      }
+      if (kstar < 0) kstar = klast;
+      if (kstar >= 0) sh.token = v0 + kstar;
     }
-    if (kstar < 0) kstar = klast;
-    if (kstar >= 0) sh.token = v0 + kstar;
   }
   __syncthreads();
-  const int token = sh.token;
-  __syncthreads();
-  return token;
+  return sh.token;
 }
 
 struct FinishShared {
   double alpha[SPEC_MAX_K_DEV];
+  RowNorm nrm[2 * SPEC_MAX_K_DEV + 1];  // target rows 0..K, then draft rows 0..K-1
   double tin;
   int cstar, residual;
   SampleShared smp;
 };
 
 // One workgroup per batch row: overlaps and the resampled / bonus token.
+// Everything the row can need except the chosen sub-chunk is requested before
+// its accept length is known, in one round trip: the overlap partials, the
+// residual masses of every step and the bonus row's statistics for the first
+// 64 sub-chunks, and the normalisers of the 2K+1 rows; the uniform of every
+// possible emitting step is drawn meanwhile, one lane per step.  Then only the
+// chosen sub-chunk is read.
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   using raw = typename E::raw;
@@ -501,37 +528,80 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   const int K = a.K, C = d.C, V = d.V;
   const int b = blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+
+  if (tid < 2 * K + 1) sh.nrm[tid] = a.norms[tid <= K ? target_row(a, b, tid) : draft_row(a, b, tid - K - 1)];
+  // overlap partials of every draft step (one wave per step, sub-chunk order fixed)
+  double al = 0.0;
+  if (a.overlap != nullptr && wave < K) {
+    const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + wave) * C;
+    for (int cc = lane; cc < C; cc += 64) al += ps[cc].alpha;
+  }
+  // wave 0, lane cc < 64: sub-chunk cc's residual mass of every step and the
+  // bonus row's statistics; lane j <= K: target row j's normaliser and the
+  // uniform u' of step j
+  double zpre[SPEC_MAX_K_DEV];
+  RowStat spre;
+  spre.m = -INFINITY; spre.pad = 0.f; spre.D = 0.0;
+  float nM = 0.f;
+  double nD = 1.0, uq = 0.0;
+  if (wave == 0) {
+#pragma unroll
+    for (int i = 0; i < SPEC_MAX_K_DEV; ++i) {
+      zpre[i] = 0.0;
+      if (i < K && lane < C) zpre[i] = a.pairs[static_cast<int64_t>(b * K + i) * C + lane].Z;
+    }
+    if (lane < C) spre = a.stats[static_cast<int64_t>(target_row(a, b, K)) * C + lane];
+    if (lane <= K) {
+      const RowNorm nl = a.norms[target_row(a, b, lane)];
+      nM = nl.M;
+      nD = nl.D;
+      const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(lane), a.offset, 0ull,
+                                         a.seed, 0ull);
+      uq = u24(g.w[1]);
+    }
+  }
   const int n = a.decision[b];
   if (n < 0) return;  // data error: decide has written every output of the row
   const float s = scale_of(temperature_of(d, b));
 
-  // overlap of every draft step (one wave per step, chunk order fixed)
-  for (int i = wave; i < K && a.overlap != nullptr; i += kWaves) {
-    double al = 0.0;
-    const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + i) * C;
-    for (int cc = lane; cc < C; cc += 64) al += ps[cc].alpha;
+  if (a.overlap != nullptr && wave < K) {
     al = wave_sum(al);
-    if (lane == 0) sh.alpha[i] = al;
+    if (lane == 0) sh.alpha[wave] = al;
+    for (int i = wave + kWaves; i < K; i += kWaves) {  // K > kWaves: the remaining steps
+      double al2 = 0.0;
+      const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + i) * C;
+      for (int cc = lane; cc < C; cc += 64) al2 += ps[cc].alpha;
+      al2 = wave_sum(al2);
+      if (lane == 0) sh.alpha[i] = al2;
+    }
   }
-  // the chunk holding the sampling target (wave 0)
+  // the sub-chunk holding the sampling target (wave 0)
   if (wave == 0) {
     const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + (n < K ? n : 0)) * C;
+    double z0 = 0.0;
+#pragma unroll
+    for (int i = 0; i < SPEC_MAX_K_DEV; ++i)
+      if (i == n) z0 = zpre[i];
     double zs = 0.0;
     if (n < K) {
-      for (int cc = lane; cc < C; cc += 64) zs += ps[cc].Z;
+      for (int cc = lane; cc < C; cc += 64) zs += cc < 64 ? z0 : ps[cc].Z;
       zs = wave_sum(zs);
     }
     // residual of the rejected step; p_n itself for the bonus row or an empty residual
     const bool residual = n < K && zs > 0.0;
     const RowStat* st = a.stats + static_cast<int64_t>(target_row(a, b, n)) * C;
-    const RowNorm nn = a.norms[target_row(a, b, n)];
-    const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(n), a.offset, 0ull,
-                                       a.seed, 0ull);
+    const float nnM = __shfl(nM, n, 64);
+    const double nnD = __shfl(nD, n, 64);
+    // this lane's mass of sub-chunk `lane` (select_chunk asks for cc = c0 + lane,
+    // c0 a multiple of 64; beyond the first 64 sub-chunks they are read)
+    auto stat_mass1 = [&](const RowStat& sc) -> double {
+      return sc.m == -INFINITY ? 0.0 : sc.D * static_cast<double>(__builtin_amdgcn_exp2f(sc.m - nnM)) / nnD;
+    };
+    const double m0 = lane < C ? (residual ? z0 : stat_mass1(n == K ? spre : st[lane])) : 0.0;
     double tin;
-    const int cstar = select_chunk(C, u24(g.w[1]), [&](int cc) -> double {
-      if (residual) return ps[cc].Z;
-      const float mc = st[cc].m;
-      return mc == -INFINITY ? 0.0 : st[cc].D * static_cast<double>(__builtin_amdgcn_exp2f(mc - nn.M)) / nn.D;
+    const int cstar = select_chunk(C, __shfl(uq, n, 64), [&](int cc) -> double {
+      if (cc < 64) return m0;
+      return residual ? ps[cc].Z : stat_mass1(st[cc]);
     }, &tin);
     if (lane == 0) {
       sh.cstar = cstar;
@@ -547,8 +617,8 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     bool al_t, al_d;
     const raw* rt = row_of<E>(d, target_row(a, b, n), &bb, &al_t);
     const raw* rd = row_of<E>(d, draft_row(a, b, n < K ? n : 0), &bb, &al_d);
-    const RowNorm nt = a.norms[target_row(a, b, n)];
-    const RowNorm nd = a.norms[draft_row(a, b, n < K ? n : 0)];
+    const RowNorm nt = sh.nrm[n];
+    const RowNorm nd = sh.nrm[K + 1 + (n < K ? n : 0)];
     token = sample_in_chunk<E, NT, S>(rt, al_t, rd, al_d, sh.residual != 0, -1, sh.cstar, sh.tin, V, d.ntiles, s, nt,
                                       nd, redv, red1, sh.smp);
   }
