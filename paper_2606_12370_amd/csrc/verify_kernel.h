@@ -52,16 +52,15 @@ __device__ __forceinline__ int draft_row(const VerifyArgs& a, int b, int i) {
 
 struct DecideShared {
   RowNorm nrm[2 * SPEC_MAX_K_DEV + 1];  // target rows 0..K, then draft rows 0..K-1
-  double px[SPEC_MAX_K_DEV], qx[SPEC_MAX_K_DEV];
-  int acc[SPEC_MAX_K_DEV], badx[SPEC_MAX_K_DEV];
-  int n;
 };
 
-// The draft token of step i and its target and draft logits, gathered by
-// lane i before the normalisers are known (the loads overlap the combine).
+// The draft token of step i, its target and draft logits and the accept
+// uniform u_i, held by lane i: requested and drawn before the normalisers are
+// known (the loads and the Philox rounds overlap the combine).
 struct DraftGather {
   int x;
   float zt, zd;
+  double u;
 };
 
 template <class E>
@@ -71,6 +70,8 @@ __device__ __forceinline__ DraftGather gather_draft(const VerifyArgs& a, int b, 
   g.x = a.ids[static_cast<int64_t>(b) * a.K + i];
   g.zt = 0.f;
   g.zd = 0.f;
+  const Philox4x64 ph = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(i), a.offset, 0ull, a.seed, 0ull);
+  g.u = u24(ph.w[0]);
   if (g.x >= 0 && g.x < d.V) {
     int bb;
     bool al;
@@ -81,67 +82,50 @@ __device__ __forceinline__ DraftGather gather_draft(const VerifyArgs& a, int b, 
 }
 
 // Accept tests and every per-row output except the overlaps and emitted[n],
-// for batch row b whose 2K+1 row normalisers are in sh.nrm (`fail` forces a
-// row error); lane i < K holds step i's gathered token and logits.  Whole
-// workgroup; returns the accept length n, or -1 for a row with a data error
-// (then every output of the row has been written).
+// for batch row b whose 2K+1 row normalisers are in sh.nrm, by one wave: lane
+// i < K tests step i (float64, u q(x) < p(x), no division), two ballots give
+// the row's error flag and its first rejection, lane j <= K writes the
+// outputs of position j.  Returns the accept length n, or -1 for a row with a
+// data error (then every output of the row has been written).
 template <class E>
-__device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& sh, const DraftGather& gx) {
+__device__ int decide_wave(const VerifyArgs& a, int b, const DecideShared& sh, const DraftGather& gx) {
   const RowsDesc& d = a.rows;
   const int K = a.K, V = d.V;
-  const int tid = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const float T = temperature_of(d, b);
   const bool t_ok = temperature_ok(T);
   const float s = t_ok ? scale_of(T) : 1.0f;
-  // accept tests in float64: u q(x) < p(x), no division; one lane per step
-  if (tid < K) {
-    const int i = tid;
-    const int x = gx.x;
-    const RowNorm& nt = sh.nrm[i];
-    const RowNorm& nd = sh.nrm[K + 1 + i];
-    int ok = 0, bad = 1;
-    double p = 0.0, q = 0.0;
-    if (x >= 0 && x < V) {
-      bad = 0;
-      if (t_ok && norm_ok(nt) && norm_ok(nd)) {
-        p = exp2(static_cast<double>(gx.zt) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
-        q = exp2(static_cast<double>(gx.zd) * static_cast<double>(s) - static_cast<double>(nd.M)) / nd.D;
-        const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(i), a.offset, 0ull,
-                                           a.seed, 0ull);
-        ok = (u24(g.w[0]) * q < p) ? 1 : 0;
-      }
+  double p = 0.0, q = 0.0;
+  bool ok = false, bad = false;
+  if (lane < K) {
+    const RowNorm& nt = sh.nrm[lane];
+    const RowNorm& nd = sh.nrm[K + 1 + lane];
+    bad = !(gx.x >= 0 && gx.x < V);
+    if (!bad && t_ok && norm_ok(nt) && norm_ok(nd)) {
+      p = exp2(static_cast<double>(gx.zt) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
+      q = exp2(static_cast<double>(gx.zd) * static_cast<double>(s) - static_cast<double>(nd.M)) / nd.D;
+      ok = gx.u * q < p;
     }
-    sh.px[i] = p; sh.qx[i] = q; sh.acc[i] = ok; sh.badx[i] = bad;
   }
-  __syncthreads();
-  if (tid == 0) {
-    bool err = !t_ok || fail;
-    for (int j = 0; j < 2 * K + 1; ++j)
-      if (!norm_ok(sh.nrm[j])) err = true;
-    int n = K;
-    for (int i = 0; i < K; ++i) {
-      if (sh.badx[i]) err = true;
-      if (n == K && !sh.acc[i]) n = i;  // the first rejection ends the chain
-    }
-    a.accept_len[b] = err ? -1 : n;
-    sh.n = err ? -1 : n;
-  }
-  __syncthreads();
-  // the per-step outputs, one lane each (the float64 log2 of the normalisers in parallel)
-  const int n = sh.n;
-  const bool err = n < 0;
-  if (tid <= K) {
-    const int j = tid;
+  const uint64_t errm = __ballot((lane < 2 * K + 1 && !norm_ok(sh.nrm[lane])) || bad);
+  const uint64_t rejm = __ballot(lane < K && !ok);
+  const bool err = !t_ok || errm != 0;
+  // the first rejection ends the chain
+  const int n = err ? -1 : (rejm ? __ffsll(static_cast<long long>(rejm)) - 1 : K);
+  if (lane == 0) a.accept_len[b] = n;
+  // the per-position outputs, one lane each (the float64 log2 of the normalisers in parallel)
+  if (lane <= K) {
+    const int j = lane;
     const int64_t ob = static_cast<int64_t>(b) * (K + 1) + j;
     // emitted[n] is written with the sampled token
-    if (err || j != n) a.emitted[ob] = (!err && j < n) ? a.ids[static_cast<int64_t>(b) * K + j] : -1;
+    if (err || j != n) a.emitted[ob] = (!err && j < n) ? gx.x : -1;
     if (a.logz_t)
       a.logz_t[ob] = err ? NAN : static_cast<float>((static_cast<double>(sh.nrm[j].M) + log2(sh.nrm[j].D)) * kLn2D);
     if (j < K) {
       const int64_t o = static_cast<int64_t>(b) * K + j;
       const RowNorm& nd = sh.nrm[K + 1 + j];
-      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(sh.px[j]);
-      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(sh.qx[j]);
+      if (a.p_at) a.p_at[o] = err ? NAN : static_cast<float>(p);
+      if (a.q_at) a.q_at[o] = err ? NAN : static_cast<float>(q);
       if (a.logz_d) a.logz_d[o] = err ? NAN : static_cast<float>((static_cast<double>(nd.M) + log2(nd.D)) * kLn2D);
       if (a.overlap && err) a.overlap[o] = NAN;
     }
@@ -149,7 +133,8 @@ __device__ int decide_row(const VerifyArgs& a, int b, bool fail, DecideShared& s
   return n;
 }
 
-// Row normalisers and accept decisions, one workgroup per batch row.
+// Row normalisers and accept decisions, one workgroup per batch row: every
+// wave combines statistics of its rows, then wave 0 alone decides.
 template <class E>
 __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
   __shared__ DecideShared sh;
@@ -157,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
   const int K = a.K, C = d.C;
   const int b = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  DraftGather gx{0, 0.f, 0.f};
+  DraftGather gx{0, 0.f, 0.f, 0.0};
   if (static_cast<int>(threadIdx.x) < K) gx = gather_draft<E>(a, b, threadIdx.x);
   // row j < K+1: target row j; row K+1+i: draft row i (one wave per row, the
   // rows of a wave combined together so that their loads are in flight at once)
@@ -182,8 +167,9 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
     }
   }
   __syncthreads();
-  const int n = decide_row<E>(a, b, false, sh, gx);
-  if (threadIdx.x == 0) a.decision[b] = n;
+  if (wave != 0) return;  // the decision is one wave's work
+  const int n = decide_wave<E>(a, b, sh, gx);
+  if (lane == 0) a.decision[b] = n;
 }
 
 // Pass 2 over one chunk of a (target, draft) pair: overlap, and the residual
