@@ -40,8 +40,6 @@ struct ToArgs {
 
 struct ToShared {
   RowNorm nrm[SPEC_MAX_K_DEV + 1];
-  double px[SPEC_MAX_K_DEV];
-  int acc[SPEC_MAX_K_DEV], badx[SPEC_MAX_K_DEV];
   int n, excl, cstar, excl_on;
   double tin;
   SampleShared smp;
@@ -66,6 +64,26 @@ __global__ __launch_bounds__(kThreads) void to_verify_kernel(ToArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int row0 = b * (K + 1);
+  // lane i < K: the greedy draft token of step i and its target logit, and
+  // lane i <= K: the uniforms of step i (accept test, residual draw), all
+  // requested and drawn before the normalisers are known
+  int x = -1;
+  float zx = 0.f;
+  double ua = 0.0, ur = 0.0;
+  if (tid <= K) {
+    if (tid < K) {
+      x = a.ids[static_cast<int64_t>(b) * K + tid];
+      if (x >= 0 && x < V) {
+        int bb;
+        bool al;
+        zx = E::one(row_of<E>(d, row0 + tid, &bb, &al) + x);
+      }
+    }
+    const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(tid), a.offset, 0ull,
+                                       a.seed, 0ull);
+    ua = u24(g.w[0]);
+    ur = u24(g.w[1]);
+  }
   for (int j = wave; j <= K; j += kWaves) {
     float M;
     double D;
@@ -76,50 +94,38 @@ __global__ __launch_bounds__(kThreads) void to_verify_kernel(ToArgs a) {
   const float T = temperature_of(d, b);
   const bool t_ok = temperature_ok(T);
   const float s = t_ok ? scale_of(T) : 1.0f;
-  // accept tests in float64: u < p(x); one lane per step
-  if (tid < K) {
-    const int i = tid;
-    const int x = a.ids[static_cast<int64_t>(b) * K + i];
-    const RowNorm& nt = sh.nrm[i];
-    int ok = 0, bad = 1;
+  // wave 0: accept tests in float64, u < p(x), lane i for step i; two ballots
+  // give the row's error flag and its first rejection; lane j writes the
+  // outputs of position j
+  if (wave == 0) {
     double p = 0.0;
-    if (x >= 0 && x < V) {
-      bad = 0;
-      if (t_ok && norm_ok(nt)) {
-        int bb;
-        bool al;
-        const raw* rt = row_of<E>(d, row0 + i, &bb, &al);
-        p = exp2(static_cast<double>(E::one(rt + x)) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
-        const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(i), a.offset, 0ull,
-                                           a.seed, 0ull);
-        ok = (u24(g.w[0]) < p) ? 1 : 0;
+    bool ok = false, bad = false;
+    if (lane < K) {
+      const RowNorm& nt = sh.nrm[lane];
+      bad = !(x >= 0 && x < V);
+      if (!bad && t_ok && norm_ok(nt)) {
+        p = exp2(static_cast<double>(zx) * static_cast<double>(s) - static_cast<double>(nt.M)) / nt.D;
+        ok = ua < p;
       }
     }
-    sh.px[i] = p; sh.acc[i] = ok; sh.badx[i] = bad;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    bool err = !t_ok;
-    for (int j = 0; j <= K; ++j)
-      if (!norm_ok(sh.nrm[j])) err = true;
-    int n = K;
-    for (int i = 0; i < K; ++i) {
-      if (sh.badx[i]) err = true;
-      if (n == K && !sh.acc[i]) n = i;
+    const uint64_t errm = __ballot((lane <= K && !norm_ok(sh.nrm[lane])) || bad);
+    const uint64_t rejm = __ballot(lane < K && !ok);
+    const bool err = !t_ok || errm != 0;
+    const int n = err ? -1 : (rejm ? __ffsll(static_cast<long long>(rejm)) - 1 : K);
+    if (lane == 0) a.accept_len[b] = n;
+    if (lane <= K) {
+      const int j = lane;
+      const int64_t ob = static_cast<int64_t>(b) * (K + 1) + j;
+      if (err || j != n) a.emitted[ob] = (!err && j < n) ? x : -1;
+      if (a.p_at && j < K) a.p_at[static_cast<int64_t>(b) * K + j] = err ? NAN : static_cast<float>(p);
+      if (a.logz_t)
+        a.logz_t[ob] = err ? NAN : static_cast<float>((static_cast<double>(sh.nrm[j].M) + log2(sh.nrm[j].D)) * kLn2D);
     }
-    a.accept_len[b] = err ? -1 : n;
-    int32_t* em = a.emitted + static_cast<int64_t>(b) * (K + 1);
-    const int32_t* xb = a.ids + static_cast<int64_t>(b) * K;
-    for (int j = 0; j <= K; ++j)
-      if (err || j != n) em[j] = (!err && j < n) ? xb[j] : -1;
-    if (a.p_at)
-      for (int i = 0; i < K; ++i) a.p_at[static_cast<int64_t>(b) * K + i] = err ? NAN : static_cast<float>(sh.px[i]);
-    if (a.logz_t)
-      for (int i = 0; i <= K; ++i)
-        a.logz_t[static_cast<int64_t>(b) * (K + 1) + i] =
-            err ? NAN : static_cast<float>((static_cast<double>(sh.nrm[i].M) + log2(sh.nrm[i].D)) * kLn2D);
-    sh.n = err ? -1 : n;
-    sh.excl = (!err && n < K) ? xb[n] : -1;
+    const int xn = __shfl(x, n < 0 ? 0 : n, 64);
+    if (lane == 0) {
+      sh.n = n;
+      sh.excl = (n >= 0 && n < K) ? xn : -1;
+    }
   }
   __syncthreads();
   const int n = sh.n;
@@ -130,6 +136,10 @@ __global__ __launch_bounds__(kThreads) void to_verify_kernel(ToArgs a) {
   bool al;
   const raw* rt = row_of<E>(d, row0 + n, &bb, &al);
   const RowStat* st = a.stats + static_cast<int64_t>(row0 + n) * C;
+  // wave 0, lane cc < 64: the mass of sub-chunk cc from its statistics,
+  // requested before the chunk holding x_n is read
+  double m0 = 0.0;
+  if (wave == 0 && lane < C) m0 = stat_mass(st, lane, nn);
   // The residual p_n without x_n: every chunk's mass comes from its
   // statistics except the chunk holding x_n, which is summed element by
   // element without x_n (a difference of two statistics would cancel when
@@ -147,14 +157,16 @@ __global__ __launch_bounds__(kThreads) void to_verify_kernel(ToArgs a) {
     for (int j = 0; j < NT; ++j) xm += W[j];
   }
   if (wave == 0) {
-    const Philox4x64 g = philox4x64_10(static_cast<uint64_t>(b), static_cast<uint64_t>(n), a.offset, 0ull,
-                                       a.seed, 0ull);
-    const double u = u24(g.w[1]);
+    const double u = __shfl(ur, n, 64);
     double tin = 0.0;
-    int cstar = select_chunk(C, u, [&](int cc) -> double { return cc == cx ? xm : stat_mass(st, cc, nn); }, &tin);
+    // select_chunk asks for cc = c0 + lane, c0 a multiple of 64: cc < 64 is
+    // this lane's prefetched sub-chunk
+    int cstar = select_chunk(C, u, [&](int cc) -> double {
+      return cc == cx ? xm : (cc < 64 ? m0 : stat_mass(st, cc, nn));
+    }, &tin);
     bool ex_on = cx >= 0;
     if (cstar < 0) {  // no residual mass: draw from p_n itself
-      cstar = select_chunk(C, u, [&](int cc) -> double { return stat_mass(st, cc, nn); }, &tin);
+      cstar = select_chunk(C, u, [&](int cc) -> double { return cc < 64 ? m0 : stat_mass(st, cc, nn); }, &tin);
       ex_on = false;
     }
     if (lane == 0) {
