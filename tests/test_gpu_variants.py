@@ -50,7 +50,8 @@ def run_to(d, ids, seed=0, offset=0):
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("B,K,V", [(4, 1, 1024), (6, 3, 20000), (3, 2, 2049), (5, 1, 1023), (4, 4, 7), (3, 1, 1),
-                                   (2, 8, 9000), (3, 3, 65536 + 24), (2, 2, 256 * 8192 + 8195)])
+                                   (2, 8, 9000), (3, 3, 65536 + 24), (2, 2, 256 * 8192 + 8195),
+                                   (3, 2, 4096), (3, 2, 8192), (3, 2, 8193)])
 def test_target_only_ragged(dtype, B, K, V):
     d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 100 + B + K + V)
     ids = W.greedy_ids(d["draft"], dtype)
@@ -184,7 +185,7 @@ def test_sample_masked_vocabularies(dtype):
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("R,V", [(40, 1024), (9, 20000), (17, 2049), (5, 7), (4, 1), (6, 65536 + 24),
-                                 (2, 256 * 8192 + 8195)])
+                                 (2, 256 * 8192 + 8195), (9, 4096), (9, 8192), (9, 8193)])
 def test_sample_ragged(dtype, R, V):
     rng = np.random.default_rng(R + V)
     z = (rng.standard_normal((R, V)) * rng.uniform(1, 8, size=(R, 1))).astype(np.float32)
@@ -261,7 +262,8 @@ def run_diag(d):
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("B,K,V", [(4, 1, 1024), (6, 3, 20000), (3, 2, 2049), (4, 4, 7), (3, 1, 1), (2, 8, 9000),
-                                   (3, 3, 65536 + 24), (2, 1, 256 * 8192 + 8195)])
+                                   (3, 3, 65536 + 24), (2, 1, 256 * 8192 + 8195),
+                                   (3, 2, 4096), (3, 2, 8191), (3, 2, 8192), (3, 2, 8193)])
 def test_diagnostics_ragged(dtype, B, K, V):
     d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 300 + B + K + V)
     out, ref = run_diag(d)

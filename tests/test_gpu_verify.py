@@ -50,7 +50,10 @@ def test_tiny_f32():
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 @pytest.mark.parametrize("B,K,V", [(6, 3, 20000), (3, 2, 2049), (5, 1, 1023), (4, 4, 7), (3, 1, 1),
-                                   (2, 8, 9000), (3, 3, 65536 + 24)])
+                                   (2, 8, 9000), (3, 3, 65536 + 24),
+                                   # sub-chunk edges: one wave streams 8192 bf16 / 4096 fp32 elements
+                                   (3, 2, 4095), (3, 2, 4096), (3, 2, 4097), (3, 2, 8191), (3, 2, 8192),
+                                   (3, 2, 8193), (2, 3, 16384)])
 def test_ragged_multi_chunk(dtype, B, K, V):
     d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 7 + B + K + V)
     out, ref = run_numpy_case(d, seed=11, offset=3)
