@@ -35,8 +35,13 @@ __device__ __forceinline__ float exp_variate(const Philox4x64& g, int k) {
   const uint64_t w = g.w[(k >> 1) & 3];
   const uint32_t bits = (k & 1) ? static_cast<uint32_t>((w >> 8) & 0xFFFFFFull) : static_cast<uint32_t>(w >> 40);
   constexpr float kInv24 = 5.9604644775390625e-8f;  // 2^-24
-  const float y = (static_cast<float>((1u << 24) - bits) - 0.5f) * kInv24;
-  const float u = (static_cast<float>(bits) + 0.5f) * kInv24;
+  constexpr float kHalf24 = 2.98023223876953125e-8f;  // 2^-25
+  // one conversion (exact: bits < 2^24); u = (bits + 1/2) 2^-24 rounded once
+  // by an FMA, y = 1 - bits 2^-24 (exact) - 2^-25, exact wherever it is used
+  // (y < 1/16, where it has at most 21 significant bits)
+  const float f = static_cast<float>(bits);
+  const float y = fmaf(-f, kInv24, 1.0f) - kHalf24;
+  const float u = fmaf(f, kInv24, kHalf24);
   // both forms, then a select: no divergent branch per element; the series
   // in Horner form with fused multiply-adds (5 FMAs and a multiply)
   const float series =
