@@ -6,6 +6,8 @@ call in this file)."""
 import ctypes
 import os
 import re
+import shutil
+import subprocess
 
 import pytest
 
@@ -335,3 +337,45 @@ def test_kl_argument_errors(lib, kw, status):
     assert lib.spec_kl_loss_fwd_bwd(*[args[k] for k in ("t", "tsn", "tsk", "d", "dsn", "dsk", "dtype", "N", "K", "V",
                                                         "T", "kind", "scale", "loss", "ps", "grad", "ws", "wsb",
                                                         "stream")]) == status
+
+
+C_CLIENT = r"""
+#include <stdio.h>
+#include "specverify.h"
+int main(void) {
+  const int32_t ids[1] = {0};
+  printf("%d\n", spec_version());
+  printf("%s\n", spec_status_string(SPEC_EINVAL));
+  printf("%zu\n", spec_verify_workspace_size(256, 3, 151936, SPEC_BF16));
+  printf("%zu\n", spec_tv_workspace_size(16384, 3, 151936, SPEC_BF16));
+  /* rejected before any GPU work: no logits */
+  printf("%d\n", (int)spec_verify(NULL, 0, 0, NULL, 0, 0, SPEC_BF16, 1, 1, 8, ids, NULL, 1.0f, 0u, 0u,
+                                  NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, 0, NULL));
+  return 0;
+}
+"""
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs a C compiler")
+def test_c99_client_links_and_calls(lib, tmp_path):
+    """A C99 program (no C++, no torch) compiled against include/specverify.h
+    with -pedantic -Werror, linked to the built library, sees the same
+    version, status strings and workspace sizes as the Python binding and
+    gets the synchronous argument error."""
+    src = tmp_path / "client.c"
+    src.write_text(C_CLIENT)
+    exe = tmp_path / "client"
+    libdir = os.path.dirname(os.path.abspath(lib._name))
+    cmd = ["gcc", "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror", "-I" + os.path.join(ROOT, "include"),
+           str(src), "-o", str(exe), "-L" + libdir, "-lspecverify", "-Wl,-rpath," + libdir]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    out = r.stdout.split("\n")
+    lib.spec_status_string.restype = ctypes.c_char_p
+    assert int(out[0]) == lib.spec_version()
+    assert out[1] == lib.spec_status_string(1).decode()
+    assert int(out[2]) == lib.spec_verify_workspace_size(256, 3, 151936, 1)
+    assert int(out[3]) == lib.spec_tv_workspace_size(16384, 3, 151936, 1)
+    assert int(out[4]) == 1  # SPEC_EINVAL
