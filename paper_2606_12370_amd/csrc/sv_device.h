@@ -274,25 +274,6 @@ __device__ __forceinline__ void wg_sum(double (&v)[N], RedLds<N>& s) {
   __syncthreads();
 }
 
-// Scan of one double per thread over the workgroup, in thread order.
-// Returns the exclusive prefix and sets *incl to the inclusive one; the
-// exclusive prefix of thread t is bit-identical to the inclusive prefix of
-// thread t-1, so the ranges [excl, incl) of consecutive threads tile exactly.
-__device__ __forceinline__ double wg_scan(double v, RedLds<1>& s, double* incl_out) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const double incl_w = wave_incl_scan(v);
-  double excl_w = __shfl_up(incl_w, 1, 64);
-  if (lane == 0) excl_w = 0.0;
-  if (lane == 63) s.d[wave][0] = incl_w;
-  __syncthreads();
-  double base = 0.0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w)
-    if (w < wave) base += s.d[w][0];
-  __syncthreads();
-  *incl_out = base + incl_w;
-  return base + excl_w;
-}
 
 // Workgroup minimum of an int (every thread receives it).
 __device__ __forceinline__ int wg_min_int(int v, RedLds<1>& s) {
