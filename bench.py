@@ -13,7 +13,9 @@ Prints ONE JSON line.  `value` = verified draft tokens/s = B*K / step time.
 read once, ids and outputs) to the call time measured with HIP events on the
 launch stream; `ms_per_call_distribution` gives p10 / median / p90 of single
 calls from a separate pass with an event between calls.  `cpu_baseline` times the float64 CPU oracle on a bounded
-sample of rows of the same workload, and `parity` compares the oracle's
+sample of rows of the same workload (`cpu_baseline_all_cores`: the same on
+every host core the box grants, rows split over worker processes), and
+`parity` compares the oracle's
 pass over every row of that batch with the library's outputs for it.  The fused TV-loss forward+backward on the training
 workload (N=16384 positions x 3 steps) is timed too and reported under
 `tv_loss`; target-only verification, the draft-stage sampler (the B*K draft
@@ -103,6 +105,52 @@ def cpu_baseline(d_host, K, budget_s=10.0, gpu_out=None):
         "kind": "oracle",
         "sample": "%d rows (passes over all %d rows of the B=256 K=3 V=151936 bf16 batch) through the "
                   "float64 NumPy oracle on one thread, %.1f s of CPU time" % (rows_done, B, t_used),
+    }
+
+
+def _oracle_rows_worker(args):
+    """One worker of the all-cores CPU baseline (a spawned process: NumPy and
+    the oracle only, no GPU): the oracle over its rows of the batch, repeated
+    for about budget_s of wall time.  Returns (rows verified, seconds)."""
+    tgt, drf, ids, T, row0, budget_s = args
+    import oracle
+
+    def f64(bits):  # bfloat16 bit patterns -> float64, exactly
+        return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+    zt, zd = f64(tgt), f64(drf)
+    B = tgt.shape[0]
+    rows, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        for s0 in range(0, B, 4):
+            sl = slice(s0, min(B, s0 + 4))
+            oracle.verify_ref(zt[sl], zd[sl], ids[sl], T[sl], 0, 0, rows=np.arange(row0 + sl.start, row0 + sl.stop))
+            rows += sl.stop - sl.start
+            if time.perf_counter() - t0 >= budget_s:
+                break
+    return rows, time.perf_counter() - t0
+
+
+def cpu_baseline_all_cores(d_host, K, budget_s=10.0, workers=None):
+    """The same oracle on every host core the box grants (at most 16): the
+    batch's rows split over spawned worker processes, each timing its own
+    loop; throughput = all rows verified / the longest worker's time."""
+    import multiprocessing as mp
+    n = workers or max(1, min(16, os.cpu_count() or 1))
+    tgt, drf, ids, T = d_host
+    parts = [c for c in np.array_split(np.arange(tgt.shape[0]), n) if len(c)]
+    with mp.get_context("spawn").Pool(len(parts)) as pool:
+        res = pool.map(_oracle_rows_worker,
+                       [(tgt[c], drf[c], ids[c], T[c], int(c[0]), budget_s) for c in parts])
+    rows = sum(r for r, _ in res)
+    span = max(t for _, t in res)
+    return {
+        "value": rows * K / span,
+        "unit": "verified draft tokens/s",
+        "cores": len(parts),
+        "kind": "oracle",
+        "sample": "%d rows of the B=256 K=3 V=151936 bf16 batch through the float64 NumPy oracle, its rows split "
+                  "over %d worker processes, %.1f s of wall time each" % (rows, len(parts), span),
     }
 
 
@@ -483,6 +531,8 @@ def main():
         del c0, g
         parity, result["cpu_baseline"] = cpu_baseline((tgt, drf, ids, T), K, gpu_out=gpu_out)
         result["parity"] = parity
+        log("timing the CPU oracle on every host core")
+        result["cpu_baseline_all_cores"] = cpu_baseline_all_cores((tgt, drf, ids, T), K)
     print(json.dumps(result), flush=True)
 
 

@@ -83,3 +83,18 @@ def test_quantiles_of_the_per_call_distribution():
     x = sorted(rng.random(101).tolist())
     for q in (0.1, 0.5, 0.9):
         assert bench.quantile(x, q) == pytest.approx(float(np.quantile(x, q)))
+
+
+def test_all_cores_baseline_on_a_tiny_batch():
+    """The all-cores oracle leg on a tiny bf16 batch, two spawned workers:
+    every row is covered and the throughput is positive."""
+    rng = np.random.default_rng(0)
+    B, K, V = 6, 2, 64
+    f32 = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    tgt = (f32.view(np.uint32) >> 16).astype(np.uint16)
+    drf = (f32[:, :K].view(np.uint32) >> 16).astype(np.uint16)
+    ids = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    T = np.ones(B, np.float64)
+    r = bench.cpu_baseline_all_cores((tgt, drf, ids, T), K, budget_s=0.3, workers=2)
+    assert r["cores"] == 2 and r["kind"] == "oracle" and r["value"] > 0
+    assert int(r["sample"].split()[0]) >= B
