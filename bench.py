@@ -212,6 +212,39 @@ def timed(torch, stream, fn, steps):
     return e0.elapsed_time(e1) / steps
 
 
+def verify_sweep(torch, binding, W, stream, warmup, steps):
+    """spec_verify over B x K x V x dtype (rollout recipe, per-row temperatures,
+    overlaps requested, two input copies of at least 1 GiB in all so that the
+    Infinity Cache cannot hold them), one JSON line each: context for the
+    headline, not part of it."""
+    for dt in (W.BF16, W.F32):
+        for V in (151936, 262144):
+            for B in (64, 256, 1024):
+                for K in (1, 2, 3):
+                    esz = 2 if dt == W.BF16 else 4
+                    batch = B * (2 * K + 1) * V * esz
+                    ncp = max(2, min(8, -(-(1 << 30) // batch)))
+                    cps = [W.verify_inputs_torch(B, K, V, dt, "rollout_t", 7000 + 97 * i + B + K) for i in range(ncp)]
+                    o = {"accept_len": torch.empty(B, dtype=torch.int32, device="cuda"),
+                         "emitted": torch.empty((B, K + 1), dtype=torch.int32, device="cuda"),
+                         "overlap": torch.empty((B, K), dtype=torch.float32, device="cuda")}
+
+                    def step(it):
+                        c = cps[it % ncp]
+                        binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=o)
+
+                    for it in range(warmup):
+                        step(it)
+                    ms = timed(torch, stream, step, steps)
+                    nbytes = verify_bytes(B, K, V, esz)
+                    print(json.dumps({"sweep": "spec_verify", "B": B, "K": K, "V": V,
+                                      "logits": "bf16" if dt == W.BF16 else "f32", "input_copies": ncp,
+                                      "ms_per_call": ms, "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
+                                      "frac_of_8TBps": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}), flush=True)
+                    del cps
+                    torch.cuda.empty_cache()
+
+
 def hbm_roofline(nbytes, ms, key):
     achieved = nbytes / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -372,6 +405,9 @@ def main():
                     help="skip spec_verify without overlaps and on the B=64 / B=1024 batches")
     ap.add_argument("--no-kl", action="store_true", help="skip the CE / KL loss legs")
     ap.add_argument("--no-tv-loss", action="store_true", help="skip the TV loss leg (keeps the KL legs)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only the context sweep of spec_verify: B in {64, 256, 1024} x K in {1, 2, 3} x "
+                         "V in {151936, 262144} x {bf16, fp32}, one JSON line per configuration")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
@@ -392,6 +428,9 @@ def main():
     stream = torch.cuda.current_stream(dev)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
+    if args.sweep:
+        verify_sweep(torch, binding, W, stream, args.warmup, args.steps)
+        return
     cfg = W.CONFIGS["verify_bf16_b256_k3_v151936"]
     B, K, V = cfg["B"], cfg["K"], cfg["V"]
     result = {
