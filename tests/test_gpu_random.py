@@ -1,0 +1,58 @@
+"""Randomized shapes, fixed generator: spec_verify and target-only
+verification against the oracle on 300 cases drawn from bf16 / fp32,
+K = 1..8, V from 1 to 40000 plus the sub-chunk edges (4096, 8191, 8192,
+8193, 16384 + a few), per-row temperatures, random seeds and offsets, and
+masked vocabularies.  Every row must match the oracle exactly or be a
+boundary draw (the comparison helpers raise otherwise)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.variants import verify_target_only_ref
+from paper_2606_12370_amd import binding
+from paper_2606_12370_amd import workloads as W
+from tests.parity import compare_target_only, compare_verify, device_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    binding.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def random_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        dt = W.BF16 if rng.random() < 0.6 else W.F32
+        K = int(rng.integers(1, 9))
+        V = int(rng.choice([int(rng.integers(1, 40000)), 8191, 8192, 8193, 4096, 16384 + int(rng.integers(0, 64))]))
+        B = int(rng.integers(1, max(2, min(48, 2_000_000 // (V * (2 * K + 1))))))
+        seed_, offset = int(rng.integers(0, 2**63)), int(rng.integers(0, 2**40))
+        masked = bool(rng.random() < 0.3 and V >= 16384)
+        gen_seed = int(rng.integers(0, 2**31))
+        yield dt, B, K, V, seed_, offset, masked, gen_seed
+
+
+def test_random_shapes_verify_and_target_only():
+    boundary = 0
+    for dt, B, K, V, seed, offset, masked, gen_seed in random_cases(300, 20261202):
+        d = (W.masked_verify_inputs_numpy(B, K, V, dt, gen_seed) if masked
+             else W.verify_inputs_numpy(B, K, V, dt, "rollout_t", gen_seed))
+        tgt, drf = device_inputs(d)
+        T = torch.from_numpy(d["temperature"]).cuda()
+        out = binding.verify(tgt, drf, torch.from_numpy(d["ids"]).cuda(), T, seed, offset, want_debug=True)
+        ids = W.greedy_ids(d["draft"], dt)
+        out_to = binding.verify_target_only(tgt, torch.from_numpy(ids).cuda(), T, seed, offset, want_debug=True)
+        torch.cuda.synchronize()
+        zt, zd = W.to_float64(d["target"], dt), W.to_float64(d["draft"], dt)
+        T64 = d["temperature"].astype(np.float64)
+        rep = compare_verify(out, oracle.verify_ref(zt, zd, d["ids"], T64, seed, offset), dt)
+        boundary += rep["boundary_rows"]
+        compare_target_only(out_to, verify_target_only_ref(zt, ids, T64, seed, offset), dt)
+    print("boundary rows", boundary)
