@@ -77,9 +77,12 @@ def tv_ref(target_logits, draft_logits, temperature, mode=MODE_E2E, scale=1.0,
 
     target_logits, draft_logits: [N, K, V]; temperature: positive scalar.
     Returns dict with loss (float), loss_per_position [N], overlap [N, K],
-    S [N, K], g [N, K] (chain factors including ``scale``), grad [N, K, V]
-    (or None), and tie_margin [N, K, V] = |log q - log p| used to exclude
-    elements whose indicator is decided by rounding.
+    S [N, K], g [N, K] (chain factors including ``scale``), scale, grad
+    [N, K, V] (or None), and with the gradient also q [N, K, V], grad_weight
+    [N, K, V] = g q / T (grad = grad_weight (1[q <= p] - S)) and tie_margin
+    [N, K, V] = |log q - log p| with tie_condition [N, K, V], the size of
+    the terms log q - log p is formed from, which locate the elements whose
+    indicator is decided by rounding and how far that moves S.
     """
     zt = np.asarray(target_logits, dtype=np.float64)
     zd = np.asarray(draft_logits, dtype=np.float64)
@@ -103,8 +106,15 @@ def tv_ref(target_logits, draft_logits, temperature, mode=MODE_E2E, scale=1.0,
         "logz_target": lzt,
         "logz_draft": lzd,
     }
+    out["scale"] = float(scale)
     if want_grad:
+        out["q"] = q
+        out["grad_weight"] = g[:, :, None] * (1.0 / T) * q
         out["grad"] = g[:, :, None] * (1.0 / T) * q * (ind.astype(np.float64) - S[:, :, None])
         with np.errstate(divide="ignore", invalid="ignore"):
             out["tie_margin"] = np.abs((zd / T - lzd[..., None]) - (zt / T - lzt[..., None]))
+            # size of the terms ln q - ln p is formed from: an evaluation with
+            # unit roundoff u decides 1[q <= p] correctly once tie_margin
+            # exceeds a small multiple of u times this
+            out["tie_condition"] = (np.abs(zd) + np.abs(zt)) / T + np.abs(lzd)[..., None] + np.abs(lzt)[..., None]
     return out

@@ -15,6 +15,8 @@ from paper_2606_12370_amd import workloads as W
 
 BOUNDARY = 1e-6
 TOL = {W.F32: 1e-5, W.BF16: 2e-3}
+TIE_ABS = 2e-6
+TIE_REL = 2.0 ** -22
 
 
 def host_logits(t, dtype):
@@ -107,9 +109,31 @@ def compare_verify(gpu, ref, dtype, rows=None, report=None):
 
 def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True):
     """Compare TV-loss outputs with the oracle (optionally for a subset of
-    positions).  The gradient is compared per (position, step) row in the
-    norm-wise sense, excluding elements whose indicator 1[q <= p] is decided
-    by rounding (|log q - log p| <= BOUNDARY)."""
+    positions).
+
+    Loss: relative tolerance of the dtype, with an absolute floor of
+    1e-6 |scale| N K for losses near zero (each of the N K overlaps carries a
+    float32 rounding of about 1e-7 of its value, so 1 - alpha cannot be
+    resolved below that).
+
+    Gradient, per (position, step) row, norm-wise: the indicator 1[q <= p] of
+    an element whose |log q - log p| <= TIE_ABS + TIE_REL * tie_condition is
+    decided by rounding (min(p, q) has a kink there and either side is a valid
+    subgradient): float32 evaluation of log q - log p from logits z / T, row
+    maxima and log-normalisers makes a handful of roundings of 2^-24 relative
+    to the size of those terms (tie_condition), plus the normalisers' own
+    summation error (TIE_ABS).  So
+    such elements are not compared.  The same bound is the relative error of
+    each q_j, and S = sum 1[q <= p] q carries both the tied elements and
+    those errors, so the rest of the row may differ from the oracle by one
+    common shift of S: grad_j - ref_j = -w_j dS with w = g q / T and |dS| <=
+    sum_{ties} q + sum q_j qerr_j.  That freedom matters where one token
+    holds nearly all the mass: S is then 1 - O(q of the rest), the row's
+    gradient is the small difference w (1 - S), and a float32 S (one ulp of
+    1 is 1.2e-7) moves it by far more than the dtype tolerance of its size.
+    dS is fitted by least squares over the untied elements and clipped to
+    that slack; what remains beyond each element's own q error, |ref_j|
+    qerr_j, must be within the tolerance times the row's largest gradient."""
     tol = TOL[dtype]
     ov = ov_g.cpu().numpy().astype(np.float64)
     if positions is not None:
@@ -119,8 +143,12 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
     out = {"max_rel_overlap": float(e_ov)}
     if loss_exact:
         lg = float(loss_g.cpu().numpy()[0])
-        e_l = abs(lg - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
-        assert e_l <= tol, "loss relative error %.3e (gpu %r, oracle %r)" % (e_l, lg, ref["loss"])
+        n_units = ref["overlap"].size
+        floor = 1e-6 * abs(ref.get("scale", 1.0)) * n_units
+        err = abs(lg - ref["loss"])
+        e_l = err / max(abs(ref["loss"]), 1e-30)
+        assert err <= tol * abs(ref["loss"]) + floor, "loss relative error %.3e (gpu %r, oracle %r)" % (
+            e_l, lg, ref["loss"])
         out["rel_loss"] = float(e_l)
     if grad_g is not None:
         g = grad_g
@@ -128,13 +156,28 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
             g = g[torch.as_tensor(positions, device=g.device)]
         g = g.cpu().numpy().astype(np.float64)
         gr = ref["grad"]
-        tie = ref["tie_margin"] <= BOUNDARY
-        diff = np.where(tie, 0.0, np.abs(g - gr)).max(axis=-1)
+        # relative error bound of q_j from its float32 log-domain evaluation,
+        # which is also the window inside which 1[q <= p] is rounding-decided
+        qerr = TIE_ABS + TIE_REL * ref["tie_condition"]
+        tie = ref["tie_margin"] <= qerr
+        untied = ~tie
+        d = np.where(untied, g - gr, 0.0)
+        w = ref["grad_weight"]
+        q = ref["q"]
+        s_slack = np.where(tie, q, 0.0).sum(axis=-1) + (q * qerr).sum(axis=-1)
+        num = (d * w).sum(axis=-1)
+        den = np.where(untied, w * w, 0.0).sum(axis=-1)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            dS = np.where(den > 0, -num / den, 0.0)
+        dS = np.clip(dS, -s_slack, s_slack)
+        resid = np.abs(d + w * dS[..., None]) - np.abs(gr) * qerr
+        resid = np.where(untied, np.maximum(resid, 0.0), 0.0).max(axis=-1)
         scale = np.maximum(np.abs(gr).max(axis=-1), 1e-300)
-        worst = float((diff / scale).max())
+        worst = float((resid / scale).max())
         assert worst <= tol, "gradient norm-wise relative error %.3e" % worst
         out["max_normwise_grad"] = worst
         out["tie_elements"] = int(tie.sum())
+        out["rows_with_shifted_S"] = int((np.abs(dS) > 0).sum())
     return out
 
 
