@@ -19,6 +19,14 @@ loss = scale * sum_n L_n; grad = d loss / d z_draft.
 Readings: the K draft steps are averaged (each MTP head has its own
 objective, as for the per-step TV loss); the paper derives the gradients at
 T = 1 and the 1/T factor of softmax(z / T) is included here.
+
+Precision: the gradients are differences of probabilities (q - p) and of
+log-probabilities (log q - log p - L).  Where one token holds all but 1e-10
+of both distributions, q - p of that token is a difference of two numbers
+within 1e-10 of 1, and float64 keeps only about six of its digits.  The
+softmax, the differences and the sums are therefore evaluated in extended
+precision (numpy.longdouble, a 64-bit significand on x86-64), then returned
+as float64.
 """
 
 import numpy as np
@@ -28,9 +36,12 @@ KIND_CE = 1
 KIND_REVERSE = 2
 
 
+XP = np.longdouble
+
+
 def log_softmax_t(z, T):
-    """log softmax(z / T) along the last axis, float64."""
-    a = np.asarray(z, dtype=np.float64) / T
+    """log softmax(z / T) along the last axis, in extended precision."""
+    a = np.asarray(z, dtype=XP) / XP(T)
     m = np.max(a, axis=-1, keepdims=True)
     with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
         lse = m + np.log(np.sum(np.exp(a - m), axis=-1, keepdims=True))
@@ -39,27 +50,28 @@ def log_softmax_t(z, T):
 
 def kl_ref(target_logits, draft_logits, temperature, kind, scale=1.0):
     """target_logits, draft_logits: [N, K, V].  Returns per_step [N, K]
-    (L_{n,k}), loss (float) and grad [N, K, V] (d loss / d z_draft)."""
+    (L_{n,k}), loss (float) and grad [N, K, V] (d loss / d z_draft), float64."""
     zt = np.asarray(target_logits, dtype=np.float64)
     zd = np.asarray(draft_logits, dtype=np.float64)
     N, K, V = zd.shape
-    T = float(temperature)
+    T = XP(float(temperature))
     lp = log_softmax_t(zt, T)
     lq = log_softmax_t(zd, T)
     p = np.exp(lp)
     q = np.exp(lq)
     with np.errstate(invalid="ignore"):
         if kind == KIND_FORWARD:
-            L = np.where(p > 0, p * (lp - lq), 0.0).sum(axis=-1)
+            L = np.where(p > 0, p * (lp - lq), XP(0)).sum(axis=-1)
             g = (q - p) / T
         elif kind == KIND_CE:
-            L = np.where(p > 0, -p * lq, 0.0).sum(axis=-1)
+            L = np.where(p > 0, -p * lq, XP(0)).sum(axis=-1)
             g = (q - p) / T
         elif kind == KIND_REVERSE:
-            L = np.where(q > 0, q * (lq - lp), 0.0).sum(axis=-1)
-            g = np.where(q > 0, q * (lq - lp - L[..., None]), 0.0) / T
+            L = np.where(q > 0, q * (lq - lp), XP(0)).sum(axis=-1)
+            g = np.where(q > 0, q * (lq - lp - L[..., None]), XP(0)) / T
         else:
             raise ValueError(kind)
     loss_pos = L.mean(axis=1)
-    return {"per_step": L, "loss": float(scale * loss_pos.sum()), "loss_pos": scale * loss_pos,
-            "grad": g * (scale / K)}
+    sc = XP(float(scale))
+    return {"per_step": L.astype(np.float64), "loss": float(sc * loss_pos.sum()),
+            "loss_pos": (sc * loss_pos).astype(np.float64), "grad": (g * (sc / K)).astype(np.float64)}

@@ -99,3 +99,37 @@ def test_loss_reduction_and_zero_weights():
     assert np.isfinite(f["per_step"]).all() and np.isfinite(r["per_step"]).all()
     assert np.all(np.isfinite(r["grad"]))
     np.testing.assert_allclose(f["per_step"][0, 0], stats.entropy([0, 1 / 3, 1 / 3, 1 / 3], [0.25] * 4), rtol=1e-13)
+
+
+def test_dominant_token_gradient_against_50_digit_arithmetic():
+    """One token holding all but about 4e-10 of both distributions: its
+    gradient (q - p) / T and the reverse-KL gradient q (log q - log p - L) / T
+    are differences of numbers within 1e-9 of each other.  The oracle's values
+    equal an evaluation in 50-digit arithmetic (mpmath), element by element,
+    to 1e-9 of the row's largest gradient."""
+    mpmath = pytest.importorskip("mpmath")
+    mpmath.mp.dps = 50
+    rng = np.random.default_rng(5)
+    V, T = 64, 0.7
+    zt = rng.normal(0.0, 1.0, size=(1, 1, V))
+    zt[0, 0, 17] = 16.0
+    zd = zt + rng.normal(0.0, 0.3, size=(1, 1, V))
+    zd[0, 0, 17] = zt[0, 0, 17] + 0.4
+    for kind in (KIND_FORWARD, KIND_REVERSE):
+        g = kl_ref(zt, zd, T, kind)["grad"][0, 0]
+        a = [mpmath.mpf(float(x)) / mpmath.mpf(T) for x in zt[0, 0]]
+        b = [mpmath.mpf(float(x)) / mpmath.mpf(T) for x in zd[0, 0]]
+        la = mpmath.log(mpmath.fsum(mpmath.exp(x) for x in a))
+        lb = mpmath.log(mpmath.fsum(mpmath.exp(x) for x in b))
+        lp = [x - la for x in a]
+        lq = [x - lb for x in b]
+        q = [mpmath.exp(x) for x in lq]
+        assert 1 - q[17] < 1e-8
+        if kind == KIND_FORWARD:
+            exact = [(mpmath.exp(y) - mpmath.exp(x)) / mpmath.mpf(T) for x, y in zip(lp, lq)]
+        else:
+            L = mpmath.fsum(qi * (y - x) for qi, x, y in zip(q, lp, lq))
+            exact = [qi * (y - x - L) / mpmath.mpf(T) for qi, x, y in zip(q, lp, lq)]
+        exact = np.array([float(e) for e in exact])
+        scale = np.abs(exact).max()
+        assert np.abs(g - exact).max() <= 1e-9 * scale, (kind, np.abs(g - exact).max() / scale)
