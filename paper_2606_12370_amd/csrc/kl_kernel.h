@@ -3,21 +3,40 @@
 // footnote, Table grad_comparison, App. B, App. C): the objectives the TV
 // loss is compared against.
 //
-//   1 row_stats, 2 row_norm (sv_device.h): each row's reference M and
-//                 normaliser, for the gradient.
+//   1 kl_stats    every target and draft row, one wave per sub-chunk: the
+//                 largest logit, how many elements hold it, and the sum of
+//                 2^(z s - r) over every other element (r an integer
+//                 reference), so that log2 of a normaliser dominated by one
+//                 token is formed as log1p of a sum of small terms, not as
+//                 the logarithm of a float32 sum near 1.
+//   2 kl_norm     each row's log2 partition function in float64 and its
+//                 per-element reference.
 //   3 kl_pass     per (position n, step k, chunk), with t = z_t s - M_t and
 //                 u = z_d s - M_d (log2 units), e = 2^t, f = 2^u: Se = sum e,
 //                 Sf = sum f and the weighted log-ratio sum W (forward:
-//                 sum e (t - u); CE: sum e (-u); reverse: sum f (u - t)), all
-//                 in float64 from the same e, f, t, u, so the loss (formed in
-//                 kl_coef) is normalised by its own sums: a small KL is not
-//                 swamped by the rounding of a separately computed log Z.
-//                 Forward KL and CE also write the gradient (q - p) here,
-//                 since it needs no global sum.
+//                 sum e (t - u); CE: sum e (-u)), all in float64 from the same
+//                 e, f, t, u, so the loss (formed in kl_coef) is normalised by
+//                 its own sums; for reverse KL the sums of f and f d over the
+//                 elements other than the draft's largest logit, and of f d
+//                 over those, with d = log2 q - log2 p.  Forward KL and CE
+//                 also write the gradient (q - p) here, since it needs no
+//                 global sum.
 //   4 kl_coef     per position: L_{n,k} from its chunks, the per-step output,
 //                 the position loss, the reverse-KL gradient constants.
 //   5 kl_grad     reverse KL only: q (log q - log p - L), read again.
 //   6 kl_loss     position losses added in a fixed order.
+//
+// Where p and q nearly agree, q - p and log q - log p are small differences
+// of large terms.  Both are formed from d = log2 q - log2 p, taken in float64
+// as ((z_d - z_t) - (zmax_d - zmax_t)) s + (lam_t - lam_d) with
+// lam = log2 Z - zmax s: the logits enter as exact differences and lam
+// carries no float32 rounding of a sum near 1.
+// Then q - p = sign(d) max(p, q) (1 - 2^-|d|), with 1 - 2^-x from its series
+// for small x.  For reverse KL, the term log q_j - log p_j - L of the element
+// holding nearly all of q is a difference of two nearly equal numbers; with
+// L = ln2 sum_i q_i d_i and sum_i q_i = 1 it equals
+// ln2 sum_{i != j} q_i (d_j - d_i), which is formed from the sums over the
+// other elements instead.
 #pragma once
 
 #include "sv_device.h"
@@ -28,8 +47,32 @@ constexpr int kKlForward = 0;
 constexpr int kKlCe = 1;
 constexpr int kKlReverse = 2;
 
+// Statistics of one sub-chunk of a row: its largest logit zmax, the number n
+// of elements equal to it, and R = sum over the other elements of
+// 2^(z s - r), r = ceil(zmax s) (an integer, so rescaling between
+// references is exact).
+struct KlStat {
+  float zmax;
+  int n;
+  double R;
+};
+
+// A row's normaliser: p_v = 2^(z_v s - M) / D with M the integer reference.
+// The log2 partition function is zmax s + lam; lam is kept apart because
+// zmax s is large and its float64 rounding would swamp the log ratio of a
+// token that holds nearly all the mass.
+struct KlNorm {
+  float M;
+  float invD;
+  float zmax;
+  int n;
+  double lam;  // log2(n + R 2^-(zmax s - M)) = log2 Z - zmax s
+  double D;
+};
+
 struct KlPart {  // one chunk of a (position, step) pair
   double se, sf, w;
+  double sfx, wx, wm;  // reverse KL: sum f, sum f d over the non-largest draft elements; sum f d over the largest
 };
 
 struct KlArgs {
@@ -38,13 +81,178 @@ struct KlArgs {
   double scale;
   float inv_t;
   float* loss; float* per_step; float* grad;
-  const RowStat* stats;  // [2 N K][C]
-  const RowNorm* norms;  // [2 N K]
+  KlStat* stats;         // [2 N K][SC]
+  int SC;                // sub-chunks per row of the statistics pass
+  KlNorm* norms;         // [2 N K]
   KlPart* parts;         // [N K][C]
-  float2* coef;          // [N K]: reverse-KL gradient constants
+  float4* coef;          // [N K]: reverse-KL gradient constants
   double* loss_pos;      // [N]
   int vec_g;
 };
+
+// 2^(z s - r).  With CORR the exponent is carried beyond float32: z s = h + l
+// exactly (h = z s rounded, l = fma(z, s, -h)), h - r is exact wherever h and
+// the integer r are within a factor of two (the elements that carry the
+// weight of the sum), and the dropped l enters to first order,
+// 2^(h - r) (1 + l ln2).  Without CORR the exponent is fma(z, s, -r), rounded
+// once.
+template <bool CORR>
+__device__ __forceinline__ float kl_term(float z, float s, float r) {
+  if constexpr (CORR) {
+    const float h = z * s;
+    const float l = fmaf(z, s, -h);
+    const float e = __builtin_amdgcn_exp2f(h - r);
+    return e > 0.f ? fmaf(e * 0.69314718f, l, e) : e;  // 0, or NaN for a NaN logit
+  } else {
+    return __builtin_amdgcn_exp2f(fmaf(z, s, -r));
+  }
+}
+
+// Statistics of every row at sub-chunk granularity, one wave per sub-chunk
+// (ST tiles of 256 vectors, streamed S vectors per lane at a time).  Each
+// lane keeps its largest logit, how often it occurred and the float64 sum of
+// its other elements relative to its own reference; one wave maximum and
+// float64 wave sums give the sub-chunk's record.
+template <class E, int ST, int S, bool CORR>
+__global__ __launch_bounds__(kThreads) void kl_stats_wave_kernel(RowsDesc d, int SC, KlStat* __restrict__ stats,
+                                                                 int64_t nsub) {
+  constexpr int EPV = E::EPV;
+  constexpr int WV = ST * (kThreads / 64);
+  static_assert(WV % S == 0, "whole load steps per sub-chunk");
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  if (g >= nsub) return;
+  const int r = static_cast<int>(g / SC), j = static_cast<int>(g - static_cast<int64_t>(g / SC) * SC);
+  int b;
+  bool aligned;
+  const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+  const float s = scale_of(d.temp_scalar);
+  const int e0 = j * WV * 64 * EPV;
+  float zm = -INFINITY, rf = 0.f;
+  int n = 0;
+  double R = 0.0;
+#pragma unroll 1
+  for (int st = 0; st < WV / S; ++st) {
+    const int es = e0 + st * S * 64 * EPV;
+    if (es >= d.V) break;
+    float x[S][EPV];
+    load_span<E, S, 64>(row, es, lane, d.V, aligned, x);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[i][k]);
+    if (mx > zm) {  // a new largest logit: the old one joins the other elements
+      const float nr = ceilf(mx * s);
+      if (zm != -INFINITY)
+        R = ldexp(R, static_cast<int>(rf - nr)) + static_cast<double>(n) * static_cast<double>(kl_term<CORR>(zm, s, nr));
+      zm = mx;
+      rf = nr;
+      n = 0;
+    }
+    if (zm != -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < S; ++i) {
+        float acc = 0.f;
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) {
+          const float z = x[i][k];
+          const float e = kl_term<CORR>(z, s, rf);
+          const bool top = z == zm;
+          n += top ? 1 : 0;
+          acc += top ? 0.f : e;
+        }
+        R += static_cast<double>(acc);
+      }
+    }
+  }
+  const float zw = wave_max(zm);
+  double Rl = 0.0;
+  int nl = 0;
+  if (zm == zw) {
+    nl = n;
+    Rl = R;
+  } else if (zm != -INFINITY) {  // this lane's largest logit is one of the others
+    const float rw = ceilf(zw * s);
+    Rl = ldexp(R, static_cast<int>(rf - rw)) + static_cast<double>(n) * static_cast<double>(kl_term<CORR>(zm, s, rw));
+  }
+  if (R != R) Rl = R;  // NaN propagates (data error)
+  Rl = wave_sum(Rl);
+  double nd = wave_sum(static_cast<double>(nl));
+  if (lane == 0) {
+    KlStat o;
+    o.zmax = zw;
+    o.n = static_cast<int>(nd);
+    o.R = Rl;
+    stats[g] = o;
+  }
+}
+
+// One wave per row: combine the row's SC sub-chunk records into its integer
+// reference M, 1/D and lam = log2(n) + log1p(R / (n 2^(zmax s - M))) / ln 2,
+// the log2 partition function less zmax s.
+__global__ __launch_bounds__(kThreads) void kl_norm_kernel(const KlStat* __restrict__ stats, int rows, int SC,
+                                                           float s, KlNorm* __restrict__ out) {
+  const int r = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const KlStat* st = stats + static_cast<int64_t>(r) * SC;
+  float zm = -INFINITY;
+  for (int c = lane; c < SC; c += 64) zm = fmaxf(zm, st[c].zmax);
+  zm = wave_max(zm);
+  const float rf = ceilf(zm * s);
+  const double zs = static_cast<double>(zm) * static_cast<double>(s);  // exact
+  double R = 0.0, nn = 0.0;
+  bool nan = false;
+  for (int c = lane; c < SC; c += 64) {
+    const KlStat k = st[c];
+    if (k.R != k.R) nan = true;
+    if (k.zmax == -INFINITY) continue;
+    if (k.zmax == zm) {
+      nn += k.n;
+      R += k.R;
+    } else {
+      const float rc = ceilf(k.zmax * s);
+      R += ldexp(k.R, static_cast<int>(rc - rf)) +
+           static_cast<double>(k.n) * exp2(static_cast<double>(k.zmax) * static_cast<double>(s) - rf);
+    }
+  }
+  R = wave_sum(R);
+  nn = wave_sum(nn);
+  nan = __ballot(nan) != 0;
+  if (lane == 0) {
+    KlNorm o;
+    o.M = rf;
+    o.zmax = zm;
+    o.n = static_cast<int>(nn);
+    const double mt = exp2(zs - static_cast<double>(rf));
+    o.D = nn * mt + R;
+    o.lam = log2(nn) + log1p(R / (nn * mt)) * kLog2eD;
+    if (nan) { o.D = NAN; o.lam = NAN; }
+    o.invD = static_cast<float>(1.0 / o.D);
+    out[r] = o;
+  }
+}
+
+// log2 q - log2 p of one element in float64,
+// ((z_d - z_t) - (zmax_d - zmax_t)) s + (lam_t - lam_d): every logit
+// difference is exact, and at the element holding both rows' largest logit
+// only lam_t - lam_d remains, which carries no float32 sum near 1.
+struct KlDelta {
+  double c1;   // zmax_d - zmax_t
+  double lam;  // lam_t - lam_d
+  double s;
+};
+__device__ __forceinline__ KlDelta kl_delta_ref(const KlNorm& t, const KlNorm& d, float s) {
+  KlDelta r;
+  r.c1 = static_cast<double>(d.zmax) - static_cast<double>(t.zmax);
+  r.lam = t.lam - d.lam;
+  r.s = static_cast<double>(s);
+  return r;
+}
+__device__ __forceinline__ float kl_delta(float zt, float zd, const KlDelta& r) {
+  return static_cast<float>(fma((static_cast<double>(zd) - static_cast<double>(zt)) - r.c1, r.s, r.lam));
+}
 
 // Write EPV gradient values of one vector (float4 stores when aligned).
 template <int EPV>
@@ -66,7 +274,7 @@ template <class E, int NT, int S, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
-  __shared__ RedLds<4> red;
+  __shared__ RedLds<6> red;
   const RowsDesc& d = a.rows;
   const int C = d.C, V = d.V, NK = a.N * a.K;
   const bool write_grad = a.grad != nullptr && KIND != kKlReverse;
@@ -78,11 +286,12 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
     const typename E::raw* rt = row_of<E>(d, u, &bb, &al_t);
     const typename E::raw* rd = row_of<E>(d, NK + u, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
-    const RowNorm nt = a.norms[u], nd = a.norms[NK + u];
+    const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
+    const KlDelta dr = kl_delta_ref(nt, nd, s);
     float* gr = write_grad ? a.grad + static_cast<int64_t>(u) * V : nullptr;
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
-    double se = 0.0, sf = 0.0, w = 0.0;
+    double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0;
 #pragma unroll
     for (int j0 = 0; j0 < NT; j0 += S) {
       if (j0 >= nt_tiles) break;
@@ -93,34 +302,53 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
       for (int j = 0; j < S; ++j) {
         float gv[EPV];
         // the EPV elements of one vector are summed in float32, vectors in float64
-        float ve = 0.f, vf = 0.f, vw = 0.f;
+        float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f;
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
           const float tt = fmaf(xt[j][k], s, -nt.M);
           const float uu = fmaf(xd[j][k], s, -nd.M);
           const float e = __builtin_amdgcn_exp2f(tt);
           const float f = __builtin_amdgcn_exp2f(uu);
+          const float dl = kl_delta(xt[j][k], xd[j][k], dr);
           float term;
           if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
           else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
-          else term = f > 0.f ? f * (uu - tt) : 0.f;
+          else term = 0.f;
+          if (KIND == kKlReverse) {
+            const float fd = f > 0.f ? f * dl : 0.f;
+            const bool top = xd[j][k] == nd.zmax;
+            vfx += top ? 0.f : f;
+            vwx += top ? 0.f : fd;
+            vwm += top ? fd : 0.f;
+          }
           ve += e;
           vf += f;
           vw += term;
-          gv[k] = gcoef * (f * nd.invD - e * nt.invD);  // (q - p) scale / (K T)
+          if (KIND != kKlReverse) {
+            // (q - p) scale / (K T) = sign(d) max(p, q) (1 - 2^-|d|) scale / (K T)
+            const float mx = fmaxf(e * nt.invD, f * nd.invD);
+            const float g = mx * one_minus_exp2_neg(fabsf(dl));
+            gv[k] = mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
+          }
         }
         se += static_cast<double>(ve);
         sf += static_cast<double>(vf);
         w += static_cast<double>(vw);
+        if (KIND == kKlReverse) {
+          sfx += static_cast<double>(vfx);
+          wx += static_cast<double>(vwx);
+          wm += static_cast<double>(vwm);
+        }
         if (write_grad)
           store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }
     }
-    double v[4] = {se, sf, w, 0.0};
-    wg_sum<4>(v, red);
+    double v[6] = {se, sf, w, sfx, wx, wm};
+    wg_sum<6>(v, red);
     if (threadIdx.x == 0) {
       KlPart o;
       o.se = v[0]; o.sf = v[1]; o.w = v[2];
+      o.sfx = v[3]; o.wx = v[4]; o.wm = v[5];
       a.parts[t] = o;
     }
   }
@@ -135,26 +363,37 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
   const int C = a.rows.C, K = a.K;
   double Ln = 0.0;
   for (int kk = 0; kk < K; ++kk) {
-    double se = 0.0, sf = 0.0, w = 0.0;
+    double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0;
     const KlPart* ps = a.parts + static_cast<int64_t>(n * K + kk) * C;
-    for (int cc = lane; cc < C; cc += 64) { se += ps[cc].se; sf += ps[cc].sf; w += ps[cc].w; }
+    for (int cc = lane; cc < C; cc += 64) {
+      se += ps[cc].se; sf += ps[cc].sf; w += ps[cc].w;
+      sfx += ps[cc].sfx; wx += ps[cc].wx; wm += ps[cc].wm;
+    }
     se = wave_sum(se);
     sf = wave_sum(sf);
     w = wave_sum(w);
-    const double le = log2(se), lf = log2(sf);
-    double L;  // log2 units
-    if (a.kind == kKlForward) L = w / se - le + lf;
-    else if (a.kind == kKlCe) L = w / se + lf;
-    else L = w / sf - lf + le;
-    L *= kLn2D;
-    Ln += L;
-    if (lane == 0) {
-      if (a.per_step) a.per_step[static_cast<int64_t>(n) * K + kk] = static_cast<float>(L);
-      // reverse-KL gradient: scale/(K T) q (ln2 (u - t + le - lf) - L), q = f / sf
-      const double A = a.scale * static_cast<double>(a.inv_t) / K * kLn2D / sf;
-      a.coef[static_cast<int64_t>(n) * K + kk] =
-          make_float2(static_cast<float>(A), static_cast<float>(le - lf - L / kLn2D));
+    double L;  // nats
+    if (a.kind == kKlReverse) {
+      sfx = wave_sum(sfx);
+      wx = wave_sum(wx);
+      wm = wave_sum(wm);
+      // L = ln2 sum_j q_j d_j with q_j = f_j / Sf
+      const double mu = (wx + wm) / sf;
+      L = kLn2D * mu;
+      if (lane == 0) {
+        // gradient: scale/(K T) q (ln2 (d - mu)), or, for the draft's single
+        // largest element, scale/(K T) q ln2 (d Sfx - Wx) / Sf
+        const double A = a.scale * static_cast<double>(a.inv_t) / K * kLn2D / sf;
+        a.coef[static_cast<int64_t>(n) * K + kk] = make_float4(static_cast<float>(A), static_cast<float>(mu),
+                                                               static_cast<float>(sfx / sf), static_cast<float>(wx / sf));
+      }
+    } else {
+      const double le = log2(se), lf = log2(sf);
+      L = (a.kind == kKlForward) ? w / se - le + lf : w / se + lf;
+      L *= kLn2D;
     }
+    Ln += L;
+    if (lane == 0 && a.per_step) a.per_step[static_cast<int64_t>(n) * K + kk] = static_cast<float>(L);
   }
   if (lane == 0) a.loss_pos[n] = a.scale * Ln / K;
 }
@@ -172,8 +411,10 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
     const typename E::raw* rt = row_of<E>(d, u, &bb, &al_t);
     const typename E::raw* rd = row_of<E>(d, NK + u, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
-    const float Mt = a.norms[u].M, Md = a.norms[NK + u].M;
-    const float2 A = a.coef[u];
+    const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
+    const KlDelta dr = kl_delta_ref(nt, nd, s);
+    const float4 A = a.coef[u];
+    const bool single_top = nd.n == 1;
     float* gr = a.grad + static_cast<int64_t>(u) * V;
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
@@ -188,10 +429,10 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
         float gv[EPV];
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
-          const float tt = fmaf(xt[j][k], s, -Mt);
-          const float uu = fmaf(xd[j][k], s, -Md);
-          const float f = __builtin_amdgcn_exp2f(uu);
-          gv[k] = f > 0.f ? A.x * f * ((uu - tt) + A.y) : 0.f;
+          const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
+          const float dl = kl_delta(xt[j][k], xd[j][k], dr);
+          const float tm = (single_top && xd[j][k] == nd.zmax) ? fmaf(dl, A.z, -A.w) : dl - A.y;
+          gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
         }
         store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <type_traits>
 #include <utility>
 
 #include "specverify.h"
@@ -135,12 +136,13 @@ struct KlLayout {
 KlLayout kl_layout(int N, int K, int V, spec_dtype dt) {
   KlLayout L;
   const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  const size_t SC = static_cast<size_t>(sub_chunks(V, dt));
   const size_t rows = static_cast<size_t>(N) * 2 * K;
   size_t off = 0;
-  L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
-  L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
+  L.stats = off; off = align_up(off + rows * SC * sizeof(sv::KlStat), 256);
+  L.norms = off; off = align_up(off + rows * sizeof(sv::KlNorm), 256);
   L.parts = off; off = align_up(off + static_cast<size_t>(N) * K * C * sizeof(sv::KlPart), 256);
-  L.coef = off; off = align_up(off + static_cast<size_t>(N) * K * sizeof(float2), 256);
+  L.coef = off; off = align_up(off + static_cast<size_t>(N) * K * sizeof(float4), 256);
   L.loss = off; off = align_up(off + static_cast<size_t>(N) * sizeof(double), 256);
   L.total = off;
   return L;
@@ -274,12 +276,16 @@ template <class E, int NT, int KIND>
 spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
   const int64_t units = int64_t{a.N} * a.K;
   const int C = a.rows.C;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(2 * units * C)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), 2 * units * C);
-  hipLaunchKernelGGL(sv::row_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
-                     dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C,
-                     const_cast<sv::RowNorm*>(a.norms));
+  // statistics per sub-chunk, one wave each; float32 logits carry their
+  // exponents beyond float32 (their tolerance is 200 times tighter)
+  const int64_t nsub = 2 * units * a.SC;
+  constexpr bool kCorr = std::is_same<E, sv::F32>::value;
+  hipLaunchKernelGGL((sv::kl_stats_wave_kernel<E, kStep, kStatVec, kCorr>),
+                     dim3(static_cast<unsigned>((nsub + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s,
+                     a.rows, a.SC, a.stats, nsub);
+  hipLaunchKernelGGL(sv::kl_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
+                     dim3(sv::kThreads), 0, s, static_cast<const sv::KlStat*>(a.stats), static_cast<int>(2 * units),
+                     a.SC, sv::scale_of(a.rows.temp_scalar), a.norms);
   // the passes that may write the gradient read bf16 as 4-element vectors: one float4 store per lane
   using G = typename GradElem<E>::type;
   constexpr int NTG = kChunkElems / (sv::kThreads * G::EPV);
@@ -697,10 +703,11 @@ spec_status spec_kl_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   a.inv_t = 1.0f / temperature;
   a.loss = loss; a.per_step = per_step; a.grad = grad_draft;
   char* ws = static_cast<char*>(workspace);
-  a.stats = reinterpret_cast<const sv::RowStat*>(ws + L.stats);
-  a.norms = reinterpret_cast<const sv::RowNorm*>(ws + L.norms);
+  a.stats = reinterpret_cast<sv::KlStat*>(ws + L.stats);
+  a.SC = sub_chunks(V, dtype);
+  a.norms = reinterpret_cast<sv::KlNorm*>(ws + L.norms);
   a.parts = reinterpret_cast<sv::KlPart*>(ws + L.parts);
-  a.coef = reinterpret_cast<float2*>(ws + L.coef);
+  a.coef = reinterpret_cast<float4*>(ws + L.coef);
   a.loss_pos = reinterpret_cast<double*>(ws + L.loss);
   a.vec_g = (grad_draft && aligned16(grad_draft) && (V % 4 == 0)) ? 1 : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);

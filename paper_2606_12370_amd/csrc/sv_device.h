@@ -302,7 +302,7 @@ struct RowStat {
   double D;    // sum of 2^(z s - m) over the chunk
 };
 
-__device__ __forceinline__ float scale_of(float T) {
+__host__ __device__ __forceinline__ float scale_of(float T) {
   return static_cast<float>(kLog2eD / static_cast<double>(T));
 }
 
@@ -436,6 +436,23 @@ __device__ __forceinline__ float prob(float z, float s, float M, float invD) {
 // One more rounding than prob() (L enters as a float), about 1e-6 relative.
 __device__ __forceinline__ float min_prob(float zt, float zd, float s, const RowNorm& t, const RowNorm& d) {
   return __builtin_amdgcn_exp2f(fminf(fmaf(zt, s, -t.M) - t.L, fmaf(zd, s, -d.M) - d.L));
+}
+
+// 1 - 2^-x for x >= 0: the series of -expm1(-y), y = x ln2, below x = 1/2
+// (degree 9, truncation below 3e-10 of the value), the exponential above.
+__device__ __forceinline__ float one_minus_exp2_neg(float x) {
+  const float y = x * 0.69314718f;
+  float p = 1.f / 362880.f;
+  p = fmaf(p, -y, 1.f / 40320.f);
+  p = fmaf(p, -y, 1.f / 5040.f);
+  p = fmaf(p, -y, 1.f / 720.f);
+  p = fmaf(p, -y, 1.f / 120.f);
+  p = fmaf(p, -y, 1.f / 24.f);
+  p = fmaf(p, -y, 1.f / 6.f);
+  p = fmaf(p, -y, 0.5f);
+  p = fmaf(p, -y, 1.f);
+  const float small = y * p;
+  return x < 0.5f ? small : 1.f - __builtin_amdgcn_exp2f(-x);
 }
 
 // Rows of a batch: target rows (b, i) for i < tper, then draft rows (b, i)

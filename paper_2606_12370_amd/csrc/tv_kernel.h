@@ -6,14 +6,18 @@
 //   1 row_stats   (sv_device.h) per-chunk statistics of every target and
 //                 draft row of the N positions x K steps.
 //   2 row_norm    (sv_device.h) each row's normaliser.
-//   3 tv_pair     per (position n, step k, chunk): alpha partial sum min(p, q)
-//                 and S partial sum 1[q <= p] q.
+//   3 tv_pair     per (position n, step k, chunk): alpha partial sum min(p, q),
+//                 S partial sum 1[q <= p] q and its complement 1 - S summed
+//                 directly as sum 1[q > p] q (where one token holds nearly
+//                 all of q, 1 - S formed from a float32 S near 1 would carry
+//                 its rounding as a large relative error).
 //   4 tv_coef     per position: alpha_k and S_k of its K steps (chunk order
 //                 fixed), the chain factors g_k = dL_n/dalpha_k of the selected
 //                 loss from prefix / suffix products, the position loss L_n,
 //                 alpha[n, :], and the two gradient coefficients of each step.
 //   5 tv_grad     per (position, step, chunk): grad = q * (1[q <= p] ? A1 : A0)
-//                 with A1 = scale g_k (1 - S_k) / T, A0 = -scale g_k S_k / T,
+//                 with A1 = scale g_k (1 - S_k) / T (from the complement sum),
+//                 A0 = -scale g_k S_k / T,
 //                 written once (skipped for a forward-only call).
 //   6 tv_loss     one workgroup adds the N position losses in a fixed order.
 // The indicator 1[q <= p] is decided once, in launch 3, on log2 q <= log2 p
@@ -27,7 +31,8 @@ namespace sv {
 
 struct TvPair {
   double alpha;
-  double S;
+  double S;   // sum 1[q <= p] q
+  double Sc;  // sum 1[q > p] q, the complement of S summed directly
 };
 
 struct TvArgs {
@@ -124,7 +129,7 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, d.ntiles - tile0);
     static_assert(NT * EPV <= 64, "indicator bits of a chunk fit one word per thread");
-    float al = 0.f, sq = 0.f;
+    float al = 0.f, sq = 0.f, sc = 0.f;
     uint64_t mbits = 0;
 #pragma unroll
     for (int j0 = 0; j0 < NT; j0 += S) {
@@ -145,6 +150,8 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
           al += mn;
           const bool le = lq <= lp;
           sq += le ? mn : 0.f;
+          // q itself where q > p (min(p, q) is p there)
+          sc += le ? 0.f : __builtin_amdgcn_exp2f(lq);
           m |= le ? (1u << kk) : 0u;
         }
         mbits |= static_cast<uint64_t>(m) << ((j0 + j) * EPV);
@@ -156,11 +163,11 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
     if (a.bits)
       __builtin_nontemporal_store(mbits, reinterpret_cast<uint64_t*>(a.bits + static_cast<int64_t>(u) * a.bits_stride) +
                                              static_cast<int64_t>(c) * kChunkWords + threadIdx.x);
-    double v[4] = {static_cast<double>(al), static_cast<double>(sq), 0.0, 0.0};
+    double v[4] = {static_cast<double>(al), static_cast<double>(sq), static_cast<double>(sc), 0.0};
     wg_sum<4>(v, red);
     if (threadIdx.x == 0) {
       TvPair o;
-      o.alpha = v[0]; o.S = v[1];
+      o.alpha = v[0]; o.S = v[1]; o.Sc = v[2];
       a.pairs[t] = o;
     }
   }
@@ -169,18 +176,19 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
 // Per position (one wave each, 4 per workgroup): alpha_k, S_k, the chain
 // factors, the loss L_n, alpha[n, :] and the gradient coefficients.
 __global__ __launch_bounds__(kThreads) void tv_coef_kernel(TvArgs a) {
-  __shared__ double al[kWaves][SPEC_MAX_K_DEV], S[kWaves][SPEC_MAX_K_DEV];
+  __shared__ double al[kWaves][SPEC_MAX_K_DEV], S[kWaves][SPEC_MAX_K_DEV], Sc[kWaves][SPEC_MAX_K_DEV];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n = blockIdx.x * kWaves + wave;
   if (n >= a.N) return;
   const int C = a.rows.C, K = a.K;
   for (int kk = 0; kk < K; ++kk) {
-    double x = 0.0, y = 0.0;
+    double x = 0.0, y = 0.0, z = 0.0;
     const TvPair* ps = a.pairs + static_cast<int64_t>(n * K + kk) * C;
-    for (int cc = lane; cc < C; cc += 64) { x += ps[cc].alpha; y += ps[cc].S; }
+    for (int cc = lane; cc < C; cc += 64) { x += ps[cc].alpha; y += ps[cc].S; z += ps[cc].Sc; }
     x = wave_sum(x);
     y = wave_sum(y);
-    if (lane == 0) { al[wave][kk] = x; S[wave][kk] = y; }
+    z = wave_sum(z);
+    if (lane == 0) { al[wave][kk] = x; S[wave][kk] = y; Sc[wave][kk] = z; }
   }
   if (lane == 0) {
     double g[SPEC_MAX_K_DEV];
@@ -190,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void tv_coef_kernel(TvArgs a) {
       if (a.overlap) a.overlap[static_cast<int64_t>(n) * K + kk] = static_cast<float>(al[wave][kk]);
       const double gk = a.scale * g[kk] * static_cast<double>(a.inv_t);
       a.coef[static_cast<int64_t>(n) * K + kk] =
-          make_float2(static_cast<float>(gk * (1.0 - S[wave][kk])), static_cast<float>(gk * (-S[wave][kk])));
+          make_float2(static_cast<float>(gk * Sc[wave][kk]), static_cast<float>(gk * (-S[wave][kk])));
     }
   }
 }

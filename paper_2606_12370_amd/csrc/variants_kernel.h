@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kThreads) void to_verify_kernel(ToArgs a) {
   double xm = 0.0;
   if (cx >= 0) {
     float tsum[NT];
-    const int ntl = tile_masses<E, NT, S>(rt, al, rt, al, false, excl, cx, V, d.ntiles, s, nn, nn, tsum);
+    const int ntl = tile_masses<E, NT, S>(rt, al, rt, al, false, excl, cx, V, d.ntiles, s, nn, nn, kNoResidual, tsum);
     double W[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) W[j] = (j < ntl) ? static_cast<double>(tsum[j]) : 0.0;
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void to_verify_kernel(ToArgs a) {
   int token = -1;
   if (sh.cstar >= 0)
     token = sample_in_chunk<E, NT, S>(rt, al, rt, al, false, sh.excl_on ? excl : -1, sh.cstar, sh.tin, V, d.ntiles,
-                                      s, nn, nn, redv, red1, sh.smp);
+                                      s, nn, nn, kNoResidual, redv, red1, sh.smp);
   if (tid == 0) a.emitted[static_cast<int64_t>(b) * (K + 1) + n] = token;
 }
 
@@ -275,7 +275,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(SampleArgs a) {
       token = v == 0x7fffffff ? -1 : v;
     } else {
       token = sample_in_chunk<E, NT, S>(row, al, row, al, false, -1, sh.cstar, sh.tin, V, d.ntiles, s, sh.nrm,
-                                        sh.nrm, redv, red1, sh.smp);
+                                        sh.nrm, kNoResidual, redv, red1, sh.smp);
     }
   }
   if (tid == 0) {

@@ -26,10 +26,71 @@
 
 namespace sv {
 
-struct PairStat {  // one chunk of a (target, draft) pair
+struct PairStat {  // one sub-chunk of a (target, draft) pair
   double alpha;    // sum min(p, q)
+  // the row's first rejected step only: with p, q from the row normalisers,
   double Z;        // sum max(0, p - q)
+  double N;        // sum min(0, p - q)
+  double Qg;       // sum of q over the elements with p > q
 };
+
+// The residual max(0, p - q) of the first rejected step, per element, to
+// float32 precision of the residual itself, also where p and q nearly agree
+// (the paper's operating regime: acceptance 0.75-0.99, residual masses down
+// to 1e-3).  d = log2 p - log2 q is formed from the exact logit difference,
+// d = (z_t - z_d) s - c, with c = log2 Z_t - log2 Z_d the difference of the
+// row normalisers in float64 (split into float32 hi + lo); then
+// p - q = sign(d) max(p, q) (1 - 2^-|d|).  The row normalisers come from
+// float32 element sums, so the two rows' normalisations are exact only to
+// about 1e-7: scaling p by rho = sum q / sum p (the sums of the same element
+// values over the whole row) makes both sum to the same total, and the
+// residual becomes max(0, (p - q) - p (1 - rho)).  1 - rho is itself formed
+// from accurate sums, (Z + N) / (alpha + Z) over the row's PairStat totals.
+struct ResidualRef {
+  float ch, cl;  // c = ch + cl
+  float w;       // 1 - rho (0 while the pair pass forms the sums)
+};
+
+__device__ __forceinline__ ResidualRef residual_ref(const RowNorm& t, const RowNorm& d, double w) {
+  const double c = (static_cast<double>(t.M) - static_cast<double>(d.M)) + (log2(t.D) - log2(d.D));
+  ResidualRef r;
+  r.ch = static_cast<float>(c);
+  r.cl = static_cast<float>(c - static_cast<double>(r.ch));
+  r.w = static_cast<float>(w);
+  return r;
+}
+
+// The reference of a mass computation that is not a residual (p itself).
+constexpr ResidualRef kNoResidual = {0.f, 0.f, 0.f};
+
+// Signed p - q of one element and its min(p, q) and max(p, q), from the
+// logits: lp, lq the float32 log2 probabilities, d the accurate log ratio
+// (which also decides which side is larger).
+struct ElemPQ {
+  float diff;  // p - q
+  float mn;    // min(p, q)
+  float mx;    // max(p, q)
+};
+__device__ __forceinline__ ElemPQ elem_pq(float zt, float zd, float s, const RowNorm& t, const RowNorm& d,
+                                          const ResidualRef& rr) {
+  const float lp = fmaf(zt, s, -t.M) - t.L;
+  const float lq = fmaf(zd, s, -d.M) - d.L;
+  const float dd = fmaf(zt - zd, s, -rr.ch) - rr.cl;
+  const bool pbig = dd > 0.f;
+  ElemPQ e;
+  e.mx = __builtin_amdgcn_exp2f(pbig ? lp : lq);
+  e.mn = __builtin_amdgcn_exp2f(pbig ? lq : lp);
+  const float g = e.mx * one_minus_exp2_neg(fabsf(dd));
+  e.diff = e.mx > 0.f ? copysignf(g, dd) : 0.f;
+  return e;
+}
+
+// The residual mass of one element with the normalisation correction.
+__device__ __forceinline__ float residual_mass(float zt, float zd, float s, const RowNorm& t, const RowNorm& d,
+                                               const ResidualRef& rr) {
+  const ElemPQ e = elem_pq(zt, zd, s, t, d, rr);
+  return e.diff > 0.f ? fmaxf(e.diff - e.mx * rr.w, 0.f) : 0.f;
+}
 
 struct VerifyArgs {
   RowsDesc rows;   // target rows: tper = K+1; draft rows: dper = K
@@ -172,8 +233,8 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
   if (lane == 0) a.decision[b] = n;
 }
 
-// Pass 2 over one chunk of a (target, draft) pair: overlap, and the residual
-// mass when this is the row's first rejected step.
+// Overlaps over one chunk of a (target, draft) pair, one workgroup per chunk
+// (Gumbel-max verification, whose token needs no residual mass).
 template <class E, int NT, int S>
 __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
@@ -185,9 +246,7 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
     const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
     const int b = u / a.K, i = u % a.K;
     const int n = a.decision[b];
-    if (n < 0) continue;  // data error: finish ignores this row's partials
-    const bool need_z = a.want_z && i == n;
-    if (!need_z && a.overlap == nullptr) continue;  // no overlap requested: only the residual step is read again
+    if (n < 0) continue;  // data error: the finish ignores this row's partials
     const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
     int bb;
     bool al_t, al_d;
@@ -197,35 +256,23 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
     const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, d.ntiles - tile0);
-    float al = 0.f, zr = 0.f;
+    float al = 0.f;
 #pragma unroll
     for (int j0 = 0; j0 < NT; j0 += S) {
       if (j0 >= nt_tiles) break;
       float xt[S][EPV], xd[S][EPV];
       load_tiles<E, S>(rt, tile0 + j0, d.V, al_t, xt);
       load_tiles<E, S>(rd, tile0 + j0, d.V, al_d, xd);
-      if (need_z) {
 #pragma unroll
-        for (int j = 0; j < S; ++j)
+      for (int j = 0; j < S; ++j)
 #pragma unroll
-          for (int k = 0; k < EPV; ++k) {
-            const float p = prob(xt[j][k], s, nt.M, nt.invD);
-            const float mn = fminf(p, prob(xd[j][k], s, nd.M, nd.invD));
-            al += mn;
-            zr += p - mn;
-          }
-      } else {
-#pragma unroll
-        for (int j = 0; j < S; ++j)
-#pragma unroll
-          for (int k = 0; k < EPV; ++k) al += min_prob(xt[j][k], xd[j][k], s, nt, nd);
-      }
+        for (int k = 0; k < EPV; ++k) al += min_prob(xt[j][k], xd[j][k], s, nt, nd);
     }
-    double v[4] = {static_cast<double>(al), static_cast<double>(zr), 0.0, 0.0};
+    double v[4] = {static_cast<double>(al), 0.0, 0.0, 0.0};
     wg_sum<4>(v, red);
     if (threadIdx.x == 0) {
       PairStat o;
-      o.alpha = v[0]; o.Z = v[1];
+      o.alpha = v[0]; o.Z = 0.0; o.N = 0.0; o.Qg = 0.0;
       a.pairs[t] = o;
     }
   }
@@ -260,8 +307,9 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
     const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
     const float s = scale_of(temperature_of(d, b));
     const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
+    const ResidualRef rr = residual_ref(nt, nd, 0.0);
     const int e0 = j * WV * 64 * EPV;
-    float al = 0.f, zr = 0.f;
+    float al = 0.f, zp = 0.f, zn = 0.f, qg = 0.f;
 #pragma unroll
     for (int st = 0; st < WV / S; ++st) {
       const int es = e0 + st * S * 64 * EPV;
@@ -274,10 +322,11 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
         for (int q = 0; q < S; ++q)
 #pragma unroll
           for (int k = 0; k < EPV; ++k) {
-            const float p = prob(xt[q][k], s, nt.M, nt.invD);
-            const float mn = fminf(p, prob(xd[q][k], s, nd.M, nd.invD));
-            al += mn;
-            zr += p - mn;
+            const ElemPQ e = elem_pq(xt[q][k], xd[q][k], s, nt, nd, rr);
+            al += e.mn;
+            zp += fmaxf(e.diff, 0.f);
+            zn += fminf(e.diff, 0.f);
+            qg += e.diff > 0.f ? e.mn : 0.f;
           }
       } else {
 #pragma unroll
@@ -288,7 +337,9 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
     }
     PairStat o;
     o.alpha = wave_sum(static_cast<double>(al));
-    o.Z = need_z ? wave_sum(static_cast<double>(zr)) : 0.0;
+    o.Z = need_z ? wave_sum(static_cast<double>(zp)) : 0.0;
+    o.N = need_z ? wave_sum(static_cast<double>(zn)) : 0.0;
+    o.Qg = need_z ? wave_sum(static_cast<double>(qg)) : 0.0;
     if (lane == 0) a.pairs[g] = o;
   }
 }
@@ -297,13 +348,13 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
 // element `excl` (-1: none) has mass 0.
 template <class E>
 __device__ __forceinline__ void vector_masses(const typename E::raw* rt, const typename E::raw* rd, bool residual,
-                                              int excl, int v0, int V, float s, float Mt, float it, float Md,
-                                              float id, float (&r)[E::EPV]) {
+                                              int excl, int v0, int V, float s, const RowNorm& nt,
+                                              const RowNorm& nd, const ResidualRef& rr, float (&r)[E::EPV]) {
 #pragma unroll
   for (int k = 0; k < E::EPV; ++k) {
     if (v0 + k < V && v0 + k != excl) {
-      const float p = prob(E::one(rt + v0 + k), s, Mt, it);
-      r[k] = residual ? p - fminf(p, prob(E::one(rd + v0 + k), s, Md, id)) : p;
+      const float zt = E::one(rt + v0 + k);
+      r[k] = residual ? residual_mass(zt, E::one(rd + v0 + k), s, nt, nd, rr) : prob(zt, s, nt.M, nt.invD);
     } else {
       r[k] = 0.f;
     }
@@ -358,8 +409,8 @@ struct SampleShared {
 template <class E, int NT, int S>
 __device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
                                            bool al_d, bool residual, int excl, int c, int V, int ntiles, float s,
-                                           const RowNorm& nt, const RowNorm& nd, float (&tsum)[NT],
-                                           float (*keep)[S][E::EPV] = nullptr) {
+                                           const RowNorm& nt, const RowNorm& nd, const ResidualRef& rr,
+                                           float (&tsum)[NT], float (*keep)[S][E::EPV] = nullptr) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   const int tile0 = c * NT;
@@ -380,8 +431,7 @@ __device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t,
     for (int j = 0; j < S; ++j)
 #pragma unroll
       for (int k = 0; k < EPV; ++k) {
-        const float p = prob(xt[j][k], s, nt.M, nt.invD);
-        float m = residual ? p - fminf(p, prob(xd[j][k], s, nd.M, nd.invD)) : p;
+        float m = residual ? residual_mass(xt[j][k], xd[j][k], s, nt, nd, rr) : prob(xt[j][k], s, nt.M, nt.invD);
         if (j0 + j == ex_tile && k == ex_k) m = 0.f;
         tsum[j0 + j] += m;
         if (keep) (*keep)[j][k] = m;
@@ -397,8 +447,8 @@ __device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t,
 template <class E, int NT, int S>
 __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typename E::raw* rd, bool al_d,
                                bool residual, int excl, int cstar, double tin, int V, int ntiles, float s,
-                               const RowNorm& nt, const RowNorm& nd, RedLds<NT>& redv, RedLds<1>& red1,
-                               SampleShared& sh) {
+                               const RowNorm& nt, const RowNorm& nd, const ResidualRef& rr, RedLds<NT>& redv,
+                               RedLds<1>& red1, SampleShared& sh) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   const int tid = threadIdx.x;
@@ -406,8 +456,8 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
   float tsum[NT];
   // a chunk of one load step keeps its element masses for the final scan
   float keep[S][EPV];
-  const int nt_tiles = tile_masses<E, NT, S>(rt, al_t, rd, al_d, residual, excl, cstar, V, ntiles, s, nt, nd, tsum,
-                                             NT == S ? &keep : nullptr);
+  const int nt_tiles = tile_masses<E, NT, S>(rt, al_t, rd, al_d, residual, excl, cstar, V, ntiles, s, nt, nd, rr,
+                                             tsum, NT == S ? &keep : nullptr);
   double W[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) W[j] = (j < nt_tiles) ? static_cast<double>(tsum[j]) : 0.0;
@@ -470,7 +520,7 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
 #pragma unroll
             for (int k = 0; k < EPV; ++k) r[k] = keep[j][k];
       } else {
-        vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt.M, nt.invD, nd.M, nd.invD, r);
+        vector_masses<E>(rt, rd, residual, excl, v0, V, s, nt, nd, rr, r);
       }
       const double tl = t_in - excl_sum;
       float cumf = 0.f;
@@ -492,15 +542,22 @@ __device__ int sample_in_chunk(const typename E::raw* rt, bool al_t, const typen
 struct FinishShared {
   double alpha[SPEC_MAX_K_DEV];
   RowNorm nrm[2 * SPEC_MAX_K_DEV + 1];  // target rows 0..K, then draft rows 0..K-1
-  double tin;
+  double tin, w;
   int cstar, residual;
   SampleShared smp;
 };
 
+// The residual mass of one sub-chunk at the rejected step, with the
+// normalisation correction w = 1 - rho: the elements with p > q lose p w
+// each, sum_{p > q} p = Qg + Z.
+__device__ __forceinline__ double corrected_mass(double z, double qg, double w) {
+  return fmax(z - (qg + z) * w, 0.0);
+}
+
 // One workgroup per batch row: overlaps and the resampled / bonus token.
 // Everything the row can need except the chosen sub-chunk is requested before
 // its accept length is known, in one round trip: the overlap partials, the
-// residual masses of every step and the bonus row's statistics for the first
+// residual sums of every step and the bonus row's statistics for the first
 // 64 sub-chunks, and the normalisers of the 2K+1 rows; the uniform of every
 // possible emitting step is drawn meanwhile, one lane per step.  Then only the
 // chosen sub-chunk is read.
@@ -522,10 +579,10 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + wave) * C;
     for (int cc = lane; cc < C; cc += 64) al += ps[cc].alpha;
   }
-  // wave 0, lane cc < 64: sub-chunk cc's residual mass of every step and the
+  // wave 0, lane cc < 64: sub-chunk cc's residual sums of every step and the
   // bonus row's statistics; lane j <= K: target row j's normaliser and the
   // uniform u' of step j
-  double zpre[SPEC_MAX_K_DEV];
+  PairStat ppre[SPEC_MAX_K_DEV];
   RowStat spre;
   spre.m = -INFINITY; spre.pad = 0.f; spre.D = 0.0;
   float nM = 0.f;
@@ -533,8 +590,8 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   if (wave == 0) {
 #pragma unroll
     for (int i = 0; i < SPEC_MAX_K_DEV; ++i) {
-      zpre[i] = 0.0;
-      if (i < K && lane < C) zpre[i] = a.pairs[static_cast<int64_t>(b * K + i) * C + lane].Z;
+      ppre[i].alpha = 0.0; ppre[i].Z = 0.0; ppre[i].N = 0.0; ppre[i].Qg = 0.0;
+      if (i < K && lane < C) ppre[i] = a.pairs[static_cast<int64_t>(b * K + i) * C + lane];
     }
     if (lane < C) spre = a.stats[static_cast<int64_t>(target_row(a, b, K)) * C + lane];
     if (lane <= K) {
@@ -564,13 +621,28 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   // the sub-chunk holding the sampling target (wave 0)
   if (wave == 0) {
     const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + (n < K ? n : 0)) * C;
-    double z0 = 0.0;
+    PairStat p0;
+    p0.alpha = 0.0; p0.Z = 0.0; p0.N = 0.0; p0.Qg = 0.0;
 #pragma unroll
     for (int i = 0; i < SPEC_MAX_K_DEV; ++i)
-      if (i == n) z0 = zpre[i];
-    double zs = 0.0;
+      if (i == n) p0 = ppre[i];
+    // the row's totals at the rejected step, and its normalisation correction
+    double w = 0.0, zs = 0.0;
     if (n < K) {
-      for (int cc = lane; cc < C; cc += 64) zs += cc < 64 ? z0 : ps[cc].Z;
+      double za = 0.0, zn = 0.0, zal = 0.0;
+      for (int cc = lane; cc < C; cc += 64) {
+        const PairStat q = cc < 64 ? p0 : ps[cc];
+        za += q.Z; zn += q.N; zal += q.alpha;
+      }
+      za = wave_sum(za);
+      zn = wave_sum(zn);
+      zal = wave_sum(zal);
+      w = (za + zn) / (zal + za);
+      if (!(w == w)) w = 0.0;
+      for (int cc = lane; cc < C; cc += 64) {
+        const PairStat q = cc < 64 ? p0 : ps[cc];
+        zs += corrected_mass(q.Z, q.Qg, w);
+      }
       zs = wave_sum(zs);
     }
     // residual of the rejected step; p_n itself for the bonus row or an empty residual
@@ -583,16 +655,18 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     auto stat_mass1 = [&](const RowStat& sc) -> double {
       return sc.m == -INFINITY ? 0.0 : sc.D * static_cast<double>(__builtin_amdgcn_exp2f(sc.m - nnM)) / nnD;
     };
-    const double m0 = lane < C ? (residual ? z0 : stat_mass1(n == K ? spre : st[lane])) : 0.0;
+    const double m0 =
+        lane < C ? (residual ? corrected_mass(p0.Z, p0.Qg, w) : stat_mass1(n == K ? spre : st[lane])) : 0.0;
     double tin;
     const int cstar = select_chunk(C, __shfl(uq, n, 64), [&](int cc) -> double {
       if (cc < 64) return m0;
-      return residual ? ps[cc].Z : stat_mass1(st[cc]);
+      return residual ? corrected_mass(ps[cc].Z, ps[cc].Qg, w) : stat_mass1(st[cc]);
     }, &tin);
     if (lane == 0) {
       sh.cstar = cstar;
       sh.tin = tin;
       sh.residual = residual ? 1 : 0;
+      sh.w = w;
     }
   }
   __syncthreads();
@@ -605,8 +679,9 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     const raw* rd = row_of<E>(d, draft_row(a, b, n < K ? n : 0), &bb, &al_d);
     const RowNorm nt = sh.nrm[n];
     const RowNorm nd = sh.nrm[K + 1 + (n < K ? n : 0)];
+    const ResidualRef rr = residual_ref(nt, nd, sh.w);
     token = sample_in_chunk<E, NT, S>(rt, al_t, rd, al_d, sh.residual != 0, -1, sh.cstar, sh.tin, V, d.ntiles, s, nt,
-                                      nd, redv, red1, sh.smp);
+                                      nd, rr, redv, red1, sh.smp);
   }
 
   // the overlaps and emitted[n] have this single writer

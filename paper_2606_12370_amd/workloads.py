@@ -20,6 +20,11 @@ against 4 target positions, K = 1..3.  Recipes (all per batch row b):
   draft ids: x[b, i] ~ softmax(stored draft[b, i, :] / T_b), drawn with the
       Gumbel-max trick from the stored (rounded) logits; for target-only
       verification the greedy ids argmax_v draft[b, i, v] instead;
+  near-equal verify ("near"): the rollout recipe with draft noise
+      sigma_b ~ U[0.01, 0.1] and T_b ~ U[0.6, 1.2], so that the per-step
+      acceptance sum_v min(p, q) lies near 0.9-0.99 and the residual mass
+      1 - alpha near 1e-2 - 1e-3 (the paper's operating regime, Sec. 6
+      Tables 1-2: acceptance 0.75-0.99);
   TV loss: s_n ~ U[1, 8], target ~ N(0, s_n^2), draft = target + N(0, 1).
 
 Two backends: ``numpy`` (host, ``numpy.random.default_rng``) for the small
@@ -101,6 +106,9 @@ def verify_inputs_numpy(B, K, V, dtype, gen, seed, shared_target=False, q_equals
     elif gen in ("rollout", "rollout_t"):
         s = rng.uniform(1.0, 8.0, size=Bg).astype(np.float32)
         sig = rng.uniform(0.2, 1.5, size=Bg).astype(np.float32)
+    elif gen == "near":
+        s = rng.uniform(1.0, 8.0, size=Bg).astype(np.float32)
+        sig = rng.uniform(0.01, 0.1, size=Bg).astype(np.float32)
     else:
         raise ValueError(gen)
     tgt32 = rng.standard_normal((Bg, K + 1, V), dtype=np.float32) * s[:, None, None]
@@ -111,7 +119,7 @@ def verify_inputs_numpy(B, K, V, dtype, gen, seed, shared_target=False, q_equals
     else:
         noise = rng.standard_normal((Bg, K, V), dtype=np.float32) * sig[:, None, None]
         drf = _store(to_float64(tgt[:, :K], dtype).astype(np.float32) + noise, dtype)
-    if gen == "rollout_t":
+    if gen in ("rollout_t", "near"):
         T = rng.uniform(0.6, 1.2, size=Bg).astype(np.float32)
     else:
         T = np.ones(Bg, np.float32)
@@ -204,8 +212,9 @@ def verify_inputs_torch(B, K, V, dtype, gen, seed, device="cuda"):
     g.manual_seed(seed)
     td = _torch_dtype(dtype)
     s = torch.empty(B, device=device).uniform_(1.0, 8.0, generator=g)
-    sig = torch.empty(B, device=device).uniform_(0.2, 1.5, generator=g)
-    if gen == "rollout_t":
+    lo, hi = (0.01, 0.1) if gen == "near" else (0.2, 1.5)
+    sig = torch.empty(B, device=device).uniform_(lo, hi, generator=g)
+    if gen in ("rollout_t", "near"):
         T = torch.empty(B, device=device).uniform_(0.6, 1.2, generator=g)
     else:
         T = torch.ones(B, device=device)

@@ -123,17 +123,15 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
     maxima and log-normalisers makes a handful of roundings of 2^-24 relative
     to the size of those terms (tie_condition), plus the normalisers' own
     summation error (TIE_ABS).  So
-    such elements are not compared.  The same bound is the relative error of
-    each q_j, and S = sum 1[q <= p] q carries both the tied elements and
-    those errors, so the rest of the row may differ from the oracle by one
-    common shift of S: grad_j - ref_j = -w_j dS with w = g q / T and |dS| <=
-    sum_{ties} q + sum q_j qerr_j.  That freedom matters where one token
-    holds nearly all the mass: S is then 1 - O(q of the rest), the row's
-    gradient is the small difference w (1 - S), and a float32 S (one ulp of
-    1 is 1.2e-7) moves it by far more than the dtype tolerance of its size.
-    dS is fitted by least squares over the untied elements and clipped to
-    that slack; what remains beyond each element's own q error, |ref_j|
-    qerr_j, must be within the tolerance times the row's largest gradient."""
+    such elements are not compared.  S = sum 1[q <= p] q moves by the mass of
+    the tied elements that land on the other side, so the rest of the row may
+    differ from the oracle by one common shift of S: grad_j - ref_j = -w_j dS
+    with w = g q / T and |dS| <= sum_{ties} q.  dS is fitted by least squares
+    over the untied elements and clipped to that slack; what remains beyond
+    each element's own q error, |ref_j| qerr_j, must be within the tolerance
+    times the row's largest gradient.  (The kernel sums S and its complement
+    1 - S separately, each from the same float32 q values, so no float32
+    rounding of S near 1 enters the gradient.)"""
     tol = TOL[dtype]
     ov = ov_g.cpu().numpy().astype(np.float64)
     if positions is not None:
@@ -164,7 +162,7 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
         d = np.where(untied, g - gr, 0.0)
         w = ref["grad_weight"]
         q = ref["q"]
-        s_slack = np.where(tie, q, 0.0).sum(axis=-1) + (q * qerr).sum(axis=-1)
+        s_slack = np.where(tie, q, 0.0).sum(axis=-1)
         num = (d * w).sum(axis=-1)
         den = np.where(untied, w * w, 0.0).sum(axis=-1)
         with np.errstate(divide="ignore", invalid="ignore"):

@@ -196,9 +196,9 @@ def test_without_overlap_output(dtype):
     compare_verify(lean, ref, dtype)
 
 
-def _sampled(cfg_name, nsample, seed=0):
+def _sampled(cfg_name, nsample, seed=0, gen=None):
     cfg = W.CONFIGS[cfg_name]
-    d = W.verify_inputs_torch(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], cfg["gen"], cfg["seed"])
+    d = W.verify_inputs_torch(cfg["B"], cfg["K"], cfg["V"], cfg["dtype"], gen or cfg["gen"], cfg["seed"])
     out = binding.verify(d["target"], d["draft"], d["ids"], d["temperature"], seed, 0, want_debug=True)
     torch.cuda.synchronize()
     rng = np.random.default_rng(cfg["seed"])
@@ -228,6 +228,14 @@ def test_benchmark_batch_sampled_rows():
 
 def test_large_batch_sampled_rows():
     _sampled("large_bf16_b1024_k3_v262144", 8, seed=7)
+
+
+def test_benchmark_shape_near_equal_sampled_rows():
+    """The B=256, K=3, V=151936 bf16 shape with the near-equal draft recipe
+    (draft noise 0.01-0.1, acceptance about 0.9-0.99): 32 sampled rows exact
+    or boundary draws."""
+    rep = _sampled("verify_bf16_b256_k3_v151936", 32, seed=11, gen="near")
+    print("near-equal boundary rows", rep["boundary_rows"])
 
 
 def test_one_workspace_across_shapes_and_kernels():
