@@ -30,12 +30,14 @@
  *    next.  Calls that share a workspace must not run concurrently (enqueue
  *    them on one stream).
  *  - Each call is a short fixed sequence of kernel launches on `stream`
- *    (spec_verify: 4, spec_tv_loss_fwd_bwd: 5, or 6 with a gradient,
- *    spec_verify_target_only: 2, spec_sample: 2, spec_diagnostics: 4,
- *    spec_verify_gumbel: 5, or 4 without overlaps, spec_sample_gumbel: 2,
- *    spec_kl_loss_fwd_bwd: 5, or 6 for reverse KL with a gradient); no
- *    launch waits on another workgroup, so any number of resident
- *    workgroups is enough.
+ *    (spec_verify: 4, or 3 on its single-read path; spec_tv_loss_fwd_bwd:
+ *    5, or 6 with a gradient; spec_verify_target_only: 2, spec_sample: 2,
+ *    spec_diagnostics: 4, spec_verify_gumbel: 5, or 4 without overlaps,
+ *    spec_sample_gumbel: 2, spec_kl_loss_fwd_bwd: 5, or 6 for reverse KL
+ *    with a gradient).  Only the single-read path of spec_verify has
+ *    workgroups that wait for other workgroups of the same launch; it is a
+ *    cooperative launch (all its workgroups resident at once) and every wait
+ *    is bounded.  No other launch waits on another workgroup.
  *  - Entry points are thread-safe; each call is independent.
  *  - Logits are bfloat16 (raw 16-bit patterns) or float32.  Arithmetic is
  *    float32 per element with float64 accumulation across vectors, threads
@@ -103,9 +105,8 @@ size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
  *                (which must then be finite and > 0)
  * accept_len     [B] int32 out
  * emitted_ids    [B, K+1] int32 out, contiguous
- * overlap        [B, K] float32 out, or NULL: then only the pair at the first
- *                rejected step is read a second time (about 1.15 reads of the
- *                logits instead of 1.9)
+ * overlap        [B, K] float32 out, or NULL (then the overlaps of the
+ *                accepted steps are not formed)
  * p_at_draft, q_at_draft  [B, K] float32 out: p_i(x_i), q_i(x_i) (may be NULL)
  * logz_target    [B, K+1] float32 out: natural-log partition function of z/T (may be NULL)
  * logz_draft     [B, K]   float32 out (may be NULL)
@@ -116,6 +117,23 @@ size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
  * fail the call: that row gets accept_len = -1, emitted = -1 and NaN in every
  * float output.  -inf logits are legal (probability 0).
  * Limits: 1 <= K <= SPEC_MAX_K, 1 <= V <= SPEC_MAX_V, 1 <= B, B*(K+1) < 2^31.
+ *
+ * Two launch paths compute the same method (spec_verify takes the chain;
+ * spec_verify_ex selects either):
+ *  - single read (K <= 4, 16-byte aligned rows, at most 64 sub-chunks of
+ *    8192 bf16 / 4096 fp32 elements per row): each batch row is spread over a
+ *    group of workgroups, one per sub-chunk, which keep their sub-chunk of all
+ *    2K+1 rows in registers, exchange the sub-chunk statistics through the
+ *    workspace and take the overlaps and residual sums without reading the
+ *    logits again; then one launch per batch row picks the resampled token
+ *    (reading one sub-chunk of one row pair again);
+ *  - chain (every other shape): statistics, decision, a second read of the
+ *    draft pairs (only the rejected pair without `overlap`), then the same
+ *    per-row launch.
+ * Tokens are bit-exact functions of the inputs, seed and offset for either
+ * path and any number of groups; the two paths' float32 normaliser sums differ
+ * in summation order, which can move a decision only where its uniform lies
+ * within float32 rounding of a decision boundary.
  */
 spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
                         const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
@@ -127,6 +145,36 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
                         float* overlap, float* p_at_draft, float* q_at_draft,
                         float* logz_target, float* logz_draft,
                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Launch controls for spec_verify_ex (tests, benchmarks and tuning). */
+typedef enum {
+  SPEC_PATH_AUTO = 0,        /* the library's choice (the chain on MI355X)        */
+  SPEC_PATH_CHAIN = 1,       /* always the four-launch chain                        */
+  SPEC_PATH_SINGLE_READ = 2  /* single read; SPEC_EUNSUPPORTED where it does not qualify */
+} spec_path;
+typedef struct {
+  int path;   /* spec_path */
+  int groups; /* single read: number of workgroup groups (0 = chosen by the library;
+                 more than the device holds at once selects the chain, or
+                 SPEC_EUNSUPPORTED with SPEC_PATH_SINGLE_READ) */
+} spec_launch;
+
+/*
+ * spec_verify_ex — spec_verify with explicit launch controls (NULL = the
+ * defaults of spec_verify).  Same arguments, outputs and errors as
+ * spec_verify; SPEC_EINVAL for an unknown path or negative group count.
+ */
+spec_status spec_verify_ex(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                           const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                           spec_dtype dtype, int B, int K, int V,
+                           const int32_t* draft_ids,
+                           const float* temperature, float temperature_scalar,
+                           uint64_t seed, uint64_t offset,
+                           int32_t* accept_len, int32_t* emitted_ids,
+                           float* overlap, float* p_at_draft, float* q_at_draft,
+                           float* logz_target, float* logz_draft,
+                           void* workspace, size_t workspace_bytes, void* stream,
+                           const spec_launch* launch);
 
 /* Bytes of workspace spec_tv_loss_fwd_bwd needs (0 on invalid sizes).  It
  * includes about one bit per logit (N*K*ceil(V/16384)*2048 bytes, about 1/32

@@ -43,6 +43,16 @@ TO_ARGTYPES = [_P, _I64, _I64, _I, _I, _I, _I, _P, _P, _F, _U64, _U64, _P, _P, _
 SAMPLE_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _P, _SZ, _P]
 SAMPLE_GUMBEL_ARGTYPES = [_P, _I64, _I, _I, _I, _P, _F, _U64, _U64, _P, _P, _SZ, _P]
 DIAG_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _P, _F, _P, _P, _P, _P, _SZ, _P]
+
+# spec_launch: launch controls of spec_verify_ex
+PATHS = {"auto": 0, "chain": 1, "single_read": 2}
+
+
+class SpecLaunch(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int), ("groups", ctypes.c_int)]
+
+
+VERIFY_EX_ARGTYPES = VERIFY_ARGTYPES + [ctypes.POINTER(SpecLaunch)]
 KL_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _SZ, _P]
 KL_KINDS = {"forward": 0, "ce": 1, "reverse": 2}
 DIAG_COLUMNS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")
@@ -77,6 +87,8 @@ def load_library():
         lib.spec_tv_workspace_size.argtypes = [_I, _I, _I, _I]
         lib.spec_verify.restype = _I
         lib.spec_verify.argtypes = VERIFY_ARGTYPES
+        lib.spec_verify_ex.restype = _I
+        lib.spec_verify_ex.argtypes = VERIFY_EX_ARGTYPES
         lib.spec_tv_loss_fwd_bwd.restype = _I
         lib.spec_tv_loss_fwd_bwd.argtypes = TV_ARGTYPES
         lib.spec_verify_target_only_workspace_size.restype = _SZ
@@ -202,9 +214,11 @@ def _check_ids(ids, B, K):
 
 
 def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offset=0,
-           want_debug=False, want_overlap=True, ws=None, out=None, gumbel=False):
+           want_debug=False, want_overlap=True, ws=None, out=None, gumbel=False, path=None, groups=0):
     """Chain rejection-sampling verification (spec_verify, or with
     gumbel=True spec_verify_gumbel: the emitted token drawn by Gumbel-max).
+    path ("auto", "chain", "single_read") and groups select the launch
+    (spec_verify_ex); by default the library chooses.
 
     target_logits [B, K+1, V], draft_logits [B, K, V] (bf16 or f32, same
     dtype, vocabulary dimension contiguous), draft_ids [B, K] int32,
@@ -247,6 +261,12 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
             out["logz_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
     size_fn = lib.spec_verify_gumbel_workspace_size if gumbel else lib.spec_verify_workspace_size
     fn, name = (lib.spec_verify_gumbel, "spec_verify_gumbel") if gumbel else (lib.spec_verify, "spec_verify")
+    extra = ()
+    if path is not None or groups:
+        if gumbel:
+            raise ValueError("launch controls apply to spec_verify only")
+        fn, name = lib.spec_verify_ex, "spec_verify_ex"
+        extra = (ctypes.byref(SpecLaunch(PATHS[path or "auto"], int(groups))),)
     need = int(size_fn(B, K, V, code))
     if need == 0:
         raise ValueError("unsupported verify shape B=%d K=%d V=%d" % (B, K, V))
@@ -259,7 +279,7 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
         _ptr(out["accept_len"]), _ptr(out["emitted"]), _ptr(out.get("overlap")),
         _ptr(out.get("p_at_draft")), _ptr(out.get("q_at_draft")),
         _ptr(out.get("logz_target")), _ptr(out.get("logz_draft")),
-        _ptr(ws), ws.numel(), _stream(dev))
+        _ptr(ws), ws.numel(), _stream(dev), *extra)
     if st != 0:
         raise SpecError(name, st)
     return out

@@ -3,7 +3,10 @@
 // include/specverify.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <atomic>
 #include <cmath>
+#include <mutex>
 #include <cstddef>
 #include <cstdint>
 #include <type_traits>
@@ -16,6 +19,7 @@
 #include "tv_kernel.h"
 #include "variants_kernel.h"
 #include "verify_kernel.h"
+#include "fused_kernel.h"
 
 namespace {
 
@@ -65,6 +69,12 @@ Geometry geometry(int V, spec_dtype dt) {
 // Sub-chunks of kStep tiles per row (the statistics granularity of multinomial verification).
 int sub_chunks(int V, spec_dtype dt) { return (geometry(V, dt).ntiles + kStep - 1) / kStep; }
 
+// Slices of kSliceTiles tiles per row: the granularity of the single-read
+// verification (one workgroup per slice, two vectors per thread and row).
+constexpr int kSliceTiles = 2;
+static_assert(kSliceTiles == sv::kFusedNV, "a slice is one vector per thread per tile");
+int slices(int V, spec_dtype dt) { return (geometry(V, dt).ntiles + kSliceTiles - 1) / kSliceTiles; }
+
 // Largest vocabulary: element indices are 32-bit and run up to one chunk
 // (16384 elements) past V where a row's last chunk is rounded up.
 constexpr int64_t kMaxV = SPEC_MAX_V;
@@ -96,7 +106,9 @@ struct VerifyLayout {
 };
 VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt, bool gumbel = false) {
   VerifyLayout L;
-  const size_t C = static_cast<size_t>(gumbel ? geometry(V, dt).C : sub_chunks(V, dt));
+  // multinomial verification: room for the per-slice records of the single-read path
+  // (two per sub-chunk of the chain)
+  const size_t C = static_cast<size_t>(gumbel ? geometry(V, dt).C : slices(V, dt));
   const size_t rows = static_cast<size_t>(B) * (2 * K + 1);
   size_t off = 0;
   L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
@@ -196,8 +208,116 @@ void launch_stats_wave(const sv::RowsDesc& d, sv::RowStat* stats, int64_t rows, 
                      stats, nsub);
 }
 
+// ---- single-read verification: launch facts per device ----------------------
+// Resident workgroups per CU of each instantiation of the single-read kernel
+// (dtype x K), the CU count and cooperative-launch support, queried once per
+// device and read-only afterwards.
+constexpr int kFusedMaxK = 4;
+constexpr int kMaxDevices = 64;
+struct FusedFacts {
+  std::atomic<int> ready{0};
+  int cus = 0, coop = 0;
+  int bpc[2][kFusedMaxK + 1] = {};
+};
+FusedFacts g_fused_facts[kMaxDevices];
+std::mutex g_fused_mu;
+
+template <class E, int K>
+const void* fused_kernel_ptr() {
+  return reinterpret_cast<const void*>(&sv::verify_fused_kernel<E, K>);
+}
 template <class E>
-spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s) {
+const void* fused_kernel_for(int K) {
+  switch (K) {
+    case 1: return fused_kernel_ptr<E, 1>();
+    case 2: return fused_kernel_ptr<E, 2>();
+    case 3: return fused_kernel_ptr<E, 3>();
+    case 4: return fused_kernel_ptr<E, 4>();
+  }
+  return nullptr;
+}
+
+const FusedFacts* fused_facts() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  FusedFacts& f = g_fused_facts[dev];
+  if (f.ready.load(std::memory_order_acquire)) return &f;
+  std::lock_guard<std::mutex> lk(g_fused_mu);
+  if (!f.ready.load(std::memory_order_relaxed)) {
+    int cus = 0, coop = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) coop = 0;
+    f.cus = cus;
+    f.coop = coop;
+    for (int k = 1; k <= kFusedMaxK; ++k) {
+      int nb = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fused_kernel_for<BF16>(k), sv::kThreads, 0) != hipSuccess)
+        nb = 0;
+      f.bpc[SPEC_BF16][k] = nb;
+      nb = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fused_kernel_for<F32>(k), sv::kThreads, 0) != hipSuccess)
+        nb = 0;
+      f.bpc[SPEC_F32][k] = nb;
+    }
+    (void)hipGetLastError();
+    f.ready.store(1, std::memory_order_release);
+  }
+  return &f;
+}
+
+// Workgroups of the single-read kernel the device holds at once, or 0 when the
+// shape does not qualify: K <= 4, 16-byte aligned rows, at most 64 sub-chunks
+// per row (the combine is one wave), cooperative launch, and room for at least
+// one group of G = sub-chunks workgroups.
+int fused_capacity(const sv::VerifyArgs& a, spec_dtype dt) {
+  const int G = slices(a.rows.V, dt);
+  if (a.K < 1 || a.K > kFusedMaxK || !a.rows.vec_t || !a.rows.vec_d || G > 64) return 0;
+  const FusedFacts* f = fused_facts();
+  if (!f || !f->coop || f->cus <= 0) return 0;
+  const int cap = f->bpc[dt][a.K] * f->cus;
+  return cap >= G ? cap : 0;
+}
+
+// Number of groups: as many as the device holds at once, at most one per
+// batch row.
+int fused_groups(int B, int G, int cap) { return std::min(cap / G, B); }
+
+template <class E>
+spec_status launch_verify_fused(sv::VerifyArgs a, int groups, hipStream_t s) {
+  // statistics, overlaps and residual sums per slice; the finish inverts the
+  // CDF inside one slice
+  const int G = a.rows.C = slices(a.rows.V, std::is_same<E, BF16>::value ? SPEC_BF16 : SPEC_F32);
+  // the record array starts all ones: a record is complete once it is not
+  const int64_t words = int64_t{a.B} * (2 * a.K + 1) * G * 2;
+  hipLaunchKernelGGL(sv::fill_ones_kernel, dim3(static_cast<unsigned>(std::min<int64_t>((words + 255) / 256, 1024))),
+                     dim3(sv::kThreads), 0, s, reinterpret_cast<uint64_t*>(const_cast<sv::RowStat*>(a.stats)), words);
+  int Gv = G, NG = groups;
+  // about a second of polling before a wait gives up (never reached while the
+  // cooperative launch keeps every workgroup resident)
+  unsigned spin_limit = 1u << 20;
+  void* args[] = {&a, &Gv, &NG, &spin_limit};
+  if (hipLaunchCooperativeKernel(fused_kernel_for<E>(a.K), dim3(static_cast<unsigned>(G * NG)), dim3(sv::kThreads),
+                                 args, 0, s) != hipSuccess)
+    return SPEC_EHIP;
+  hipLaunchKernelGGL((sv::finish_kernel<E, kSliceTiles, kSliceTiles>), dim3(static_cast<unsigned>(a.B)),
+                     dim3(sv::kThreads), 0, s, a);
+  return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
+}
+
+template <class E>
+spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, const spec_launch* lc = nullptr) {
+  const spec_dtype dt = std::is_same<E, BF16>::value ? SPEC_BF16 : SPEC_F32;
+  // the automatic choice is the chain: on MI355X it measures faster than the
+  // single-read path at every benchmarked shape (B = 64..1024, K = 3, bf16)
+  const int path = lc ? lc->path : SPEC_PATH_AUTO;
+  if (path == SPEC_PATH_SINGLE_READ) {
+    const int cap = fused_capacity(a, dt);
+    const int G = slices(a.rows.V, dt);
+    int groups = cap ? fused_groups(a.B, G, cap) : 0;
+    if (lc && lc->groups > 0) groups = (cap && lc->groups <= std::min(cap / G, a.B)) ? lc->groups : 0;
+    if (groups > 0) return launch_verify_fused<E>(a, groups, s);
+    return SPEC_EUNSUPPORTED;
+  }
   // statistics and pair sums per sub-chunk of kStep tiles, one wave per sub-chunk
   launch_stats_wave<E>(a.rows, const_cast<sv::RowStat*>(a.stats), rows, s);
   hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
@@ -433,6 +553,20 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
                         uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
                         float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
                         void* workspace, size_t workspace_bytes, void* stream) {
+  return spec_verify_ex(target_logits, t_stride_b, t_stride_k, draft_logits, d_stride_b, d_stride_k, dtype, B, K, V,
+                        draft_ids, temperature, temperature_scalar, seed, offset, accept_len, emitted_ids, overlap,
+                        p_at_draft, q_at_draft, logz_target, logz_draft, workspace, workspace_bytes, stream, nullptr);
+}
+
+spec_status spec_verify_ex(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                           const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                           spec_dtype dtype, int B, int K, int V, const int32_t* draft_ids,
+                           const float* temperature, float temperature_scalar, uint64_t seed,
+                           uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
+                           float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
+                           void* workspace, size_t workspace_bytes, void* stream, const spec_launch* launch) {
+  if (launch && (launch->path < SPEC_PATH_AUTO || launch->path > SPEC_PATH_SINGLE_READ || launch->groups < 0))
+    return SPEC_EINVAL;
   sv::VerifyArgs a;
   sv::GumbelBest* gb;
   const spec_status st = prepare_verify(target_logits, t_stride_b, t_stride_k, draft_logits, d_stride_b, d_stride_k,
@@ -442,7 +576,7 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
   if (st != SPEC_OK) return st;
   const int64_t rows = int64_t{B} * (2 * K + 1);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return dtype == SPEC_BF16 ? launch_verify<BF16>(a, rows, s) : launch_verify<F32>(a, rows, s);
+  return dtype == SPEC_BF16 ? launch_verify<BF16>(a, rows, s, launch) : launch_verify<F32>(a, rows, s, launch);
 }
 
 size_t spec_verify_gumbel_workspace_size(int B, int K, int V, spec_dtype dtype) {

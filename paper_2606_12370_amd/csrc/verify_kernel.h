@@ -146,10 +146,12 @@ __device__ __forceinline__ DraftGather gather_draft(const VerifyArgs& a, int b, 
 // for batch row b whose 2K+1 row normalisers are in sh.nrm, by one wave: lane
 // i < K tests step i (float64, u q(x) < p(x), no division), two ballots give
 // the row's error flag and its first rejection, lane j <= K writes the
-// outputs of position j.  Returns the accept length n, or -1 for a row with a
-// data error (then every output of the row has been written).
+// outputs of position j (only with `write`: several workgroups may take the
+// same decision, one of them writes it).  Returns the accept length n, or -1
+// for a row with a data error (then every output of the row has been written).
 template <class E>
-__device__ int decide_wave(const VerifyArgs& a, int b, const DecideShared& sh, const DraftGather& gx) {
+__device__ int decide_wave(const VerifyArgs& a, int b, const DecideShared& sh, const DraftGather& gx,
+                           bool write = true) {
   const RowsDesc& d = a.rows;
   const int K = a.K, V = d.V;
   const int lane = threadIdx.x & 63;
@@ -173,6 +175,7 @@ __device__ int decide_wave(const VerifyArgs& a, int b, const DecideShared& sh, c
   const bool err = !t_ok || errm != 0;
   // the first rejection ends the chain
   const int n = err ? -1 : (rejm ? __ffsll(static_cast<long long>(rejm)) - 1 : K);
+  if (!write) return n;
   if (lane == 0) a.accept_len[b] = n;
   // the per-position outputs, one lane each (the float64 log2 of the normalisers in parallel)
   if (lane <= K) {

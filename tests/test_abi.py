@@ -41,7 +41,7 @@ def test_exports_every_declared_function(lib):
                            "spec_diagnostics_workspace_size", "spec_diagnostics",
                            "spec_verify_gumbel_workspace_size", "spec_verify_gumbel",
                            "spec_sample_gumbel_workspace_size", "spec_sample_gumbel",
-                           "spec_kl_workspace_size", "spec_kl_loss_fwd_bwd"}
+                           "spec_kl_workspace_size", "spec_kl_loss_fwd_bwd", "spec_verify_ex"}
     for name in protos:
         assert hasattr(lib, name), name
 
@@ -57,6 +57,8 @@ def test_ctypes_prototypes_match_header():
     assert protos["spec_verify_gumbel"] == protos["spec_verify"]
     assert len(protos["spec_sample_gumbel"]) == len(binding.SAMPLE_GUMBEL_ARGTYPES)
     assert len(protos["spec_kl_loss_fwd_bwd"]) == len(binding.KL_ARGTYPES)
+    assert len(protos["spec_verify_ex"]) == len(binding.VERIFY_EX_ARGTYPES)
+    assert protos["spec_verify_ex"][:-1] == protos["spec_verify"]
 
 
 def test_diag_columns_match_header():
@@ -162,6 +164,30 @@ def call_verify(lib, **kw):
 ])
 def test_verify_argument_errors(lib, kw, status):
     assert call_verify(lib, **kw) == status
+
+
+def call_verify_ex(lib, path, groups, **kw):
+    args = dict(t=FAKE, tsb=400, tsk=100, d=FAKE, dsb=300, dsk=100, dtype=1, B=4, K=3, V=100, ids=FAKE,
+                temp=None, temp_s=1.0, seed=0, off=0, acc=FAKE, em=FAKE, ov=None, p=None, q=None,
+                lzt=None, lzd=None, ws=FAKE, wsb=1 << 30, stream=None)
+    args.update(kw)
+    lc = binding.SpecLaunch(path, groups)
+    return lib.spec_verify_ex(*[args[k] for k in ("t", "tsb", "tsk", "d", "dsb", "dsk", "dtype", "B", "K", "V", "ids",
+                                                  "temp", "temp_s", "seed", "off", "acc", "em", "ov", "p", "q", "lzt",
+                                                  "lzd", "ws", "wsb", "stream")], ctypes.byref(lc))
+
+
+@pytest.mark.parametrize("path,groups,kw,status", [
+    (3, 0, {}, 1),
+    (-1, 0, {}, 1),
+    (0, -2, {}, 1),
+    (2, 0, dict(K=9), 2),
+    (1, 0, dict(B=0), 1),
+    (2, 4, dict(ws=None), 4),
+    (0, 0, dict(temp_s=0.0), 1),
+])
+def test_verify_ex_argument_errors(lib, path, groups, kw, status):
+    assert call_verify_ex(lib, path, groups, **kw) == status
 
 
 def call_tv(lib, **kw):

@@ -255,3 +255,49 @@ def test_one_workspace_across_shapes_and_kernels():
         ref = oracle.verify_ref(W.to_float64(d["target"], dt), W.to_float64(d["draft"], dt), d["ids"],
                                 d["temperature"].astype(np.float64), 3, 0)
         compare_verify(out, ref, dt)
+
+
+@pytest.mark.parametrize("dtype,B,K,V", [(W.BF16, 37, 3, 151936), (W.F32, 9, 2, 50000), (W.BF16, 5, 4, 20000),
+                                         (W.BF16, 13, 1, 8200)])
+def test_launch_shape_independence(dtype, B, K, V):
+    """Every draw depends only on (seed, row, step, offset): the single-read
+    path gives bit-identical accept lengths, tokens and overlaps for any
+    number of workgroup groups, and both paths (single read, chain) match the
+    oracle row by row."""
+    d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 90 + B)
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    ref = oracle.verify_ref(W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype), d["ids"],
+                            d["temperature"].astype(np.float64), 3, 5)
+    base = binding.verify(tgt, drf, ids, T, 3, 5, want_debug=True, path="single_read")
+    torch.cuda.synchronize()
+    compare_verify(base, ref, dtype)
+    for groups in (1, 2, 3, 7):
+        if groups > B:
+            continue
+        out = binding.verify(tgt, drf, ids, T, 3, 5, want_debug=True, path="single_read", groups=groups)
+        torch.cuda.synchronize()
+        for key in base:
+            assert torch.equal(out[key], base[key]), (groups, key)
+    chain = binding.verify(tgt, drf, ids, T, 3, 5, want_debug=True, path="chain")
+    torch.cuda.synchronize()
+    rep = compare_verify(chain, ref, dtype)
+    same = bool(torch.equal(chain["accept_len"], base["accept_len"]) and torch.equal(chain["emitted"], base["emitted"]))
+    print(dtype, B, K, V, "chain and single read give the same tokens:", same, rep)
+
+
+def test_single_read_unsupported_shapes_fall_back_or_refuse():
+    """K = 8 (beyond the single-read path): the automatic launch takes the
+    chain and matches the oracle; asking for the single-read path refuses."""
+    d = W.verify_inputs_numpy(3, 8, 3000, W.BF16, "rollout_t", 17)
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    out = binding.verify(tgt, drf, ids, T, 1, 2)
+    torch.cuda.synchronize()
+    ref = oracle.verify_ref(W.to_float64(d["target"], W.BF16), W.to_float64(d["draft"], W.BF16), d["ids"],
+                            d["temperature"].astype(np.float64), 1, 2)
+    compare_verify(out, ref, W.BF16)
+    with pytest.raises(binding.SpecError):
+        binding.verify(tgt, drf, ids, T, 1, 2, path="single_read")
