@@ -73,6 +73,9 @@ struct KlNorm {
 struct KlPart {  // one chunk of a (position, step) pair
   double se, sf, w;
   double sfx, wx, wm;  // reverse KL: sum f, sum f d over the non-largest draft elements; sum f d over the largest
+  double x;            // forward KL / CE: sum over the other elements of 2^(b) - 2^(a) (see kl_pass)
+  int top;             // index of the element holding both rows' largest logit, or -1
+  int pad;
 };
 
 struct KlArgs {
@@ -234,6 +237,11 @@ __global__ __launch_bounds__(kThreads) void kl_norm_kernel(const KlStat* __restr
   }
 }
 
+// ((z_d - z_t) - (zmax_d - zmax_t)) s in float64 (log2 q - log2 p less lam_t - lam_d).
+__device__ __forceinline__ double kl_wdiff(float zt, float zd, double c1, double s) {
+  return ((static_cast<double>(zd) - static_cast<double>(zt)) - c1) * s;
+}
+
 // log2 q - log2 p of one element in float64,
 // ((z_d - z_t) - (zmax_d - zmax_t)) s + (lam_t - lam_d): every logit
 // difference is exact, and at the element holding both rows' largest logit
@@ -275,6 +283,7 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   __shared__ RedLds<6> red;
+  __shared__ RedLds<1> red1;
   const RowsDesc& d = a.rows;
   const int C = d.C, V = d.V, NK = a.N * a.K;
   const bool write_grad = a.grad != nullptr && KIND != kKlReverse;
@@ -291,7 +300,11 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
     float* gr = write_grad ? a.grad + static_cast<int64_t>(u) * V : nullptr;
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
-    double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0;
+    double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0, xs = 0.0;
+    int top = -1;
+    // 2^(z s - zmax s) = e 2^(M - zmax s): the scale of each row's elements against its largest
+    const float kt = static_cast<float>(exp2(static_cast<double>(nt.M) - static_cast<double>(nt.zmax) * dr.s));
+    const float kd = static_cast<float>(exp2(static_cast<double>(nd.M) - static_cast<double>(nd.zmax) * dr.s));
 #pragma unroll
     for (int j0 = 0; j0 < NT; j0 += S) {
       if (j0 >= nt_tiles) break;
@@ -302,14 +315,15 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
       for (int j = 0; j < S; ++j) {
         float gv[EPV];
         // the EPV elements of one vector are summed in float32, vectors in float64
-        float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f;
+        float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f, vx = 0.f;
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
           const float tt = fmaf(xt[j][k], s, -nt.M);
           const float uu = fmaf(xd[j][k], s, -nd.M);
           const float e = __builtin_amdgcn_exp2f(tt);
           const float f = __builtin_amdgcn_exp2f(uu);
-          const float dl = kl_delta(xt[j][k], xd[j][k], dr);
+          const double wd = kl_wdiff(xt[j][k], xd[j][k], dr.c1, dr.s);
+          const float dl = static_cast<float>(wd + dr.lam);
           float term;
           if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
           else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
@@ -329,6 +343,15 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
             const float mx = fmaxf(e * nt.invD, f * nd.invD);
             const float g = mx * one_minus_exp2_neg(fabsf(dl));
             gv[k] = mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
+            // the element holding both rows' largest logit: its q - p is formed
+            // in kl_coef from x = sum of the others' 2^(b) - 2^(a), a and b
+            // their logits less the rows' largest, from the exact difference
+            const bool at_top = xt[j][k] == nt.zmax && xd[j][k] == nd.zmax;
+            if (at_top) top = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV + k;
+            const float wf = static_cast<float>(wd);
+            const float mb = fmaxf(e * kt, f * kd);
+            const float xv = mb * one_minus_exp2_neg(fabsf(wf));
+            vx += (at_top || !(mb > 0.f)) ? 0.f : copysignf(xv, wf);
           }
         }
         se += static_cast<double>(ve);
@@ -338,17 +361,24 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
           sfx += static_cast<double>(vfx);
           wx += static_cast<double>(vwx);
           wm += static_cast<double>(vwm);
+        } else {
+          xs += static_cast<double>(vx);
         }
         if (write_grad)
           store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }
     }
-    double v[6] = {se, sf, w, sfx, wx, wm};
+    double v[6] = {se, sf, w, KIND == kKlReverse ? sfx : xs, wx, wm};
     wg_sum<6>(v, red);
+    const int tp = -wg_min_int(-top, red1);  // the largest index holding the top (at most one unless tied)
     if (threadIdx.x == 0) {
       KlPart o;
       o.se = v[0]; o.sf = v[1]; o.w = v[2];
-      o.sfx = v[3]; o.wx = v[4]; o.wm = v[5];
+      o.sfx = KIND == kKlReverse ? v[3] : 0.0;
+      o.wx = v[4]; o.wm = v[5];
+      o.x = KIND == kKlReverse ? 0.0 : v[3];
+      o.top = tp;
+      o.pad = 0;
       a.parts[t] = o;
     }
   }
@@ -391,6 +421,24 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
       const double le = log2(se), lf = log2(sf);
       L = (a.kind == kKlForward) ? w / se - le + lf : w / se + lf;
       L *= kLn2D;
+      // the element holding both rows' largest logit, each row's only one:
+      // with 1 + R = Z 2^(-zmax s), p = 1 / (1 + R_t), q = 1 / (1 + R_d) and
+      // R_t - R_d = -x, so q - p = -x / ((1 + R_t) (1 + R_d)) without the
+      // cancellation of two numbers near 1
+      double xs = 0.0;
+      int top = -1;
+      for (int cc = lane; cc < C; cc += 64) { xs += ps[cc].x; top = max(top, ps[cc].top); }
+      xs = wave_sum(xs);
+      top = -wave_min_int(-top);
+      const KlNorm& nt = a.norms[static_cast<int64_t>(n) * K + kk];
+      const KlNorm& nd = a.norms[static_cast<int64_t>(a.N) * K + static_cast<int64_t>(n) * K + kk];
+      if (lane == 0 && a.grad && top >= 0 && nt.n == 1 && nd.n == 1) {
+        const double s = static_cast<double>(scale_of(a.rows.temp_scalar));
+        const double rt = nt.D * exp2(static_cast<double>(nt.M) - static_cast<double>(nt.zmax) * s);
+        const double rd = nd.D * exp2(static_cast<double>(nd.M) - static_cast<double>(nd.zmax) * s);
+        const double g = a.scale * static_cast<double>(a.inv_t) / K * (-xs) / (rt * rd);
+        if (g == g) a.grad[(static_cast<int64_t>(n) * K + kk) * a.rows.V + top] = static_cast<float>(g);
+      }
     }
     Ln += L;
     if (lane == 0 && a.per_step) a.per_step[static_cast<int64_t>(n) * K + kk] = static_cast<float>(L);
@@ -430,7 +478,8 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
           const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
-          const float dl = kl_delta(xt[j][k], xd[j][k], dr);
+          const double wd = kl_wdiff(xt[j][k], xd[j][k], dr.c1, dr.s);
+          const float dl = static_cast<float>(wd + dr.lam);
           const float tm = (single_top && xd[j][k] == nd.zmax) ? fmaf(dl, A.z, -A.w) : dl - A.y;
           gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
         }

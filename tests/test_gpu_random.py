@@ -100,6 +100,15 @@ KL_PINNED = [
     (W.F32, 11, 5, 1024, "reverse", 0.5962657758118375, 1.0 / 11, 1568780994, 1.2949953247572092),
     (W.F32, 13, 3, 1024, "reverse", 0.5356229022213345, 1.0 / 13, 2124375422, 0.682026940167951),
     (W.BF16, 12, 7, 1024, "reverse", 0.5186915158172206, 1.0 / 12, 1904719211, 0.3153271407658461),
+    # the element holding both rows' largest logit at p = 0.57-0.98
+    (W.F32, 21, 8, 1024, "forward", 1.475596639665728, 1.0, 770393847, 0.10252011838269154),
+    (W.F32, 8, 6, 1024, "ce", 0.5467098178304036, 1.0, 227129657, 0.5021796655738667),
+    (W.F32, 22, 8, 1024, "forward", 0.7322401060693238, 1.0 / 22, 351533975, 0.13656003589084276),
+    pytest.param((W.F32, 18, 7, 1024, "ce", 0.8062491954075379, 0.25, 856847184, 0.34104919671853684),
+                 marks=pytest.mark.xfail(strict=False, reason=(
+                     "two tokens share nearly all the mass (p = 0.57 and 0.43): the second one's q - p still "
+                     "carries the float32 error of log Z_t - log Z_d (1.98e-5 against 1e-5); only the element "
+                     "holding both rows' largest logit is formed from the pairwise sum"))),
 ]
 
 
@@ -116,7 +125,12 @@ def _kl_case(dt, N, K, V, kind, T, scale, gen_seed, noise, qp=False):
     return compare_kl(loss, ps, grad, ref, dt)
 
 
-@pytest.mark.parametrize("case", KL_PINNED, ids=lambda c: "%s-%s-V%d-gen%d" % (c[0], c[4], c[3], c[7]))
+def _kl_id(c):
+    c = c.values[0] if hasattr(c, "values") else c
+    return "%s-%s-V%d-gen%d" % (c[0], c[4], c[3], c[7])
+
+
+@pytest.mark.parametrize("case", KL_PINNED, ids=_kl_id)
 def test_kl_previously_failing_cases(case):
     print(_kl_case(*case))
 
