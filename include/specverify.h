@@ -176,6 +176,34 @@ spec_status spec_verify_ex(const void* target_logits, int64_t t_stride_b, int64_
                            void* workspace, size_t workspace_bytes, void* stream,
                            const spec_launch* launch);
 
+/*
+ * spec_verify_noalloc — spec_verify for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same arguments without the workspace, which is
+ * instead a device array inside the library, one per GPU, held until the
+ * process ends.  The call itself allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine); the first call on a device looks up that
+ * device's copy of the array.
+ * Returns SPEC_EWORKSPACE when the shape needs more than
+ * spec_verify_noalloc_max_workspace() bytes (32 MiB: every shape up to
+ * B = 1024, K = 3, V = 262144 bf16 fits), and otherwise the statuses of
+ * spec_verify.  Calls on one GPU share its array: calls that overlap in time
+ * on one GPU (other streams, other host threads) race and must not be
+ * issued; calls queued on one stream are safe.
+ */
+spec_status spec_verify_noalloc(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                                const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                                spec_dtype dtype, int B, int K, int V,
+                                const int32_t* draft_ids,
+                                const float* temperature, float temperature_scalar,
+                                uint64_t seed, uint64_t offset,
+                                int32_t* accept_len, int32_t* emitted_ids,
+                                float* overlap, float* p_at_draft, float* q_at_draft,
+                                float* logz_target, float* logz_draft, void* stream);
+
+/* Largest workspace (bytes) spec_verify_noalloc can hold. */
+size_t spec_verify_noalloc_max_workspace(void);
+
 /* Bytes of workspace spec_tv_loss_fwd_bwd needs (0 on invalid sizes).  It
  * includes about one bit per logit (N*K*ceil(V/16384)*2048 bytes, about 1/32
  * of the gradient): the indicator 1[q <= p] of the forward pass, which the

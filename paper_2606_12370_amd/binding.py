@@ -53,6 +53,8 @@ class SpecLaunch(ctypes.Structure):
 
 
 VERIFY_EX_ARGTYPES = VERIFY_ARGTYPES + [ctypes.POINTER(SpecLaunch)]
+# spec_verify_noalloc: spec_verify without the workspace pointer and size
+VERIFY_NOALLOC_ARGTYPES = VERIFY_ARGTYPES[:-3] + [_P]
 KL_ARGTYPES = [_P, _I64, _I64, _P, _I64, _I64, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _SZ, _P]
 KL_KINDS = {"forward": 0, "ce": 1, "reverse": 2}
 DIAG_COLUMNS = ("entropy_target", "entropy_draft", "max_p", "alpha_to", "alpha_rs", "alpha_p_gt_q", "alpha_q_ge_p")
@@ -89,6 +91,10 @@ def load_library():
         lib.spec_verify.argtypes = VERIFY_ARGTYPES
         lib.spec_verify_ex.restype = _I
         lib.spec_verify_ex.argtypes = VERIFY_EX_ARGTYPES
+        lib.spec_verify_noalloc.restype = _I
+        lib.spec_verify_noalloc.argtypes = VERIFY_NOALLOC_ARGTYPES
+        lib.spec_verify_noalloc_max_workspace.restype = _SZ
+        lib.spec_verify_noalloc_max_workspace.argtypes = []
         lib.spec_tv_loss_fwd_bwd.restype = _I
         lib.spec_tv_loss_fwd_bwd.argtypes = TV_ARGTYPES
         lib.spec_verify_target_only_workspace_size.restype = _SZ
@@ -214,11 +220,13 @@ def _check_ids(ids, B, K):
 
 
 def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offset=0,
-           want_debug=False, want_overlap=True, ws=None, out=None, gumbel=False, path=None, groups=0):
+           want_debug=False, want_overlap=True, ws=None, out=None, gumbel=False, path=None, groups=0,
+           noalloc=False):
     """Chain rejection-sampling verification (spec_verify, or with
     gumbel=True spec_verify_gumbel: the emitted token drawn by Gumbel-max).
     path ("auto", "chain", "single_read") and groups select the launch
-    (spec_verify_ex); by default the library chooses.
+    (spec_verify_ex); by default the library chooses.  noalloc=True calls
+    spec_verify_noalloc (the library's own scratch array, no workspace).
 
     target_logits [B, K+1, V], draft_logits [B, K, V] (bf16 or f32, same
     dtype, vocabulary dimension contiguous), draft_ids [B, K] int32,
@@ -259,6 +267,19 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
             out["q_at_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
             out["logz_target"] = torch.empty((B, K + 1), dtype=torch.float32, device=dev)
             out["logz_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
+    if noalloc:
+        if gumbel or path is not None or groups:
+            raise ValueError("spec_verify_noalloc takes no launch controls")
+        st = lib.spec_verify_noalloc(
+            _ptr(target_logits), target_logits.stride(0), target_logits.stride(1),
+            _ptr(draft_logits), draft_logits.stride(0), draft_logits.stride(1),
+            code, B, K, V, _ptr(ids), t_ptr, t_scalar, int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
+            _ptr(out["accept_len"]), _ptr(out["emitted"]), _ptr(out.get("overlap")),
+            _ptr(out.get("p_at_draft")), _ptr(out.get("q_at_draft")),
+            _ptr(out.get("logz_target")), _ptr(out.get("logz_draft")), _stream(dev))
+        if st != 0:
+            raise SpecError("spec_verify_noalloc", st)
+        return out
     size_fn = lib.spec_verify_gumbel_workspace_size if gumbel else lib.spec_verify_workspace_size
     fn, name = (lib.spec_verify_gumbel, "spec_verify_gumbel") if gumbel else (lib.spec_verify, "spec_verify")
     extra = ()

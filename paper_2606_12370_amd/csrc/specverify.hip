@@ -516,6 +516,37 @@ spec_status prepare_verify(const void* target_logits, int64_t t_stride_b, int64_
   return SPEC_OK;
 }
 
+// ---- scratch memory for spec_verify_noalloc -------------------------------
+// The workspace of spec_verify_noalloc: a file-scope device array, one copy
+// on every GPU the library runs on, held until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is only a
+// stand-in for the symbol); it uses the device address that
+// hipGetSymbolAddress returns, once per device, with that device current.
+constexpr size_t kScratchBytes = size_t{32} << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+void* g_scratch_ptr[kMaxDevices] = {};
+std::atomic<int> g_scratch_ready[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+// The current device's address of `scratch`, or nullptr on failure.
+void* scratch_ptr() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  if (g_scratch_ready[dev].load(std::memory_order_acquire)) return g_scratch_ptr[dev];
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ready[dev].load(std::memory_order_relaxed)) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+    g_scratch_ready[dev].store(1, std::memory_order_release);
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -577,6 +608,39 @@ spec_status spec_verify_ex(const void* target_logits, int64_t t_stride_b, int64_
   const int64_t rows = int64_t{B} * (2 * K + 1);
   hipStream_t s = static_cast<hipStream_t>(stream);
   return dtype == SPEC_BF16 ? launch_verify<BF16>(a, rows, s, launch) : launch_verify<F32>(a, rows, s, launch);
+}
+
+size_t spec_verify_noalloc_max_workspace(void) { return kScratchBytes; }
+
+spec_status spec_verify_noalloc(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
+                                const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,
+                                spec_dtype dtype, int B, int K, int V, const int32_t* draft_ids,
+                                const float* temperature, float temperature_scalar, uint64_t seed,
+                                uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
+                                float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
+                                void* stream) {
+  const size_t need = spec_verify_workspace_size(B, K, V, dtype);
+  if (need > kScratchBytes) return SPEC_EWORKSPACE;  // beyond the scratch array (also: need 0 is checked below)
+  // a first pass over the arguments (with a stand-in workspace address that is
+  // never used) returns argument errors before the scratch address is looked
+  // up, so a bad call does not touch the GPU
+  sv::VerifyArgs a;
+  sv::GumbelBest* gb;
+  spec_status st = prepare_verify(target_logits, t_stride_b, t_stride_k, draft_logits, d_stride_b, d_stride_k,
+                                  dtype, B, K, V, draft_ids, temperature, temperature_scalar, seed, offset,
+                                  accept_len, emitted_ids, overlap, p_at_draft, q_at_draft, logz_target,
+                                  logz_draft, reinterpret_cast<void*>(uintptr_t{256}), kScratchBytes, false, &a,
+                                  &gb);
+  if (st != SPEC_OK) return st;
+  void* ws = scratch_ptr();
+  if (!ws) return SPEC_EHIP;
+  st = prepare_verify(target_logits, t_stride_b, t_stride_k, draft_logits, d_stride_b, d_stride_k, dtype, B, K, V,
+                      draft_ids, temperature, temperature_scalar, seed, offset, accept_len, emitted_ids, overlap,
+                      p_at_draft, q_at_draft, logz_target, logz_draft, ws, kScratchBytes, false, &a, &gb);
+  if (st != SPEC_OK) return st;
+  const int64_t rows = int64_t{B} * (2 * K + 1);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return dtype == SPEC_BF16 ? launch_verify<BF16>(a, rows, s) : launch_verify<F32>(a, rows, s);
 }
 
 size_t spec_verify_gumbel_workspace_size(int B, int K, int V, spec_dtype dtype) {

@@ -41,7 +41,8 @@ def test_exports_every_declared_function(lib):
                            "spec_diagnostics_workspace_size", "spec_diagnostics",
                            "spec_verify_gumbel_workspace_size", "spec_verify_gumbel",
                            "spec_sample_gumbel_workspace_size", "spec_sample_gumbel",
-                           "spec_kl_workspace_size", "spec_kl_loss_fwd_bwd", "spec_verify_ex"}
+                           "spec_kl_workspace_size", "spec_kl_loss_fwd_bwd", "spec_verify_ex",
+                           "spec_verify_noalloc", "spec_verify_noalloc_max_workspace"}
     for name in protos:
         assert hasattr(lib, name), name
 
@@ -59,6 +60,8 @@ def test_ctypes_prototypes_match_header():
     assert len(protos["spec_kl_loss_fwd_bwd"]) == len(binding.KL_ARGTYPES)
     assert len(protos["spec_verify_ex"]) == len(binding.VERIFY_EX_ARGTYPES)
     assert protos["spec_verify_ex"][:-1] == protos["spec_verify"]
+    assert len(protos["spec_verify_noalloc"]) == len(binding.VERIFY_NOALLOC_ARGTYPES)
+    assert protos["spec_verify_noalloc"][:-1] == protos["spec_verify"][:-3]
 
 
 def test_diag_columns_match_header():
@@ -405,3 +408,16 @@ def test_c99_client_links_and_calls(lib, tmp_path):
     assert int(out[2]) == lib.spec_verify_workspace_size(256, 3, 151936, 1)
     assert int(out[3]) == lib.spec_tv_workspace_size(16384, 3, 151936, 1)
     assert int(out[4]) == 1  # SPEC_EINVAL
+
+
+def test_verify_noalloc_limits_without_a_gpu(lib):
+    """The scratch array's size is reported, a shape beyond it is refused and
+    argument errors are returned, all before the GPU is touched."""
+    assert lib.spec_verify_noalloc_max_workspace() == 32 << 20
+    big = lib.spec_verify_noalloc(FAKE, 1 << 22, 1 << 18, FAKE, 1 << 22, 1 << 18, 1, 4096, 8, 262144, FAKE, None,
+                                  1.0, 0, 0, FAKE, FAKE, None, None, None, None, None, None)
+    assert big == 4  # SPEC_EWORKSPACE
+    assert lib.spec_verify_noalloc(None, 400, 100, FAKE, 300, 100, 1, 4, 3, 100, FAKE, None, 1.0, 0, 0, FAKE, FAKE,
+                                   None, None, None, None, None, None) == 1
+    assert lib.spec_verify_noalloc(FAKE, 400, 100, FAKE, 300, 100, 1, 4, 9, 100, FAKE, None, 1.0, 0, 0, FAKE, FAKE,
+                                   None, None, None, None, None, None) == 2
