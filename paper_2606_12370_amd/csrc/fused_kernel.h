@@ -276,7 +276,7 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
   if (n >= 0) {
     const float s = scale_of(temperature_of(a.rows, b));
     float al[K];
-    float zp = 0.f, zn = 0.f, qg = 0.f;
+    float zp = 0.f, sd = 0.f, qg = 0.f;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
       al[i] = 0.f;
@@ -294,7 +294,7 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
             const ElemPQ e = elem_pq(xt[k], xd[k], s, nt, nd, rr);
             al[i] += e.mn;
             zp += fmaxf(e.diff, 0.f);
-            zn += fminf(e.diff, 0.f);
+            sd += e.diff;
             qg += e.diff > 0.f ? e.mn : 0.f;
           }
         }
@@ -317,7 +317,7 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
     }
     if (n < K) {
       const double v0 = wave_sum(static_cast<double>(zp));
-      const double v1 = wave_sum(static_cast<double>(zn));
+      const double v1 = wave_sum(static_cast<double>(sd));
       const double v2 = wave_sum(static_cast<double>(qg));
       if (lane == 0) {
         sh.pr[c.wave][K] = v0;
@@ -338,7 +338,7 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
           t[3] += sh.pr[q][K + 2];
         }
       }
-      o.alpha = t[0]; o.Z = t[1]; o.N = t[2]; o.Qg = t[3];
+      o.alpha = t[0]; o.Z = t[1]; o.Sd = t[2]; o.Qg = t[3];
       a.pairs[static_cast<int64_t>(b * K + c.tid) * G + c.g] = o;
     }
   }

@@ -32,6 +32,7 @@ struct BF16 {
   using raw = uint16_t;
   using vec = u32x4;
   static constexpr int EPV = 8;
+  static constexpr bool kFoldRef = true;  // the overlap may fold M + L into one constant
   static __device__ __forceinline__ void widen(const vec v, float (&x)[8]) {
     x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xffff0000u);
     x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xffff0000u);
@@ -47,6 +48,7 @@ struct BF16H {
   using raw = uint16_t;
   using vec = u32x2;
   static constexpr int EPV = 4;
+  static constexpr bool kFoldRef = true;
   static __device__ __forceinline__ void widen(const vec v, float (&x)[4]) {
     x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xffff0000u);
     x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xffff0000u);
@@ -58,6 +60,7 @@ struct F32 {
   using raw = float;
   using vec = u32x4;
   static constexpr int EPV = 4;
+  static constexpr bool kFoldRef = false;
   static __device__ __forceinline__ void widen(const vec v, float (&x)[4]) {
     x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y);
     x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
@@ -436,6 +439,22 @@ __device__ __forceinline__ float prob(float z, float s, float M, float invD) {
 // One more rounding than prob() (L enters as a float), about 1e-6 relative.
 __device__ __forceinline__ float min_prob(float zt, float zd, float s, const RowNorm& t, const RowNorm& d) {
   return __builtin_amdgcn_exp2f(fminf(fmaf(zt, s, -t.M) - t.L, fmaf(zd, s, -d.M) - d.L));
+}
+
+// min(p, q) with each row's reference and log2 normaliser folded into one
+// float32 constant r = M + L: one rounding of r (about 6e-8 |r|, a few 1e-6
+// relative for logits of size 100) against the two subtractions it saves;
+// used for bfloat16 logits, whose tolerance is 2e-3.
+__device__ __forceinline__ float min_prob_folded(float zt, float zd, float s, float rt, float rd) {
+  return __builtin_amdgcn_exp2f(fminf(fmaf(zt, s, -rt), fmaf(zd, s, -rd)));
+}
+
+// The overlap term of element type E: folded references for bfloat16 logits.
+template <class E>
+__device__ __forceinline__ float overlap_term(float zt, float zd, float s, const RowNorm& t, const RowNorm& d,
+                                              float rt, float rd) {
+  if constexpr (E::kFoldRef) return min_prob_folded(zt, zd, s, rt, rd);
+  else return min_prob(zt, zd, s, t, d);
 }
 
 // 1 - 2^-x for x >= 0: the series of -expm1(-y), y = x ln2, below x = 1/2

@@ -30,7 +30,7 @@ struct PairStat {  // one sub-chunk of a (target, draft) pair
   double alpha;    // sum min(p, q)
   // the row's first rejected step only: with p, q from the row normalisers,
   double Z;        // sum max(0, p - q)
-  double N;        // sum min(0, p - q)
+  double Sd;       // sum (p - q)
   double Qg;       // sum of q over the elements with p > q
 };
 
@@ -45,7 +45,7 @@ struct PairStat {  // one sub-chunk of a (target, draft) pair
 // about 1e-7: scaling p by rho = sum q / sum p (the sums of the same element
 // values over the whole row) makes both sum to the same total, and the
 // residual becomes max(0, (p - q) - p (1 - rho)).  1 - rho is itself formed
-// from accurate sums, (Z + N) / (alpha + Z) over the row's PairStat totals.
+// from accurate sums, Sd / (alpha + Z) over the row's PairStat totals.
 struct ResidualRef {
   float ch, cl;  // c = ch + cl
   float w;       // 1 - rho (0 while the pair pass forms the sums)
@@ -64,8 +64,12 @@ __device__ __forceinline__ ResidualRef residual_ref(const RowNorm& t, const RowN
 constexpr ResidualRef kNoResidual = {0.f, 0.f, 0.f};
 
 // Signed p - q of one element and its min(p, q) and max(p, q), from the
-// logits: lp, lq the float32 log2 probabilities, d the accurate log ratio
-// (which also decides which side is larger).
+// logits: lp, lq the float32 log2 probabilities, d the accurate log ratio.
+// Below |d| = 1/2, |p - q| = max(p, q) (1 - 2^-|d|) with the series of
+// 1 - e^-y (y = |d| ln 2 < 0.35, terms to y^7: truncation below 6e-8 of the
+// value); above it the difference of the two exponentials, whose ratio is
+// then at most 2^-1/2, so their rounding is at most six times the exponentials'
+// own relative error.
 struct ElemPQ {
   float diff;  // p - q
   float mn;    // min(p, q)
@@ -76,12 +80,23 @@ __device__ __forceinline__ ElemPQ elem_pq(float zt, float zd, float s, const Row
   const float lp = fmaf(zt, s, -t.M) - t.L;
   const float lq = fmaf(zd, s, -d.M) - d.L;
   const float dd = fmaf(zt - zd, s, -rr.ch) - rr.cl;
-  const bool pbig = dd > 0.f;
   ElemPQ e;
-  e.mx = __builtin_amdgcn_exp2f(pbig ? lp : lq);
-  e.mn = __builtin_amdgcn_exp2f(pbig ? lq : lp);
-  const float g = e.mx * one_minus_exp2_neg(fabsf(dd));
-  e.diff = e.mx > 0.f ? copysignf(g, dd) : 0.f;
+  e.mx = __builtin_amdgcn_exp2f(fmaxf(lp, lq));
+  const float mn = __builtin_amdgcn_exp2f(fminf(lp, lq));
+  const float y = fabsf(dd) * 0.69314718f;
+  float p = 1.f / 5040.f;
+  p = fmaf(p, -y, 1.f / 720.f);
+  p = fmaf(p, -y, 1.f / 120.f);
+  p = fmaf(p, -y, 1.f / 24.f);
+  p = fmaf(p, -y, 1.f / 6.f);
+  p = fmaf(p, -y, 0.5f);
+  p = fmaf(p, -y, 1.f);
+  const bool small = y < 0.34657359f;  // |d| < 1/2
+  // (both logits -inf: mx = mn = 0 and g = 0; one of them -inf: |d| = inf and
+  // g = mx, the other probability)
+  const float g = small ? e.mx * (y * p) : e.mx - mn;
+  e.diff = copysignf(g, dd);
+  e.mn = small ? e.mx - g : mn;
   return e;
 }
 
@@ -275,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
     wg_sum<4>(v, red);
     if (threadIdx.x == 0) {
       PairStat o;
-      o.alpha = v[0]; o.Z = 0.0; o.N = 0.0; o.Qg = 0.0;
+      o.alpha = v[0]; o.Z = 0.0; o.Sd = 0.0; o.Qg = 0.0;
       a.pairs[t] = o;
     }
   }
@@ -311,16 +326,20 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
     const float s = scale_of(temperature_of(d, b));
     const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
     const ResidualRef rr = residual_ref(nt, nd, 0.0);
+    const float rft = static_cast<float>(static_cast<double>(nt.M) + static_cast<double>(nt.L));
+    const float rfd = static_cast<float>(static_cast<double>(nd.M) + static_cast<double>(nd.L));
     const int e0 = j * WV * 64 * EPV;
-    float al = 0.f, zp = 0.f, zn = 0.f, qg = 0.f;
-#pragma unroll
-    for (int st = 0; st < WV / S; ++st) {
-      const int es = e0 + st * S * 64 * EPV;
-      if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
-      float xt[S][EPV], xd[S][EPV];
-      load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
-      load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
-      if (need_z) {
+    float al = 0.f, zp = 0.f, sd = 0.f, qg = 0.f;
+    if (need_z) {
+      // the rejected step: overlap and residual sums (a loop that is not
+      // unrolled, so that its longer body does not multiply the code size)
+#pragma unroll 1
+      for (int st = 0; st < WV / S; ++st) {
+        const int es = e0 + st * S * 64 * EPV;
+        if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+        float xt[S][EPV], xd[S][EPV];
+        load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
+        load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
 #pragma unroll
         for (int q = 0; q < S; ++q)
 #pragma unroll
@@ -328,20 +347,28 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
             const ElemPQ e = elem_pq(xt[q][k], xd[q][k], s, nt, nd, rr);
             al += e.mn;
             zp += fmaxf(e.diff, 0.f);
-            zn += fminf(e.diff, 0.f);
+            sd += e.diff;
             qg += e.diff > 0.f ? e.mn : 0.f;
           }
-      } else {
+      }
+    } else {
+#pragma unroll
+      for (int st = 0; st < WV / S; ++st) {
+        const int es = e0 + st * S * 64 * EPV;
+        if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+        float xt[S][EPV], xd[S][EPV];
+        load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
+        load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
 #pragma unroll
         for (int q = 0; q < S; ++q)
 #pragma unroll
-          for (int k = 0; k < EPV; ++k) al += min_prob(xt[q][k], xd[q][k], s, nt, nd);
+          for (int k = 0; k < EPV; ++k) al += overlap_term<E>(xt[q][k], xd[q][k], s, nt, nd, rft, rfd);
       }
     }
     PairStat o;
     o.alpha = wave_sum(static_cast<double>(al));
     o.Z = need_z ? wave_sum(static_cast<double>(zp)) : 0.0;
-    o.N = need_z ? wave_sum(static_cast<double>(zn)) : 0.0;
+    o.Sd = need_z ? wave_sum(static_cast<double>(sd)) : 0.0;
     o.Qg = need_z ? wave_sum(static_cast<double>(qg)) : 0.0;
     if (lane == 0) a.pairs[g] = o;
   }
@@ -593,7 +620,7 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   if (wave == 0) {
 #pragma unroll
     for (int i = 0; i < SPEC_MAX_K_DEV; ++i) {
-      ppre[i].alpha = 0.0; ppre[i].Z = 0.0; ppre[i].N = 0.0; ppre[i].Qg = 0.0;
+      ppre[i].alpha = 0.0; ppre[i].Z = 0.0; ppre[i].Sd = 0.0; ppre[i].Qg = 0.0;
       if (i < K && lane < C) ppre[i] = a.pairs[static_cast<int64_t>(b * K + i) * C + lane];
     }
     if (lane < C) spre = a.stats[static_cast<int64_t>(target_row(a, b, K)) * C + lane];
@@ -625,22 +652,22 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
   if (wave == 0) {
     const PairStat* ps = a.pairs + static_cast<int64_t>(b * K + (n < K ? n : 0)) * C;
     PairStat p0;
-    p0.alpha = 0.0; p0.Z = 0.0; p0.N = 0.0; p0.Qg = 0.0;
+    p0.alpha = 0.0; p0.Z = 0.0; p0.Sd = 0.0; p0.Qg = 0.0;
 #pragma unroll
     for (int i = 0; i < SPEC_MAX_K_DEV; ++i)
       if (i == n) p0 = ppre[i];
     // the row's totals at the rejected step, and its normalisation correction
     double w = 0.0, zs = 0.0;
     if (n < K) {
-      double za = 0.0, zn = 0.0, zal = 0.0;
+      double za = 0.0, zd = 0.0, zal = 0.0;
       for (int cc = lane; cc < C; cc += 64) {
         const PairStat q = cc < 64 ? p0 : ps[cc];
-        za += q.Z; zn += q.N; zal += q.alpha;
+        za += q.Z; zd += q.Sd; zal += q.alpha;
       }
       za = wave_sum(za);
-      zn = wave_sum(zn);
+      zd = wave_sum(zd);
       zal = wave_sum(zal);
-      w = (za + zn) / (zal + za);
+      w = zd / (zal + za);
       if (!(w == w)) w = 0.0;
       for (int cc = lane; cc < C; cc += 64) {
         const PairStat q = cc < 64 ? p0 : ps[cc];
