@@ -293,9 +293,9 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
           for (int k = 0; k < EPV; ++k) {
             const ElemPQ e = elem_pq(xt[k], xd[k], s, nt, nd, rr);
             al[i] += e.mn;
-            zp += fmaxf(e.diff, 0.f);
-            sd += e.diff;
-            qg += e.diff > 0.f ? e.mn : 0.f;
+            zp += e.pos ? e.g : 0.f;
+            sd += e.diff();
+            qg += e.pos ? e.mn : 0.f;
           }
         }
       } else {

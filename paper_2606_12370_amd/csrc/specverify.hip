@@ -323,8 +323,9 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, 
   hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
   // one workgroup per four (pair, sub-chunk) items: measured faster than a
   // grid of what the device holds at once striding over them (73.6 against
-  // 75.0 us at B=256, K=3, V=151936 bf16)
-  const int64_t items = int64_t{a.B} * a.K * a.rows.C;
+  // 75.0 us at B=256, K=3, V=151936 bf16); without overlaps only each batch
+  // row's residual step is read again
+  const int64_t items = int64_t{a.B} * (a.overlap ? a.K : 1) * a.rows.C;
   hipLaunchKernelGGL((sv::pair_pass_wave_kernel<E, kStep, kPairVec>),
                      dim3(static_cast<unsigned>((items + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s, a,
                      items);

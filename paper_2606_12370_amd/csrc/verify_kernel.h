@@ -71,19 +71,23 @@ constexpr ResidualRef kNoResidual = {0.f, 0.f, 0.f};
 // then at most 2^-1/2, so their rounding is at most six times the exponentials'
 // own relative error.
 struct ElemPQ {
-  float diff;  // p - q
-  float mn;    // min(p, q)
-  float mx;    // max(p, q)
+  float g;    // |p - q|
+  float dd;   // the accurate log2 p - log2 q (its sign is the sign of p - q)
+  float mn;   // min(p, q)
+  float mx;   // max(p, q)
+  bool pos;   // p > q by the accurate log ratio
+  __device__ __forceinline__ float diff() const { return copysignf(g, dd); }  // p - q
 };
 __device__ __forceinline__ ElemPQ elem_pq(float zt, float zd, float s, const RowNorm& t, const RowNorm& d,
                                           const ResidualRef& rr) {
   const float lp = fmaf(zt, s, -t.M) - t.L;
   const float lq = fmaf(zd, s, -d.M) - d.L;
-  const float dd = fmaf(zt - zd, s, -rr.ch) - rr.cl;
   ElemPQ e;
+  e.dd = fmaf(zt - zd, s, -rr.ch) - rr.cl;
+  e.pos = e.dd > 0.f;
   e.mx = __builtin_amdgcn_exp2f(fmaxf(lp, lq));
   const float mn = __builtin_amdgcn_exp2f(fminf(lp, lq));
-  const float y = fabsf(dd) * 0.69314718f;
+  const float y = fabsf(e.dd) * 0.69314718f;
   float p = 1.f / 5040.f;
   p = fmaf(p, -y, 1.f / 720.f);
   p = fmaf(p, -y, 1.f / 120.f);
@@ -94,9 +98,8 @@ __device__ __forceinline__ ElemPQ elem_pq(float zt, float zd, float s, const Row
   const bool small = y < 0.34657359f;  // |d| < 1/2
   // (both logits -inf: mx = mn = 0 and g = 0; one of them -inf: |d| = inf and
   // g = mx, the other probability)
-  const float g = small ? e.mx * (y * p) : e.mx - mn;
-  e.diff = copysignf(g, dd);
-  e.mn = small ? e.mx - g : mn;
+  e.g = small ? e.mx * (y * p) : e.mx - mn;
+  e.mn = small ? e.mx - e.g : mn;
   return e;
 }
 
@@ -104,7 +107,7 @@ __device__ __forceinline__ ElemPQ elem_pq(float zt, float zd, float s, const Row
 __device__ __forceinline__ float residual_mass(float zt, float zd, float s, const RowNorm& t, const RowNorm& d,
                                                const ResidualRef& rr) {
   const ElemPQ e = elem_pq(zt, zd, s, t, d, rr);
-  return e.diff > 0.f ? fmaxf(e.diff - e.mx * rr.w, 0.f) : 0.f;
+  return e.pos ? fmaxf(e.g - e.mx * rr.w, 0.f) : 0.f;
 }
 
 struct VerifyArgs {
@@ -296,12 +299,68 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
   }
 }
 
-// Pass 2 with one wave per (pair, sub-chunk) item: item g = u * C + j is
-// sub-chunk j (ST tiles of 256 vectors, i.e. ST * 4 vectors of the wave's 64
-// lanes) of draft pair u = b * K + i.  The wave sums the overlap (and, for the
-// row's first rejected step, the residual mass) S vectors per lane at a time,
-// then one float64 wave sum per quantity: no LDS and no barrier.  Written
-// grid-stride over groups of kWaves items (launched one workgroup per group).
+// The pair-pass sums of one wave over load steps st0 .. st1-1 of the sub-chunk
+// at element e0: the overlap, and for the residual step the residual sums.
+struct PairSums {
+  float al = 0.f, zp = 0.f, sd = 0.f, qg = 0.f;
+};
+
+template <class E, int S>
+__device__ __forceinline__ void pair_span_sums(const typename E::raw* rt, const typename E::raw* rd, bool al_t,
+                                               bool al_d, int e0, int st0, int st1, int lane, int V, float s,
+                                               const RowNorm& nt, const RowNorm& nd, bool need_z, PairSums& o) {
+  constexpr int EPV = E::EPV;
+  if (need_z) {
+    const ResidualRef rr = residual_ref(nt, nd, 0.0);
+    // (a loop that is not unrolled, so that its longer body does not multiply
+    // the code size)
+#pragma unroll 1
+    for (int st = st0; st < st1; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      if (es >= V) break;  // wave-uniform: the row's last sub-chunk may be short
+      float xt[S][EPV], xd[S][EPV];
+      load_span<E, S, 64>(rt, es, lane, V, al_t, xt);
+      load_span<E, S, 64>(rd, es, lane, V, al_d, xd);
+#pragma unroll
+      for (int q = 0; q < S; ++q)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) {
+          const ElemPQ e = elem_pq(xt[q][k], xd[q][k], s, nt, nd, rr);
+          o.al += e.mn;
+          o.zp += e.pos ? e.g : 0.f;
+          o.sd += e.diff();
+          o.qg += e.pos ? e.mn : 0.f;
+        }
+    }
+  } else {
+    const float rft = static_cast<float>(static_cast<double>(nt.M) + static_cast<double>(nt.L));
+    const float rfd = static_cast<float>(static_cast<double>(nd.M) + static_cast<double>(nd.L));
+#pragma unroll
+    for (int st = st0; st < st1; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      if (es >= V) break;  // wave-uniform: the row's last sub-chunk may be short
+      float xt[S][EPV], xd[S][EPV];
+      load_span<E, S, 64>(rt, es, lane, V, al_t, xt);
+      load_span<E, S, 64>(rd, es, lane, V, al_d, xd);
+#pragma unroll
+      for (int q = 0; q < S; ++q)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) o.al += overlap_term<E>(xt[q][k], xd[q][k], s, nt, nd, rft, rfd);
+    }
+  }
+}
+
+// Pass 2 with one wave per (pair, sub-chunk) item.  Sub-chunk j covers ST
+// tiles of 256 vectors (ST * 4 vectors of the wave's 64 lanes), read S vectors
+// per lane and load step, then one float64 wave sum per quantity: no LDS and
+// no barrier.  Items are ordered longest first: items 0 .. B*C-1 are the
+// sub-chunks of each batch row's residual step (its first rejected step, or
+// step K-1 of a row that accepts every draft), the B*(K-1)*C items after them
+// the row's other steps (item (b*(K-1) + m)*C + j is sub-chunk j of the m-th
+// of row b's other steps).  A residual item costs about three times an
+// overlap item, and taking those first keeps them from piling up on a few
+// SIMDs at the end of the launch.  Without overlaps only the first B*C items
+// are launched.  kWaves items per workgroup.
 template <class E, int ST, int S>
 __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, int64_t nitems) {
   constexpr int EPV = E::EPV;
@@ -310,68 +369,42 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
   const RowsDesc& d = a.rows;
   const int C = d.C;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave; g < nitems;
-       g += static_cast<int64_t>(gridDim.x) * kWaves) {
-    const int u = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
-    const int b = u / a.K, i = u % a.K;
-    const int n = a.decision[b];
-    if (n < 0) continue;  // data error: finish ignores this row's partials
-    const bool need_z = a.want_z && i == n;
-    if (!need_z && a.overlap == nullptr) continue;  // no overlap requested: only the residual step is read again
-    const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
-    int bb;
-    bool al_t, al_d;
-    const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
-    const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
-    const float s = scale_of(temperature_of(d, b));
-    const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-    const ResidualRef rr = residual_ref(nt, nd, 0.0);
-    const float rft = static_cast<float>(static_cast<double>(nt.M) + static_cast<double>(nt.L));
-    const float rfd = static_cast<float>(static_cast<double>(nd.M) + static_cast<double>(nd.L));
-    const int e0 = j * WV * 64 * EPV;
-    float al = 0.f, zp = 0.f, sd = 0.f, qg = 0.f;
-    if (need_z) {
-      // the rejected step: overlap and residual sums (a loop that is not
-      // unrolled, so that its longer body does not multiply the code size)
-#pragma unroll 1
-      for (int st = 0; st < WV / S; ++st) {
-        const int es = e0 + st * S * 64 * EPV;
-        if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
-        float xt[S][EPV], xd[S][EPV];
-        load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
-        load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
-#pragma unroll
-        for (int q = 0; q < S; ++q)
-#pragma unroll
-          for (int k = 0; k < EPV; ++k) {
-            const ElemPQ e = elem_pq(xt[q][k], xd[q][k], s, nt, nd, rr);
-            al += e.mn;
-            zp += fmaxf(e.diff, 0.f);
-            sd += e.diff;
-            qg += e.diff > 0.f ? e.mn : 0.f;
-          }
-      }
-    } else {
-#pragma unroll
-      for (int st = 0; st < WV / S; ++st) {
-        const int es = e0 + st * S * 64 * EPV;
-        if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
-        float xt[S][EPV], xd[S][EPV];
-        load_span<E, S, 64>(rt, es, lane, d.V, al_t, xt);
-        load_span<E, S, 64>(rd, es, lane, d.V, al_d, xd);
-#pragma unroll
-        for (int q = 0; q < S; ++q)
-#pragma unroll
-          for (int k = 0; k < EPV; ++k) al += overlap_term<E>(xt[q][k], xd[q][k], s, nt, nd, rft, rfd);
-      }
-    }
-    PairStat o;
-    o.alpha = wave_sum(static_cast<double>(al));
-    o.Z = need_z ? wave_sum(static_cast<double>(zp)) : 0.0;
-    o.Sd = need_z ? wave_sum(static_cast<double>(sd)) : 0.0;
-    o.Qg = need_z ? wave_sum(static_cast<double>(qg)) : 0.0;
-    if (lane == 0) a.pairs[g] = o;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  if (g >= nitems) return;
+  const int64_t first = static_cast<int64_t>(a.B) * C;
+  int b, j, m = 0;
+  if (g < first) {
+    b = static_cast<int>(g / C);
+    j = static_cast<int>(g - static_cast<int64_t>(b) * C);
+  } else {
+    const int64_t g2 = g - first, per = static_cast<int64_t>(a.K - 1) * C;
+    b = static_cast<int>(g2 / per);
+    const int r = static_cast<int>(g2 - static_cast<int64_t>(b) * per);
+    m = r / C;
+    j = r - m * C;
   }
+  const int n = a.decision[b];
+  if (n < 0) return;  // data error: finish ignores this row's partials
+  const bool rejects = a.want_z && n < a.K;
+  const int i0 = rejects ? n : a.K - 1;
+  const int i = g < first ? i0 : (m < i0 ? m : m + 1);
+  const bool need_z = rejects && g < first;
+  if (!need_z && a.overlap == nullptr) return;  // no overlap requested: only the residual step is read again
+  const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
+  int bb;
+  bool al_t, al_d;
+  const typename E::raw* rt = row_of<E>(d, rt_i, &bb, &al_t);
+  const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
+  const float s = scale_of(temperature_of(d, b));
+  const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
+  PairSums o;
+  pair_span_sums<E, S>(rt, rd, al_t, al_d, j * WV * 64 * EPV, 0, WV / S, lane, d.V, s, nt, nd, need_z, o);
+  PairStat ps;
+  ps.alpha = wave_sum(static_cast<double>(o.al));
+  ps.Z = need_z ? wave_sum(static_cast<double>(o.zp)) : 0.0;
+  ps.Sd = need_z ? wave_sum(static_cast<double>(o.sd)) : 0.0;
+  ps.Qg = need_z ? wave_sum(static_cast<double>(o.qg)) : 0.0;
+  if (lane == 0) a.pairs[(static_cast<int64_t>(b) * a.K + i) * C + j] = ps;
 }
 
 // Residual (or target) mass of the EPV elements of one thread's vector;
