@@ -132,9 +132,11 @@ def _oracle_rows_worker(args):
 
 
 def cpu_baseline_all_cores(d_host, K, budget_s=10.0, workers=None):
-    """The same oracle on every host core the box grants (at most 16): the
-    batch's rows split over spawned worker processes, each timing its own
-    loop; throughput = all rows verified / the longest worker's time."""
+    """The same oracle on up to 16 worker processes (fewer where the host
+    reports fewer CPUs): the batch's rows split over spawned workers, each
+    timing its own loop; throughput = all rows verified / the longest
+    worker's time.  `cores` is the number of workers, `host_cpus` what the
+    host reports (os.cpu_count(), which may exceed what the job is granted)."""
     import multiprocessing as mp
     n = workers or max(1, min(16, os.cpu_count() or 1))
     tgt, drf, ids, T = d_host
@@ -148,9 +150,11 @@ def cpu_baseline_all_cores(d_host, K, budget_s=10.0, workers=None):
         "value": rows * K / span,
         "unit": "verified draft tokens/s",
         "cores": len(parts),
+        "host_cpus": os.cpu_count(),
         "kind": "oracle",
         "sample": "%d rows of the B=256 K=3 V=151936 bf16 batch through the float64 NumPy oracle, its rows split "
-                  "over %d worker processes, %.1f s of wall time each" % (rows, len(parts), span),
+                  "over %d worker processes (the host reports %s CPUs), %.1f s of wall time each"
+                  % (rows, len(parts), os.cpu_count(), span),
     }
 
 

@@ -18,8 +18,10 @@
  *    library allocates no device or host memory and keeps no mutable state
  *    between calls other than what lives in the caller's workspace.
  *  - The last dimension (vocabulary, length V) must be contiguous.  Other
- *    dimensions take element strides, so shifted views of larger tensors can
- *    be passed without copies.
+ *    dimensions take element strides (>= 0), so shifted views of larger
+ *    tensors can be passed without copies.  A tensor whose last element,
+ *    reached through the strides, lies beyond the 64-bit address space is
+ *    SPEC_EINVAL.
  *  - Work is only enqueued on `stream` (a hipStream_t passed as void*, NULL =
  *    the null stream); no call synchronises with the host.
  *  - Host-checkable argument errors are returned synchronously before any
@@ -54,14 +56,24 @@ extern "C" {
 #endif
 
 #define SPEC_VERSION 1
+
+/* The enumerations below are int-sized.  C++ gives them int as their fixed
+ * underlying type, so that any int a caller passes (a C program, a foreign
+ * function interface) is a value of the type and the library's range checks
+ * see it; C declares them without one. */
+#ifdef __cplusplus
+#define SPEC_ENUM_INT : int
+#else
+#define SPEC_ENUM_INT
+#endif
 #define SPEC_MAX_K 8 /* largest number of draft steps K */
 /* largest vocabulary V (2^31 - 2^16): element indices are 32-bit and run one
  * 16384-element chunk past V where a row's last chunk is rounded up */
 #define SPEC_MAX_V 2147418112
 
-typedef enum { SPEC_F32 = 0, SPEC_BF16 = 1 } spec_dtype;
+typedef enum SPEC_ENUM_INT { SPEC_F32 = 0, SPEC_BF16 = 1 } spec_dtype;
 
-typedef enum {
+typedef enum SPEC_ENUM_INT {
   SPEC_OK = 0,
   SPEC_EINVAL = 1,       /* bad pointer, size, stride, temperature, mode */
   SPEC_EUNSUPPORTED = 2, /* dtype or K outside what the library handles */
@@ -69,7 +81,7 @@ typedef enum {
   SPEC_EHIP = 5          /* the HIP runtime reported an error (launch, device query) */
 } spec_status;
 
-typedef enum {
+typedef enum SPEC_ENUM_INT {
   SPEC_TV_E2E = 0,     /* Sec. 4.2 Eq. e2e_tv: L = 1 - (1/K) sum_j prod_{i<=j} alpha_i        */
   SPEC_TV_PROD = 1,    /* L = -prod_k alpha_k (negated probability that all K drafts pass)  */
   SPEC_TV_PER_STEP = 2 /* Sec. 4.1 Eq. tv_loss averaged over steps: (1/K) sum_k (1 - alpha_k) */
@@ -147,7 +159,7 @@ spec_status spec_verify(const void* target_logits, int64_t t_stride_b, int64_t t
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* Launch controls for spec_verify_ex (tests, benchmarks and tuning). */
-typedef enum {
+typedef enum SPEC_ENUM_INT {
   SPEC_PATH_AUTO = 0,        /* the library's choice (the chain on MI355X)        */
   SPEC_PATH_CHAIN = 1,       /* always the four-launch chain                        */
   SPEC_PATH_SINGLE_READ = 2  /* single read; SPEC_EUNSUPPORTED where it does not qualify */
@@ -357,7 +369,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* Columns of the per-step output of spec_diagnostics. */
-typedef enum {
+typedef enum SPEC_ENUM_INT {
   SPEC_DIAG_ENTROPY_TARGET = 0, /* H(p_i) in nats (Sec. 3.1)                               */
   SPEC_DIAG_ENTROPY_DRAFT = 1,  /* H(q_i) in nats                                           */
   SPEC_DIAG_MAX_P = 2,          /* max_v p_i(v) (Prop. to_entropy: >= exp(-H(p_i)))         */
@@ -401,7 +413,7 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
                              float* diag, int32_t* greedy_draft, int32_t* rs_preferred,
                              void* workspace, size_t workspace_bytes, void* stream);
 
-typedef enum {
+typedef enum SPEC_ENUM_INT {
   SPEC_KL_FORWARD = 0, /* sum_v p_v log(p_v / q_v)   (App. B)                     */
   SPEC_KL_CE = 1,      /* -sum_v p_v log q_v        (= H(p) + forward KL)         */
   SPEC_KL_REVERSE = 2  /* sum_v q_v log(q_v / p_v)   (App. C)                     */

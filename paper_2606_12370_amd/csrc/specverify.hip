@@ -192,9 +192,24 @@ DiagLayout diag_layout(int B, int K, int V, spec_dtype dt) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+// Both strides keep 16-byte vectors aligned (the products are taken modulo
+// 2^64, which leaves them unchanged modulo 16).
 bool rows_vec_aligned(const void* base, int64_t s0, int64_t s1, size_t esize) {
-  return aligned16(base) && ((s0 * static_cast<int64_t>(esize)) % 16 == 0) &&
-         ((s1 * static_cast<int64_t>(esize)) % 16 == 0);
+  return aligned16(base) && (static_cast<uint64_t>(s0) * esize) % 16 == 0 &&
+         (static_cast<uint64_t>(s1) * esize) % 16 == 0;
+}
+
+// The last byte a tensor of n0 x n1 rows of V elements (strides s0, s1 in
+// elements, both >= 0) occupies from base lies within the address space: the
+// kernels' 64-bit row offsets then never overflow.
+bool extent_ok(const void* base, int64_t n0, int64_t s0, int64_t n1, int64_t s1, int V, size_t esize) {
+  int64_t a, b, last, bytes;
+  if (__builtin_mul_overflow(n0 - 1, s0, &a) || __builtin_mul_overflow(n1 - 1, s1, &b) ||
+      __builtin_add_overflow(a, b, &last) || __builtin_add_overflow(last, static_cast<int64_t>(V), &last) ||
+      __builtin_mul_overflow(last, static_cast<int64_t>(esize), &bytes))
+    return false;
+  uintptr_t end;
+  return !__builtin_add_overflow(reinterpret_cast<uintptr_t>(base), static_cast<uintptr_t>(bytes), &end);
 }
 
 // Statistics per sub-chunk of every row, one wave per sub-chunk and four
@@ -484,6 +499,9 @@ spec_status prepare_verify(const void* target_logits, int64_t t_stride_b, int64_
   if (!verify_sizes_ok(B, K, V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
   if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!extent_ok(target_logits, B, t_stride_b, K + 1, t_stride_k, V, esize_of(dtype)) ||
+      !extent_ok(draft_logits, B, d_stride_b, K, d_stride_k, V, esize_of(dtype)))
+    return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
   const VerifyLayout L = verify_layout(B, K, V, dtype, gumbel);
   if (!workspace) return SPEC_EWORKSPACE;
@@ -682,6 +700,7 @@ spec_status spec_sample_gumbel(const void* logits, int64_t stride_r, spec_dtype 
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
   if (!rows_ok(R, V, dtype)) return SPEC_EINVAL;
   if (!logits || !tokens || stride_r < 0) return SPEC_EINVAL;
+  if (!extent_ok(logits, R, stride_r, 1, 0, V, esize_of(dtype))) return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar >= 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
   if (!workspace || workspace_bytes < spec_sample_gumbel_workspace_size(R, V, dtype)) return SPEC_EWORKSPACE;
   if (!aligned16(workspace)) return SPEC_EINVAL;
@@ -713,6 +732,9 @@ spec_status spec_tv_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   if (!tv_sizes_ok(N, K, V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_logits || !loss) return SPEC_EINVAL;
   if (t_stride_n < 0 || t_stride_k < 0 || d_stride_n < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!extent_ok(target_logits, N, t_stride_n, K, t_stride_k, V, esize_of(dtype)) ||
+      !extent_ok(draft_logits, N, d_stride_n, K, d_stride_k, V, esize_of(dtype)))
+    return SPEC_EINVAL;
   if (!(temperature > 0.f && std::isfinite(temperature))) return SPEC_EINVAL;
   if (mode != SPEC_TV_E2E && mode != SPEC_TV_PROD && mode != SPEC_TV_PER_STEP) return SPEC_EINVAL;
   if (!std::isfinite(scale)) return SPEC_EINVAL;
@@ -765,6 +787,7 @@ spec_status spec_verify_target_only(const void* target_logits, int64_t t_stride_
   if (B < 1 || K < 1 || !rows_sub_ok(int64_t{B} * (K + 1), V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_ids || !accept_len || !emitted_ids) return SPEC_EINVAL;
   if (t_stride_b < 0 || t_stride_k < 0) return SPEC_EINVAL;
+  if (!extent_ok(target_logits, B, t_stride_b, K + 1, t_stride_k, V, esize_of(dtype))) return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
   const ToLayout L = to_layout(B, K, V, dtype);
   if (!workspace || workspace_bytes < L.total) return SPEC_EWORKSPACE;
@@ -800,6 +823,7 @@ spec_status spec_sample(const void* logits, int64_t stride_r, spec_dtype dtype, 
   if (dtype != SPEC_F32 && dtype != SPEC_BF16) return SPEC_EUNSUPPORTED;
   if (!rows_sub_ok(R, V, dtype)) return SPEC_EINVAL;
   if (!logits || !tokens || stride_r < 0) return SPEC_EINVAL;
+  if (!extent_ok(logits, R, stride_r, 1, 0, V, esize_of(dtype))) return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar >= 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
   if (!workspace || workspace_bytes < sample_ws(R, V, dtype)) return SPEC_EWORKSPACE;
   if (!aligned16(workspace)) return SPEC_EINVAL;
@@ -837,6 +861,9 @@ spec_status spec_diagnostics(const void* target_logits, int64_t t_stride_b, int6
   if (B < 1 || K < 1 || !rows_sub_ok(int64_t{B} * 2 * K, V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_logits || !diag) return SPEC_EINVAL;
   if (t_stride_b < 0 || t_stride_k < 0 || d_stride_b < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!extent_ok(target_logits, B, t_stride_b, K, t_stride_k, V, esize_of(dtype)) ||
+      !extent_ok(draft_logits, B, d_stride_b, K, d_stride_k, V, esize_of(dtype)))
+    return SPEC_EINVAL;
   if (!temperature && !(temperature_scalar > 0.f && std::isfinite(temperature_scalar))) return SPEC_EINVAL;
   const DiagLayout L = diag_layout(B, K, V, dtype);
   if (!workspace || workspace_bytes < L.total) return SPEC_EWORKSPACE;
@@ -879,6 +906,9 @@ spec_status spec_kl_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   if (!tv_sizes_ok(N, K, V, dtype)) return SPEC_EINVAL;
   if (!target_logits || !draft_logits || !loss) return SPEC_EINVAL;
   if (t_stride_n < 0 || t_stride_k < 0 || d_stride_n < 0 || d_stride_k < 0) return SPEC_EINVAL;
+  if (!extent_ok(target_logits, N, t_stride_n, K, t_stride_k, V, esize_of(dtype)) ||
+      !extent_ok(draft_logits, N, d_stride_n, K, d_stride_k, V, esize_of(dtype)))
+    return SPEC_EINVAL;
   if (!(temperature > 0.f && std::isfinite(temperature))) return SPEC_EINVAL;
   if (kind != SPEC_KL_FORWARD && kind != SPEC_KL_CE && kind != SPEC_KL_REVERSE) return SPEC_EINVAL;
   if (!std::isfinite(scale)) return SPEC_EINVAL;

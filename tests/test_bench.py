@@ -97,4 +97,5 @@ def test_all_cores_baseline_on_a_tiny_batch():
     T = np.ones(B, np.float64)
     r = bench.cpu_baseline_all_cores((tgt, drf, ids, T), K, budget_s=0.3, workers=2)
     assert r["cores"] == 2 and r["kind"] == "oracle" and r["value"] > 0
+    assert r["host_cpus"] == os.cpu_count()
     assert int(r["sample"].split()[0]) >= B
