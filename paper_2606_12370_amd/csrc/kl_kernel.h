@@ -39,6 +39,8 @@
 // other elements instead.
 #pragma once
 
+#include <type_traits>
+
 #include "sv_device.h"
 
 namespace sv {
@@ -250,13 +252,54 @@ struct KlDelta {
   double c1;   // zmax_d - zmax_t
   double lam;  // lam_t - lam_d
   double s;
+  float c1f, lam_hi, lam_lo, sf;  // the same in float32 (lam = lam_hi + lam_lo)
 };
 __device__ __forceinline__ KlDelta kl_delta_ref(const KlNorm& t, const KlNorm& d, float s) {
   KlDelta r;
   r.c1 = static_cast<double>(d.zmax) - static_cast<double>(t.zmax);
   r.lam = t.lam - d.lam;
   r.s = static_cast<double>(s);
+  r.c1f = static_cast<float>(r.c1);
+  r.lam_hi = static_cast<float>(r.lam);
+  r.lam_lo = static_cast<float>(r.lam - static_cast<double>(r.lam_hi));
+  r.sf = s;
   return r;
+}
+
+// The log ratios of one element: dl = log2 q - log2 p and wf = dl without
+// the normaliser difference, ((z_d - z_t) - (zmax_d - zmax_t)) s.  Float32
+// logits take them in float64.  For bfloat16 logits the logit differences
+// are exact in float32 (or within one rounding when the two exponents lie
+// more than 16 apart), so one float32 product and the normaliser
+// difference in two floats leave an error of a few float32 roundings of
+// |wf|, far inside the bfloat16 tolerance.
+struct KlRatio {
+  float dl, wf;
+};
+template <class E>
+__device__ __forceinline__ KlRatio kl_ratio(float zt, float zd, const KlDelta& r) {
+  KlRatio o;
+  if constexpr (std::is_same<E, F32>::value) {
+    const double wd = kl_wdiff(zt, zd, r.c1, r.s);
+    o.dl = static_cast<float>(wd + r.lam);
+    o.wf = static_cast<float>(wd);
+  } else {
+    const float w0 = (zd - zt) - r.c1f;
+    o.wf = w0 * r.sf;
+    o.dl = fmaf(w0, r.sf, r.lam_hi) + r.lam_lo;
+  }
+  return o;
+}
+
+// |q - p| of one element from its probabilities and the accurate log ratio:
+// below |d| = 1/2 max(p, q) (1 - 2^-|d|) from the series (float32 logits:
+// terms to y^7; bfloat16 logits: to y^4), above it max - min, whose
+// rounding is then at most six times the two probabilities' own.
+template <class E>
+__device__ __forceinline__ float kl_absdiff(float mx, float mn, float d) {
+  constexpr int D = std::is_same<E, F32>::value ? 6 : 3;
+  const float ad = fabsf(d);
+  return ad < 0.5f ? mx * one_minus_exp2_neg_small<D>(ad) : mx - mn;
 }
 __device__ __forceinline__ float kl_delta(float zt, float zd, const KlDelta& r) {
   return static_cast<float>(fma((static_cast<double>(zd) - static_cast<double>(zt)) - r.c1, r.s, r.lam));
@@ -322,8 +365,8 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
           const float uu = fmaf(xd[j][k], s, -nd.M);
           const float e = __builtin_amdgcn_exp2f(tt);
           const float f = __builtin_amdgcn_exp2f(uu);
-          const double wd = kl_wdiff(xt[j][k], xd[j][k], dr.c1, dr.s);
-          const float dl = static_cast<float>(wd + dr.lam);
+          const KlRatio rk = kl_ratio<E>(xt[j][k], xd[j][k], dr);
+          const float dl = rk.dl;
           float term;
           if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
           else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
@@ -339,19 +382,25 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
           vf += f;
           vw += term;
           if (KIND != kKlReverse) {
-            // (q - p) scale / (K T) = sign(d) max(p, q) (1 - 2^-|d|) scale / (K T)
-            const float mx = fmaxf(e * nt.invD, f * nd.invD);
-            const float g = mx * one_minus_exp2_neg(fabsf(dl));
+            // (q - p) scale / (K T) = sign(d) |q - p| scale / (K T)
+            const float pe = e * nt.invD, qf = f * nd.invD;
+            const float mx = fmaxf(pe, qf);
+            const float g = kl_absdiff<E>(mx, fminf(pe, qf), dl);
             gv[k] = mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
             // the element holding both rows' largest logit: its q - p is formed
             // in kl_coef from x = sum of the others' 2^(b) - 2^(a), a and b
-            // their logits less the rows' largest, from the exact difference
+            // their logits less the rows' largest (float32 logits: from the
+            // exact difference; bfloat16 logits: the two terms' difference)
             const bool at_top = xt[j][k] == nt.zmax && xd[j][k] == nd.zmax;
             if (at_top) top = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV + k;
-            const float wf = static_cast<float>(wd);
-            const float mb = fmaxf(e * kt, f * kd);
-            const float xv = mb * one_minus_exp2_neg(fabsf(wf));
-            vx += (at_top || !(mb > 0.f)) ? 0.f : copysignf(xv, wf);
+            const float ea = e * kt, fb = f * kd;
+            if constexpr (std::is_same<E, F32>::value) {
+              const float mb = fmaxf(ea, fb);
+              const float xv = kl_absdiff<E>(mb, fminf(ea, fb), rk.wf);
+              vx += (at_top || !(mb > 0.f)) ? 0.f : copysignf(xv, rk.wf);
+            } else {
+              vx += at_top ? 0.f : fb - ea;
+            }
           }
         }
         se += static_cast<double>(ve);
@@ -478,8 +527,7 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
           const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
-          const double wd = kl_wdiff(xt[j][k], xd[j][k], dr.c1, dr.s);
-          const float dl = static_cast<float>(wd + dr.lam);
+          const float dl = kl_ratio<E>(xt[j][k], xd[j][k], dr).dl;
           const float tm = (single_top && xd[j][k] == nd.zmax) ? fmaf(dl, A.z, -A.w) : dl - A.y;
           gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
         }

@@ -459,19 +459,18 @@ __device__ __forceinline__ float overlap_term(float zt, float zd, float s, const
 
 // 1 - 2^-x for x >= 0: the series of -expm1(-y), y = x ln2, below x = 1/2
 // (degree 9, truncation below 3e-10 of the value), the exponential above.
-__device__ __forceinline__ float one_minus_exp2_neg(float x) {
+// 1 - 2^-x for 0 <= x < 1/2 from the series of 1 - e^-y, y = x ln 2 < 0.35,
+// with the terms up to y^(D+1): truncation below y^(D+1) / (D+2)! of the
+// value (D = 6: 6e-8, D = 3: 7e-6).
+template <int D>
+__device__ __forceinline__ float one_minus_exp2_neg_small(float x) {
   const float y = x * 0.69314718f;
-  float p = 1.f / 362880.f;
-  p = fmaf(p, -y, 1.f / 40320.f);
-  p = fmaf(p, -y, 1.f / 5040.f);
-  p = fmaf(p, -y, 1.f / 720.f);
-  p = fmaf(p, -y, 1.f / 120.f);
-  p = fmaf(p, -y, 1.f / 24.f);
-  p = fmaf(p, -y, 1.f / 6.f);
-  p = fmaf(p, -y, 0.5f);
-  p = fmaf(p, -y, 1.f);
-  const float small = y * p;
-  return x < 0.5f ? small : 1.f - __builtin_amdgcn_exp2f(-x);
+  constexpr float c[8] = {1.f, 0.5f, 1.f / 6.f, 1.f / 24.f, 1.f / 120.f, 1.f / 720.f, 1.f / 5040.f, 1.f / 40320.f};
+  static_assert(D >= 1 && D <= 7, "series length");
+  float p = c[D];
+#pragma unroll
+  for (int i = D - 1; i >= 0; --i) p = fmaf(p, -y, c[i]);
+  return y * p;
 }
 
 // Rows of a batch: target rows (b, i) for i < tper, then draft rows (b, i)

@@ -73,21 +73,34 @@ def test_determinism():
         assert torch.equal(x, y)
 
 
-def test_training_workload_sampled_positions():
-    """N=16384 positions x 3 steps x V=151936 (bf16), product-of-overlaps
-    loss.  Sampled positions against the oracle; the total loss against the
-    loss recomputed in float64 from the kernel's own per-step overlaps."""
+@pytest.fixture(scope="module")
+def training_inputs():
     cfg = W.CONFIGS["tv_bf16_n16384_k3_v151936"]
     d = W.tv_inputs_torch(cfg["N"], cfg["K"], cfg["V"], cfg["dtype"], cfg["seed"])
-    loss, ov, grad = binding.tv_loss_fwd_bwd(d["target"], d["draft"], 1.0, "prod", 1.0)
+    yield cfg, d
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode,scale", [("prod", 1.0), ("e2e", 1.0 / 16384), ("per_step", 0.5)])
+def test_training_workload_sampled_positions(training_inputs, mode, scale):
+    """N=16384 positions x 3 steps x V=151936 (bf16) in each loss mode: the
+    paper's multi-step loss (Eq. e2e_tv) with a mean over positions, the
+    product-of-overlaps loss and the per-step loss.  Sampled positions
+    (their overlaps and every gradient element of their 3 x 151936 draft
+    logits) against the oracle; the total loss against the loss recomputed in
+    float64 from the kernel's own per-step overlaps."""
+    cfg, d = training_inputs
+    loss, ov, grad = binding.tv_loss_fwd_bwd(d["target"], d["draft"], 1.0, mode, scale)
     torch.cuda.synchronize()
-    rng = np.random.default_rng(cfg["seed"])
+    rng = np.random.default_rng(cfg["seed"] + len(mode))
     pos = np.sort(rng.choice(cfg["N"], size=4, replace=False))
     pi = torch.as_tensor(pos, device="cuda")
+    sc = float(np.float32(scale))
     ref = oracle.tv_ref(host_logits(d["target"][pi], W.BF16), host_logits(d["draft"][pi], W.BF16), 1.0,
-                        MODES["prod"], 1.0)
+                        MODES[mode], sc)
     rep = compare_tv(loss, ov, grad, ref, W.BF16, positions=pos, loss_exact=False)
-    _, L = chain_factors(ov.cpu().numpy().astype(np.float64), MODES["prod"])
+    _, L = chain_factors(ov.cpu().numpy().astype(np.float64), MODES[mode])
     lg = float(loss.cpu().numpy()[0])
-    assert abs(lg - L.sum()) <= TOL[W.BF16] * abs(L.sum())
-    print("training workload", rep, "loss", lg)
+    assert abs(lg - sc * L.sum()) <= TOL[W.BF16] * abs(sc * L.sum())
+    print("training workload", mode, rep, "loss", lg)
