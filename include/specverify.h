@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPEC_VERSION 1
+#define SPEC_VERSION 2
 
 /* The enumerations below are int-sized.  C++ gives them int as their fixed
  * underlying type, so that any int a caller passes (a C program, a foreign
@@ -169,12 +169,17 @@ typedef struct {
   int groups; /* single read: number of workgroup groups (0 = chosen by the library;
                  more than the device holds at once selects the chain, or
                  SPEC_EUNSUPPORTED with SPEC_PATH_SINGLE_READ) */
+  int residual_shape; /* chain: how the second pass reads each row's residual step
+                         (0 = chosen by the library from B and V; 1 = one wave
+                         per sub-chunk; 2 = one workgroup per sub-chunk, the
+                         small-batch shape).  Every shape gives the same bits. */
 } spec_launch;
 
 /*
  * spec_verify_ex — spec_verify with explicit launch controls (NULL = the
  * defaults of spec_verify).  Same arguments, outputs and errors as
- * spec_verify; SPEC_EINVAL for an unknown path or negative group count.
+ * spec_verify; SPEC_EINVAL for an unknown path or residual shape, or a
+ * negative group count.
  */
 spec_status spec_verify_ex(const void* target_logits, int64_t t_stride_b, int64_t t_stride_k,
                            const void* draft_logits, int64_t d_stride_b, int64_t d_stride_k,

@@ -49,7 +49,10 @@ PATHS = {"auto": 0, "chain": 1, "single_read": 2}
 
 
 class SpecLaunch(ctypes.Structure):
-    _fields_ = [("path", ctypes.c_int), ("groups", ctypes.c_int)]
+    _fields_ = [("path", ctypes.c_int), ("groups", ctypes.c_int), ("residual_shape", ctypes.c_int)]
+
+
+RESIDUAL_SHAPES = {"auto": 0, "wave": 1, "workgroup": 2}
 
 
 VERIFY_EX_ARGTYPES = VERIFY_ARGTYPES + [ctypes.POINTER(SpecLaunch)]
@@ -221,11 +224,12 @@ def _check_ids(ids, B, K):
 
 def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offset=0,
            want_debug=False, want_overlap=True, ws=None, out=None, gumbel=False, path=None, groups=0,
-           noalloc=False):
+           noalloc=False, residual_shape=None):
     """Chain rejection-sampling verification (spec_verify, or with
     gumbel=True spec_verify_gumbel: the emitted token drawn by Gumbel-max).
-    path ("auto", "chain", "single_read") and groups select the launch
-    (spec_verify_ex); by default the library chooses.  noalloc=True calls
+    path ("auto", "chain", "single_read"), groups and residual_shape ("auto",
+    "wave", "workgroup") select the launch (spec_verify_ex); by default the
+    library chooses.  noalloc=True calls
     spec_verify_noalloc (the library's own scratch array, no workspace).
 
     target_logits [B, K+1, V], draft_logits [B, K, V] (bf16 or f32, same
@@ -268,7 +272,7 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
             out["logz_target"] = torch.empty((B, K + 1), dtype=torch.float32, device=dev)
             out["logz_draft"] = torch.empty((B, K), dtype=torch.float32, device=dev)
     if noalloc:
-        if gumbel or path is not None or groups:
+        if gumbel or path is not None or groups or residual_shape is not None:
             raise ValueError("spec_verify_noalloc takes no launch controls")
         st = lib.spec_verify_noalloc(
             _ptr(target_logits), target_logits.stride(0), target_logits.stride(1),
@@ -283,11 +287,12 @@ def verify(target_logits, draft_logits, draft_ids, temperature=1.0, seed=0, offs
     size_fn = lib.spec_verify_gumbel_workspace_size if gumbel else lib.spec_verify_workspace_size
     fn, name = (lib.spec_verify_gumbel, "spec_verify_gumbel") if gumbel else (lib.spec_verify, "spec_verify")
     extra = ()
-    if path is not None or groups:
+    if path is not None or groups or residual_shape is not None:
         if gumbel:
             raise ValueError("launch controls apply to spec_verify only")
         fn, name = lib.spec_verify_ex, "spec_verify_ex"
-        extra = (ctypes.byref(SpecLaunch(PATHS[path or "auto"], int(groups))),)
+        extra = (ctypes.byref(SpecLaunch(PATHS[path or "auto"], int(groups),
+                                         RESIDUAL_SHAPES[residual_shape or "auto"])),)
     need = int(size_fn(B, K, V, code))
     if need == 0:
         raise ValueError("unsupported verify shape B=%d K=%d V=%d" % (B, K, V))

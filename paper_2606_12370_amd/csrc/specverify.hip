@@ -38,6 +38,9 @@ constexpr int kStep = 4;
 // pass) or kDiagPairVec (diagnostics pair pass) vectors per lane at a time.
 constexpr int kStatVec = 8;
 constexpr int kPairVec = 4;
+// Pair-pass items below which each one gets a workgroup (the small-batch
+// launch shape).
+constexpr int64_t kSharedItems = 4096;
 constexpr int kDiagPairVec = 2;
 constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
@@ -336,14 +339,20 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, 
   // statistics and pair sums per sub-chunk of kStep tiles, one wave per sub-chunk
   launch_stats_wave<E>(a.rows, const_cast<sv::RowStat*>(a.stats), rows, s);
   hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
-  // one workgroup per four (pair, sub-chunk) items: measured faster than a
-  // grid of what the device holds at once striding over them (73.6 against
-  // 75.0 us at B=256, K=3, V=151936 bf16); without overlaps only each batch
-  // row's residual step is read again
+  // pair pass: without overlaps only each batch row's residual step is read
+  // again.  One wave per item, four per workgroup (measured faster than a
+  // grid of what the device holds at once striding over them), or one
+  // workgroup per item where that measured faster: calls without overlaps
+  // (B = 32..256, K = 3, V = 151936 bf16: 42.1 against 50.8 us at B = 32,
+  // 54.0 against 63.5 at B = 64, 135.3 against 136.8 at B = 256) and calls
+  // with fewer than kSharedItems items (47.8 against 53.2 us at B = 32, 70.1
+  // against 71.5 at B = 64; 113.2 against 107.9 at B = 128)
   const int64_t items = int64_t{a.B} * (a.overlap ? a.K : 1) * a.rows.C;
-  hipLaunchKernelGGL((sv::pair_pass_wave_kernel<E, kStep, kPairVec>),
-                     dim3(static_cast<unsigned>((items + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s, a,
-                     items);
+  const int shape = lc ? lc->residual_shape : 0;
+  const int split = shape == 2 || (shape == 0 && (items < kSharedItems || a.overlap == nullptr)) ? 1 : 0;
+  const int64_t wgs = split ? items : (items + sv::kWaves - 1) / sv::kWaves;
+  hipLaunchKernelGGL((sv::pair_pass_wave_kernel<E, kStep, kPairVec>), dim3(static_cast<unsigned>(wgs)),
+                     dim3(sv::kThreads), 0, s, a, items, split);
   // the finish inverts the CDF inside one sub-chunk (kStep tiles, one load step)
   hipLaunchKernelGGL((sv::finish_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
                      s, a);
@@ -615,7 +624,8 @@ spec_status spec_verify_ex(const void* target_logits, int64_t t_stride_b, int64_
                            uint64_t offset, int32_t* accept_len, int32_t* emitted_ids, float* overlap,
                            float* p_at_draft, float* q_at_draft, float* logz_target, float* logz_draft,
                            void* workspace, size_t workspace_bytes, void* stream, const spec_launch* launch) {
-  if (launch && (launch->path < SPEC_PATH_AUTO || launch->path > SPEC_PATH_SINGLE_READ || launch->groups < 0))
+  if (launch && (launch->path < SPEC_PATH_AUTO || launch->path > SPEC_PATH_SINGLE_READ || launch->groups < 0 ||
+                 launch->residual_shape < 0 || launch->residual_shape > 2))
     return SPEC_EINVAL;
   sv::VerifyArgs a;
   sv::GumbelBest* gb;

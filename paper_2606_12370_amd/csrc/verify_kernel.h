@@ -299,79 +299,77 @@ __global__ __launch_bounds__(kThreads) void pair_pass_kernel(VerifyArgs a, int64
   }
 }
 
-// The pair-pass sums of one wave over load steps st0 .. st1-1 of the sub-chunk
-// at element e0: the overlap, and for the residual step the residual sums.
-struct PairSums {
-  float al = 0.f, zp = 0.f, sd = 0.f, qg = 0.f;
+// The pair-pass sums of one lane over one load step (S vectors of each row
+// at element es): the overlap, and for the residual step the residual sums,
+// in float32.
+struct StepSums {
+  float v[4];  // overlap, residual mass, sum of p - q, sum over p > q of q
 };
 
 template <class E, int S>
-__device__ __forceinline__ void pair_span_sums(const typename E::raw* rt, const typename E::raw* rd, bool al_t,
-                                               bool al_d, int e0, int st0, int st1, int lane, int V, float s,
-                                               const RowNorm& nt, const RowNorm& nd, bool need_z, PairSums& o) {
+__device__ __forceinline__ StepSums pair_step_sums(const typename E::raw* rt, const typename E::raw* rd, bool al_t,
+                                                   bool al_d, int es, int lane, int V, float s, const RowNorm& nt,
+                                                   const RowNorm& nd, bool need_z, const ResidualRef& rr, float rft,
+                                                   float rfd) {
   constexpr int EPV = E::EPV;
+  StepSums o = {{0.f, 0.f, 0.f, 0.f}};
+  float xt[S][EPV], xd[S][EPV];
+  load_span<E, S, 64>(rt, es, lane, V, al_t, xt);
+  load_span<E, S, 64>(rd, es, lane, V, al_d, xd);
   if (need_z) {
-    const ResidualRef rr = residual_ref(nt, nd, 0.0);
-    // (a loop that is not unrolled, so that its longer body does not multiply
-    // the code size)
-#pragma unroll 1
-    for (int st = st0; st < st1; ++st) {
-      const int es = e0 + st * S * 64 * EPV;
-      if (es >= V) break;  // wave-uniform: the row's last sub-chunk may be short
-      float xt[S][EPV], xd[S][EPV];
-      load_span<E, S, 64>(rt, es, lane, V, al_t, xt);
-      load_span<E, S, 64>(rd, es, lane, V, al_d, xd);
 #pragma unroll
-      for (int q = 0; q < S; ++q)
+    for (int q = 0; q < S; ++q)
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          const ElemPQ e = elem_pq(xt[q][k], xd[q][k], s, nt, nd, rr);
-          o.al += e.mn;
-          o.zp += e.pos ? e.g : 0.f;
-          o.sd += e.diff();
-          o.qg += e.pos ? e.mn : 0.f;
-        }
-    }
+      for (int k = 0; k < EPV; ++k) {
+        const ElemPQ e = elem_pq(xt[q][k], xd[q][k], s, nt, nd, rr);
+        o.v[0] += e.mn;
+        o.v[1] += e.pos ? e.g : 0.f;
+        o.v[2] += e.diff();
+        o.v[3] += e.pos ? e.mn : 0.f;
+      }
   } else {
-    const float rft = static_cast<float>(static_cast<double>(nt.M) + static_cast<double>(nt.L));
-    const float rfd = static_cast<float>(static_cast<double>(nd.M) + static_cast<double>(nd.L));
 #pragma unroll
-    for (int st = st0; st < st1; ++st) {
-      const int es = e0 + st * S * 64 * EPV;
-      if (es >= V) break;  // wave-uniform: the row's last sub-chunk may be short
-      float xt[S][EPV], xd[S][EPV];
-      load_span<E, S, 64>(rt, es, lane, V, al_t, xt);
-      load_span<E, S, 64>(rd, es, lane, V, al_d, xd);
+    for (int q = 0; q < S; ++q)
 #pragma unroll
-      for (int q = 0; q < S; ++q)
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) o.al += overlap_term<E>(xt[q][k], xd[q][k], s, nt, nd, rft, rfd);
-    }
+      for (int k = 0; k < EPV; ++k) o.v[0] += overlap_term<E>(xt[q][k], xd[q][k], s, nt, nd, rft, rfd);
   }
+  return o;
 }
 
-// Pass 2 with one wave per (pair, sub-chunk) item.  Sub-chunk j covers ST
-// tiles of 256 vectors (ST * 4 vectors of the wave's 64 lanes), read S vectors
-// per lane and load step, then one float64 wave sum per quantity: no LDS and
-// no barrier.  Items are ordered longest first: items 0 .. B*C-1 are the
-// sub-chunks of each batch row's residual step (its first rejected step, or
-// step K-1 of a row that accepts every draft), the B*(K-1)*C items after them
-// the row's other steps (item (b*(K-1) + m)*C + j is sub-chunk j of the m-th
-// of row b's other steps).  A residual item costs about three times an
-// overlap item, and taking those first keeps them from piling up on a few
-// SIMDs at the end of the launch.  Without overlaps only the first B*C items
-// are launched.  kWaves items per workgroup.
+// Pass 2 over (pair, sub-chunk) items.  Sub-chunk j covers ST tiles of 256
+// vectors (ST * 4 vectors per lane of one wave), read in NS load steps of S
+// vectors per lane.  Every item's sums are formed the same way, whichever
+// launch shape runs it: per lane and load step in float32, per lane over the
+// load steps in float64 (in step order), then one float64 sum over the
+// wave's lanes.
+//
+// Items 0 .. B*C-1 are the sub-chunks of each batch row's residual step (its
+// first rejected step, or step K-1 of a row that accepts every draft), the
+// B*(K-1)*C items after them the rows' other steps (item (b*(K-1) + m)*C + j
+// is sub-chunk j of the m-th of row b's other steps).  A residual item costs
+// about three times an overlap item, so these come first in the launch.
+// Two launch shapes:
+//  - split == 0: one wave per item, kWaves items per workgroup;
+//  - split == 1 (small batches, where one wave per item leaves the device
+//    with too few loads in flight and the residual items' serial latency
+//    bounds the launch): one workgroup per item, its kWaves waves sharing
+//    the item's load steps and handing their per-lane step sums to wave 0
+//    through LDS.
+// Without overlaps only the residual-step items are launched.
 template <class E, int ST, int S>
-__global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, int64_t nitems) {
+__global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, int64_t nitems, int split) {
   constexpr int EPV = E::EPV;
   constexpr int WV = ST * (kThreads / 64);
-  static_assert(WV % S == 0, "whole load steps per sub-chunk");
+  constexpr int NS = WV / S;  // load steps per sub-chunk
+  static_assert(WV % S == 0 && NS % kWaves == 0, "whole load steps per sub-chunk and wave");
+  __shared__ float part[NS][4][64];
   const RowsDesc& d = a.rows;
   const int C = d.C;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
-  if (g >= nitems) return;
   const int64_t first = static_cast<int64_t>(a.B) * C;
+  const bool shared_item = split != 0;
+  const int64_t g = shared_item ? static_cast<int64_t>(blockIdx.x) : static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  if (g >= nitems) return;  // (uniform over a workgroup that shares its item)
   int b, j, m = 0;
   if (g < first) {
     b = static_cast<int>(g / C);
@@ -383,6 +381,8 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
     m = r / C;
     j = r - m * C;
   }
+  // (uniform over a workgroup that shares its item, so the returns below
+  // leave its barrier to all of its waves or to none)
   const int n = a.decision[b];
   if (n < 0) return;  // data error: finish ignores this row's partials
   const bool rejects = a.want_z && n < a.K;
@@ -397,14 +397,54 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
   const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
   const float s = scale_of(temperature_of(d, b));
   const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-  PairSums o;
-  pair_span_sums<E, S>(rt, rd, al_t, al_d, j * WV * 64 * EPV, 0, WV / S, lane, d.V, s, nt, nd, need_z, o);
-  PairStat ps;
-  ps.alpha = wave_sum(static_cast<double>(o.al));
-  ps.Z = need_z ? wave_sum(static_cast<double>(o.zp)) : 0.0;
-  ps.Sd = need_z ? wave_sum(static_cast<double>(o.sd)) : 0.0;
-  ps.Qg = need_z ? wave_sum(static_cast<double>(o.qg)) : 0.0;
-  if (lane == 0) a.pairs[(static_cast<int64_t>(b) * a.K + i) * C + j] = ps;
+  const ResidualRef rr = need_z ? residual_ref(nt, nd, 0.0) : kNoResidual;
+  const float rft = static_cast<float>(static_cast<double>(nt.M) + static_cast<double>(nt.L));
+  const float rfd = static_cast<float>(static_cast<double>(nd.M) + static_cast<double>(nd.L));
+  const int e0 = j * WV * 64 * EPV;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  if (shared_item) {
+    constexpr int NW = NS / kWaves;
+#pragma unroll 1
+    for (int st = wave * NW; st < (wave + 1) * NW; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      StepSums ps = {{0.f, 0.f, 0.f, 0.f}};
+      if (es < d.V) ps = pair_step_sums<E, S>(rt, rd, al_t, al_d, es, lane, d.V, s, nt, nd, need_z, rr, rft, rfd);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) part[st][q][lane] = ps.v[q];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    // (a step beyond the row adds +0, as the one-wave shape skips it)
+#pragma unroll
+    for (int st = 0; st < NS; ++st)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] += static_cast<double>(part[st][q][lane]);
+  } else if (need_z) {
+    // (a loop that is not unrolled, so that its longer body does not
+    // multiply the code size)
+#pragma unroll 1
+    for (int st = 0; st < NS; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+      const StepSums ps = pair_step_sums<E, S>(rt, rd, al_t, al_d, es, lane, d.V, s, nt, nd, true, rr, rft, rfd);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] += static_cast<double>(ps.v[q]);
+    }
+  } else {
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+      const StepSums ps = pair_step_sums<E, S>(rt, rd, al_t, al_d, es, lane, d.V, s, nt, nd, false, rr, rft, rfd);
+      acc[0] += static_cast<double>(ps.v[0]);
+    }
+  }
+  PairStat o;
+  o.alpha = wave_sum(acc[0]);
+  o.Z = need_z ? wave_sum(acc[1]) : 0.0;
+  o.Sd = need_z ? wave_sum(acc[2]) : 0.0;
+  o.Qg = need_z ? wave_sum(acc[3]) : 0.0;
+  if (lane == 0) a.pairs[(static_cast<int64_t>(b) * a.K + i) * C + j] = o;
 }
 
 // Residual (or target) mass of the EPV elements of one thread's vector;

@@ -108,12 +108,15 @@ int main() {
                      int64_t{1} << 31, P, SIZE_MAX));
   EXPECT_FAIL(verify(B, K, INT_MAX, SPEC_F32, INT64_MAX / 8, INT64_MAX / 64, 3000, 1000, P, SIZE_MAX));
   // launch controls
-  spec_launch bad = {5, 0}, neg = {SPEC_PATH_CHAIN, -1};
+  spec_launch bad = {5, 0, 0}, neg = {SPEC_PATH_CHAIN, -1, 0}, shape = {SPEC_PATH_CHAIN, 0, 7};
   EXPECT(spec_verify_ex(P, 4000, 1000, P, 3000, 1000, SPEC_BF16, B, K, V, Ids, nullptr, 1.f, 1, 2, Out, Out, F, F, F,
                         F, F, P, need, nullptr, &bad),
          SPEC_EINVAL);
   EXPECT(spec_verify_ex(P, 4000, 1000, P, 3000, 1000, SPEC_BF16, B, K, V, Ids, nullptr, 1.f, 1, 2, Out, Out, F, F, F,
                         F, F, P, need, nullptr, &neg),
+         SPEC_EINVAL);
+  EXPECT(spec_verify_ex(P, 4000, 1000, P, 3000, 1000, SPEC_BF16, B, K, V, Ids, nullptr, 1.f, 1, 2, Out, Out, F, F, F,
+                        F, F, P, need, nullptr, &shape),
          SPEC_EINVAL);
   // the entry point without a workspace: beyond its array, and argument errors
   EXPECT(spec_verify_noalloc(P, int64_t{262144} * 4, 262144, P, int64_t{262144} * 3, 262144, SPEC_BF16, 65536, 3,

@@ -169,12 +169,12 @@ def test_verify_argument_errors(lib, kw, status):
     assert call_verify(lib, **kw) == status
 
 
-def call_verify_ex(lib, path, groups, **kw):
+def call_verify_ex(lib, path, groups, shape=0, **kw):
     args = dict(t=FAKE, tsb=400, tsk=100, d=FAKE, dsb=300, dsk=100, dtype=1, B=4, K=3, V=100, ids=FAKE,
                 temp=None, temp_s=1.0, seed=0, off=0, acc=FAKE, em=FAKE, ov=None, p=None, q=None,
                 lzt=None, lzd=None, ws=FAKE, wsb=1 << 30, stream=None)
     args.update(kw)
-    lc = binding.SpecLaunch(path, groups)
+    lc = binding.SpecLaunch(path, groups, shape)
     return lib.spec_verify_ex(*[args[k] for k in ("t", "tsb", "tsk", "d", "dsb", "dsk", "dtype", "B", "K", "V", "ids",
                                                   "temp", "temp_s", "seed", "off", "acc", "em", "ov", "p", "q", "lzt",
                                                   "lzd", "ws", "wsb", "stream")], ctypes.byref(lc))
@@ -188,6 +188,8 @@ def call_verify_ex(lib, path, groups, **kw):
     (1, 0, dict(B=0), 1),
     (2, 4, dict(ws=None), 4),
     (0, 0, dict(temp_s=0.0), 1),
+    (1, 0, dict(shape=3), 1),
+    (1, 0, dict(shape=-1), 1),
 ])
 def test_verify_ex_argument_errors(lib, path, groups, kw, status):
     assert call_verify_ex(lib, path, groups, **kw) == status

@@ -287,6 +287,34 @@ def test_launch_shape_independence(dtype, B, K, V):
     print(dtype, B, K, V, "chain and single read give the same tokens:", same, rep)
 
 
+@pytest.mark.parametrize("dtype,B,K,V,recipe", [(W.BF16, 64, 3, 151936, "rollout_t"), (W.F32, 7, 2, 50000, "near"),
+                                                (W.BF16, 300, 3, 20000, "near"), (W.BF16, 5, 1, 8200, "rollout_t"),
+                                                (W.F32, 33, 4, 16385, "rollout_t")])
+def test_residual_shapes_give_identical_bits(dtype, B, K, V, recipe):
+    """The chain's pair pass reads each row's residual step with one wave or
+    one workgroup per sub-chunk (the small-batch shape), or as the library
+    chooses: every output is bit-identical across the three, with and
+    without overlaps, and the rows match the oracle."""
+    d = W.verify_inputs_numpy(B, K, V, dtype, recipe, 300 + B)
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    for want_ov in (True, False):
+        outs = {}
+        for shape in ("wave", "workgroup", "auto"):
+            outs[shape] = binding.verify(tgt, drf, ids, T, 11, 4, want_debug=True, want_overlap=want_ov,
+                                         path="chain", residual_shape=shape)
+        torch.cuda.synchronize()
+        for shape in ("workgroup", "auto"):
+            for key in outs["wave"]:
+                assert torch.equal(outs[shape][key], outs["wave"][key]), (shape, key, want_ov)
+    ref = oracle.verify_ref(W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype), d["ids"],
+                            d["temperature"].astype(np.float64), 11, 4)
+    out = binding.verify(tgt, drf, ids, T, 11, 4, want_debug=True, residual_shape="workgroup")
+    torch.cuda.synchronize()
+    print(dtype, B, K, V, recipe, compare_verify(out, ref, dtype))
+
+
 def test_single_read_unsupported_shapes_fall_back_or_refuse():
     """K = 8 (beyond the single-read path): the automatic launch takes the
     chain and matches the oracle; asking for the single-read path refuses."""
