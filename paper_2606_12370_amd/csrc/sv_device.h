@@ -403,7 +403,7 @@ struct RowNorm {
   float M;      // log2 units; +inf / NaN / -inf mark a bad row
   float invD;   // 1 / D rounded once
   float L;      // log2(D) rounded once
-  float pad;
+  float Llo;    // log2(D) - L, so that L + Llo carries log2(D) to about 2^-48
   double D;
 };
 
@@ -411,8 +411,9 @@ __device__ __forceinline__ RowNorm make_norm(float M, double D) {
   RowNorm n;
   n.M = M;
   n.invD = static_cast<float>(1.0 / D);
-  n.L = static_cast<float>(log2(D));
-  n.pad = 0.f;
+  const double l2 = log2(D);
+  n.L = static_cast<float>(l2);
+  n.Llo = (l2 - l2 == 0.0) ? static_cast<float>(l2 - static_cast<double>(n.L)) : 0.f;  // 0 for D = 0 or inf
   n.D = D;
   return n;
 }

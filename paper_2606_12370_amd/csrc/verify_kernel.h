@@ -52,7 +52,9 @@ struct ResidualRef {
 };
 
 __device__ __forceinline__ ResidualRef residual_ref(const RowNorm& t, const RowNorm& d, double w) {
-  const double c = (static_cast<double>(t.M) - static_cast<double>(d.M)) + (log2(t.D) - log2(d.D));
+  const double c = (static_cast<double>(t.M) - static_cast<double>(d.M)) +
+                   ((static_cast<double>(t.L) - static_cast<double>(d.L)) +
+                    (static_cast<double>(t.Llo) - static_cast<double>(d.Llo)));
   ResidualRef r;
   r.ch = static_cast<float>(c);
   r.cl = static_cast<float>(c - static_cast<double>(r.ch));
@@ -730,7 +732,8 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
     for (int i = 0; i < SPEC_MAX_K_DEV; ++i)
       if (i == n) p0 = ppre[i];
     // the row's totals at the rejected step, and its normalisation correction
-    double w = 0.0, zs = 0.0;
+    double w = 0.0;
+    bool any_residual = false;
     if (n < K) {
       double za = 0.0, zd = 0.0, zal = 0.0;
       for (int cc = lane; cc < C; cc += 64) {
@@ -742,14 +745,15 @@ __global__ __launch_bounds__(kThreads) void finish_kernel(VerifyArgs a) {
       zal = wave_sum(zal);
       w = zd / (zal + za);
       if (!(w == w)) w = 0.0;
+      bool pos = false;
       for (int cc = lane; cc < C; cc += 64) {
         const PairStat q = cc < 64 ? p0 : ps[cc];
-        zs += corrected_mass(q.Z, q.Qg, w);
+        pos = pos || corrected_mass(q.Z, q.Qg, w) > 0.0;
       }
-      zs = wave_sum(zs);
+      any_residual = __ballot(pos) != 0;
     }
     // residual of the rejected step; p_n itself for the bonus row or an empty residual
-    const bool residual = n < K && zs > 0.0;
+    const bool residual = n < K && any_residual;
     const RowStat* st = a.stats + static_cast<int64_t>(target_row(a, b, n)) * C;
     const float nnM = __shfl(nM, n, 64);
     const double nnD = __shfl(nD, n, 64);
