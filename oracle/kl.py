@@ -21,12 +21,23 @@ objective, as for the per-step TV loss); the paper derives the gradients at
 T = 1 and the 1/T factor of softmax(z / T) is included here.
 
 Precision: the gradients are differences of probabilities (q - p) and of
-log-probabilities (log q - log p - L).  Where one token holds all but 1e-10
+log-probabilities (log q - log p - L).  Where one token holds all but 1e-14
 of both distributions, q - p of that token is a difference of two numbers
-within 1e-10 of 1, and float64 keeps only about six of its digits.  The
-softmax, the differences and the sums are therefore evaluated in extended
-precision (numpy.longdouble, a 64-bit significand on x86-64), then returned
-as float64.
+within 1e-14 of 1; where two tokens share the mass of two nearly equal
+distributions, log q - log p of each is the small difference of two log
+partition functions.  So every quantity is evaluated in extended precision
+(numpy.longdouble, a 64-bit significand on x86-64), and the log ratio of one
+element is formed without subtracting two separately rounded log partition
+functions:
+
+  log q_v - log p_v = w_v - log(1 + X / Z_t'),  w_v = ((zd_v - zt_v) - (max zd - max zt)) / T,
+  Z_t' = sum_v e^(zt_v / T - max zt / T),  X = Z_d' - Z_t' = sum_v e^(zt_v / T - max zt / T) (e^(w_v) - 1),
+
+with e^w - 1 and log(1 + x) evaluated by expm1 and log1p, and
+q - p = p (e^(log q - log p) - 1).  For reverse KL the draft's single
+largest element takes log q - log p - L as sum over the other elements u of
+q_u (d - d_u), d = log q - log p (the q_u sum to 1), which keeps it accurate
+where that element holds nearly all of q.  Results are returned as float64.
 """
 
 import numpy as np
@@ -59,19 +70,60 @@ def kl_ref(target_logits, draft_logits, temperature, kind, scale=1.0):
     lq = log_softmax_t(zd, T)
     p = np.exp(lp)
     q = np.exp(lq)
+    dl = log_ratio(zt, zd, T)  # log q - log p
     with np.errstate(invalid="ignore"):
+        # q - p: p (e^dl - 1) where p > 0 (dl = -inf gives -p), q where p = 0
+        qmp = np.where(p > 0, p * np.expm1(dl), q)
         if kind == KIND_FORWARD:
-            L = np.where(p > 0, p * (lp - lq), XP(0)).sum(axis=-1)
-            g = (q - p) / T
+            L = np.where(p > 0, -p * dl, XP(0)).sum(axis=-1)
+            g = qmp / T
         elif kind == KIND_CE:
             L = np.where(p > 0, -p * lq, XP(0)).sum(axis=-1)
-            g = (q - p) / T
+            g = qmp / T
         elif kind == KIND_REVERSE:
-            L = np.where(q > 0, q * (lq - lp), XP(0)).sum(axis=-1)
-            g = np.where(q > 0, q * (lq - lp - L[..., None]), XP(0)) / T
+            qdl = np.where(q > 0, q * dl, XP(0))
+            L = qdl.sum(axis=-1)
+            g = np.where(q > 0, q * (dl - L[..., None]), XP(0))
+            # the draft's single largest element: dl - L = sum over the other
+            # elements u of q_u (dl - dl_u) (the q_u sum to 1), which does
+            # not cancel when that element holds nearly all of q
+            top = np.argmax(zd, axis=-1)[..., None]
+            single = (zd == np.max(zd, axis=-1, keepdims=True)).sum(axis=-1, keepdims=True) == 1
+            dl_top = np.take_along_axis(dl, top, axis=-1)
+            q_top = np.take_along_axis(q, top, axis=-1)
+            others = np.ones(zd.shape, dtype=bool)
+            np.put_along_axis(others, top, False, axis=-1)
+            comp = np.where(others & (q > 0), q * (dl_top - dl), XP(0)).sum(axis=-1, keepdims=True)
+            g_top = np.where(single & np.isfinite(dl_top), q_top * comp, np.take_along_axis(g, top, axis=-1))
+            np.put_along_axis(g, top, g_top, axis=-1)
+            g = g / T
         else:
             raise ValueError(kind)
     loss_pos = L.mean(axis=1)
     sc = XP(float(scale))
     return {"per_step": L.astype(np.float64), "loss": float(sc * loss_pos.sum()),
             "loss_pos": (sc * loss_pos).astype(np.float64), "grad": (g * (sc / K)).astype(np.float64)}
+
+
+def log_ratio(target_logits, draft_logits, T):
+    """log q_v - log p_v along the last axis in extended precision, from the
+    exact logit differences and the pairwise difference X = Z_d' - Z_t' of
+    the two partition sums taken relative to each row's largest logit (see
+    the module docstring).  Elements whose p or q is zero get -inf / +inf
+    (both zero: NaN, never used)."""
+    zt = np.asarray(target_logits, dtype=XP)
+    zd = np.asarray(draft_logits, dtype=XP)
+    T = XP(T)
+    mt = np.max(zt, axis=-1, keepdims=True)
+    md = np.max(zd, axis=-1, keepdims=True)
+    with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
+        ea = np.exp((zt - mt) / T)
+        eb = np.exp((zd - md) / T)
+        w = ((zd - zt) - (md - mt)) / T
+        both = (ea > 0) & (eb > 0)
+        # e^(b') - e^(a') per element: ea (e^w - 1) where both are non-zero,
+        # else the one non-zero term
+        diff = np.where(both, ea * np.expm1(np.where(both, w, XP(0))), eb - ea)
+        X = diff.sum(axis=-1, keepdims=True)
+        Zt = ea.sum(axis=-1, keepdims=True)
+        return np.where(both, w - np.log1p(X / Zt), np.log(eb) - np.log(ea) - np.log1p(X / Zt))
