@@ -75,9 +75,7 @@ struct KlNorm {
 struct KlPart {  // one chunk of a (position, step) pair
   double se, sf, w;
   double sfx, wx, wm;  // reverse KL: sum f, sum f d over the non-largest draft elements; sum f d over the largest
-  double x;            // forward KL / CE: sum over the other elements of 2^(b) - 2^(a) (see kl_pass)
-  int top;             // index of the element holding both rows' largest logit, or -1
-  int pad;
+  double x;            // forward KL / CE: Z_d' - Z_t', the sum of 2^(b) - 2^(a) (see kl_pass)
 };
 
 struct KlArgs {
@@ -90,7 +88,7 @@ struct KlArgs {
   int SC;                // sub-chunks per row of the statistics pass
   KlNorm* norms;         // [2 N K]
   KlPart* parts;         // [N K][C]
-  float4* coef;          // [N K]: reverse-KL gradient constants
+  float4* coef;          // [N K]: gradient constants (reverse KL), or lam_t - lam_d as hi + lo (forward KL, CE)
   double* loss_pos;      // [N]
   int vec_g;
 };
@@ -254,6 +252,11 @@ struct KlDelta {
   double s;
   float c1f, lam_hi, lam_lo, sf;  // the same in float32 (lam = lam_hi + lam_lo)
 };
+__device__ __forceinline__ void kl_delta_set_lam(KlDelta& r, double lam) {
+  r.lam = lam;
+  r.lam_hi = static_cast<float>(lam);
+  r.lam_lo = static_cast<float>(lam - static_cast<double>(r.lam_hi));
+}
 __device__ __forceinline__ KlDelta kl_delta_ref(const KlNorm& t, const KlNorm& d, float s) {
   KlDelta r;
   r.c1 = static_cast<double>(d.zmax) - static_cast<double>(t.zmax);
@@ -326,11 +329,8 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   __shared__ RedLds<6> red;
-  __shared__ RedLds<1> red1;
   const RowsDesc& d = a.rows;
   const int C = d.C, V = d.V, NK = a.N * a.K;
-  const bool write_grad = a.grad != nullptr && KIND != kKlReverse;
-  const float gcoef = static_cast<float>(a.scale * static_cast<double>(a.inv_t) / a.K);
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
     const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
     int bb;
@@ -340,11 +340,9 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
     const float s = scale_of(d.temp_scalar);
     const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
     const KlDelta dr = kl_delta_ref(nt, nd, s);
-    float* gr = write_grad ? a.grad + static_cast<int64_t>(u) * V : nullptr;
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
     double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0, xs = 0.0;
-    int top = -1;
     // 2^(z s - zmax s) = e 2^(M - zmax s): the scale of each row's elements against its largest
     const float kt = static_cast<float>(exp2(static_cast<double>(nt.M) - static_cast<double>(nt.zmax) * dr.s));
     const float kd = static_cast<float>(exp2(static_cast<double>(nd.M) - static_cast<double>(nd.zmax) * dr.s));
@@ -356,7 +354,6 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
       load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
 #pragma unroll
       for (int j = 0; j < S; ++j) {
-        float gv[EPV];
         // the EPV elements of one vector are summed in float32, vectors in float64
         float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f, vx = 0.f;
 #pragma unroll
@@ -382,25 +379,14 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
           vf += f;
           vw += term;
           if (KIND != kKlReverse) {
-            // (q - p) scale / (K T) = sign(d) |q - p| scale / (K T)
-            const float pe = e * nt.invD, qf = f * nd.invD;
-            const float mx = fmaxf(pe, qf);
-            const float g = kl_absdiff<E>(mx, fminf(pe, qf), dl);
-            gv[k] = mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
-            // the element holding both rows' largest logit: its q - p is formed
-            // in kl_coef from x = sum of the others' 2^(b) - 2^(a), a and b
-            // their logits less the rows' largest (float32 logits: from the
-            // exact difference; bfloat16 logits: the two terms' difference)
-            const bool at_top = xt[j][k] == nt.zmax && xd[j][k] == nd.zmax;
-            if (at_top) top = (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV + k;
+            // x = Z_d' - Z_t' from every element's 2^(b) - 2^(a), a and b its
+            // logits less the rows' largest (Z' = sum 2^(.)), each formed
+            // from the exact log ratio wf: kl_coef turns it into the log ratio
+            // of the two partition functions that the gradient pass uses
             const float ea = e * kt, fb = f * kd;
-            if constexpr (std::is_same<E, F32>::value) {
-              const float mb = fmaxf(ea, fb);
-              const float xv = kl_absdiff<E>(mb, fminf(ea, fb), rk.wf);
-              vx += (at_top || !(mb > 0.f)) ? 0.f : copysignf(xv, rk.wf);
-            } else {
-              vx += at_top ? 0.f : fb - ea;
-            }
+            const float mb = fmaxf(ea, fb);
+            const float xv = kl_absdiff<E>(mb, fminf(ea, fb), rk.wf);
+            vx += mb > 0.f ? copysignf(xv, rk.wf) : 0.f;
           }
         }
         se += static_cast<double>(ve);
@@ -413,21 +399,16 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
         } else {
           xs += static_cast<double>(vx);
         }
-        if (write_grad)
-          store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }
     }
     double v[6] = {se, sf, w, KIND == kKlReverse ? sfx : xs, wx, wm};
     wg_sum<6>(v, red);
-    const int tp = -wg_min_int(-top, red1);  // the largest index holding the top (at most one unless tied)
     if (threadIdx.x == 0) {
       KlPart o;
       o.se = v[0]; o.sf = v[1]; o.w = v[2];
       o.sfx = KIND == kKlReverse ? v[3] : 0.0;
       o.wx = v[4]; o.wm = v[5];
       o.x = KIND == kKlReverse ? 0.0 : v[3];
-      o.top = tp;
-      o.pad = 0;
       a.parts[t] = o;
     }
   }
@@ -470,23 +451,23 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
       const double le = log2(se), lf = log2(sf);
       L = (a.kind == kKlForward) ? w / se - le + lf : w / se + lf;
       L *= kLn2D;
-      // the element holding both rows' largest logit, each row's only one:
-      // with 1 + R = Z 2^(-zmax s), p = 1 / (1 + R_t), q = 1 / (1 + R_d) and
-      // R_t - R_d = -x, so q - p = -x / ((1 + R_t) (1 + R_d)) without the
-      // cancellation of two numbers near 1
+      // the log ratio of the two partition functions, lam_t - lam_d =
+      // log2(Z_t' / Z_d') = log2(1 - x / Z_d') with x = Z_d' - Z_t' summed
+      // pairwise (Z' = 2^lam): not the difference of two separately rounded
+      // sums, whose float32 error would set q - p of tokens that nearly
+      // coincide in the two rows
       double xs = 0.0;
-      int top = -1;
-      for (int cc = lane; cc < C; cc += 64) { xs += ps[cc].x; top = max(top, ps[cc].top); }
+      for (int cc = lane; cc < C; cc += 64) xs += ps[cc].x;
       xs = wave_sum(xs);
-      top = -wave_min_int(-top);
       const KlNorm& nt = a.norms[static_cast<int64_t>(n) * K + kk];
       const KlNorm& nd = a.norms[static_cast<int64_t>(a.N) * K + static_cast<int64_t>(n) * K + kk];
-      if (lane == 0 && a.grad && top >= 0 && nt.n == 1 && nd.n == 1) {
-        const double s = static_cast<double>(scale_of(a.rows.temp_scalar));
-        const double rt = nt.D * exp2(static_cast<double>(nt.M) - static_cast<double>(nt.zmax) * s);
-        const double rd = nd.D * exp2(static_cast<double>(nd.M) - static_cast<double>(nd.zmax) * s);
-        const double g = a.scale * static_cast<double>(a.inv_t) / K * (-xs) / (rt * rd);
-        if (g == g) a.grad[(static_cast<int64_t>(n) * K + kk) * a.rows.V + top] = static_cast<float>(g);
+      double dlam = nt.lam - nd.lam;
+      const double r = -xs * exp2(-nd.lam);
+      if (r > -1.0 && r < INFINITY && dlam - dlam == 0.0) dlam = log1p(r) * (1.0 / kLn2D);
+      if (lane == 0) {
+        const float hi = static_cast<float>(dlam);
+        a.coef[static_cast<int64_t>(n) * K + kk] =
+            make_float4(hi, static_cast<float>(dlam - static_cast<double>(hi)), 0.f, 0.f);
       }
     }
     Ln += L;
@@ -495,12 +476,18 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
   if (lane == 0) a.loss_pos[n] = a.scale * Ln / K;
 }
 
-template <class E, int NT, int S>
+// The gradient pass.  Forward KL and CE: (q - p) scale / (K T) =
+// sign(d) |q - p| scale / (K T), d = log2 q - log2 p formed with the
+// pairwise partition-function ratio of kl_coef.  Reverse KL: scale / (K T)
+// q ln2 (d - mu), or for the draft's single largest element
+// scale / (K T) q ln2 (d Sfx - Wx) / Sf.
+template <class E, int NT, int S, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
   const RowsDesc& d = a.rows;
   const int C = d.C, V = d.V, NK = a.N * a.K;
+  const float gcoef = static_cast<float>(a.scale * static_cast<double>(a.inv_t) / a.K);
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
     const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
     int bb;
@@ -509,8 +496,9 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
     const typename E::raw* rd = row_of<E>(d, NK + u, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
     const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
-    const KlDelta dr = kl_delta_ref(nt, nd, s);
+    KlDelta dr = kl_delta_ref(nt, nd, s);
     const float4 A = a.coef[u];
+    if (KIND != kKlReverse) kl_delta_set_lam(dr, static_cast<double>(A.x) + static_cast<double>(A.y));
     const bool single_top = nd.n == 1;
     float* gr = a.grad + static_cast<int64_t>(u) * V;
     const int tile0 = c * NT;
@@ -528,8 +516,16 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
         for (int k = 0; k < EPV; ++k) {
           const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
           const float dl = kl_ratio<E>(xt[j][k], xd[j][k], dr).dl;
-          const float tm = (single_top && xd[j][k] == nd.zmax) ? fmaf(dl, A.z, -A.w) : dl - A.y;
-          gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
+          if constexpr (KIND == kKlReverse) {
+            const float tm = (single_top && xd[j][k] == nd.zmax) ? fmaf(dl, A.z, -A.w) : dl - A.y;
+            gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
+          } else {
+            const float e = __builtin_amdgcn_exp2f(fmaf(xt[j][k], s, -nt.M));
+            const float pe = e * nt.invD, qf = f * nd.invD;
+            const float mx = fmaxf(pe, qf);
+            const float g = kl_absdiff<E>(mx, fminf(pe, qf), dl);
+            gv[k] = mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
+          }
         }
         store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }

@@ -440,8 +440,8 @@ spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
                      units * C);
   hipLaunchKernelGGL(sv::kl_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
-  if (KIND == sv::kKlReverse && a.grad) {
-    void (*kg)(sv::KlArgs, int64_t) = sv::kl_grad_kernel<G, NTG, kStep>;
+  if (a.grad) {
+    void (*kg)(sv::KlArgs, int64_t) = sv::kl_grad_kernel<G, NTG, kStep, KIND>;
     hipLaunchKernelGGL(kg, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a, units * C);
   }
   hipLaunchKernelGGL(sv::kl_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
