@@ -431,10 +431,16 @@ spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(sv::kl_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, static_cast<const sv::KlStat*>(a.stats), static_cast<int>(2 * units),
                      a.SC, sv::scale_of(a.rows.temp_scalar), a.norms);
-  // the passes that may write the gradient read bf16 as 4-element vectors: one float4 store per lane
+  // the gradient pass reads bf16 as 4-element vectors, so that each lane
+  // writes one float4; so does the forward-KL / CE statistics pass (with
+  // 16-byte vectors it needs 124 VGPRs and measured 11.0 against 9.8 ms at
+  // N=16384, K=3, V=151936), while the reverse-KL one reads 16-byte vectors
+  // (6.8 against 7.2 ms)
   using G = typename GradElem<E>::type;
+  using P = typename std::conditional<KIND == sv::kKlReverse, E, G>::type;
+  constexpr int NTP = kChunkElems / (sv::kThreads * P::EPV);
   constexpr int NTG = kChunkElems / (sv::kThreads * G::EPV);
-  void (*kp)(sv::KlArgs, int64_t) = sv::kl_pass_kernel<G, NTG, kStep, KIND>;
+  void (*kp)(sv::KlArgs, int64_t) = sv::kl_pass_kernel<P, NTP, kStep, KIND>;
   // one workgroup per task (measured faster than a resident grid: reverse KL 22.8 -> 21.2 ms per call)
   hipLaunchKernelGGL(kp, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a,
                      units * C);
