@@ -41,6 +41,9 @@ constexpr int kPairVec = 4;
 // Pair-pass items below which each one gets a workgroup (the small-batch
 // launch shape).
 constexpr int64_t kSharedItems = 4096;
+// Residual-step items up to which the pair pass takes them first (about the
+// waves the device holds at once).
+constexpr int64_t kLongestFirstItems = 8192;
 constexpr int kDiagPairVec = 2;
 constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
@@ -351,8 +354,12 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, 
   const int shape = lc ? lc->residual_shape : 0;
   const int split = shape == 2 || (shape == 0 && (items < kSharedItems || a.overlap == nullptr)) ? 1 : 0;
   const int64_t wgs = split ? items : (items + sv::kWaves - 1) / sv::kWaves;
+  // residual-step items first while they fit in about one round of what the
+  // device holds at once, else the pair order (without overlaps every item
+  // is a residual-step item)
+  const int longest_first = (a.overlap == nullptr || int64_t{a.B} * a.rows.C <= kLongestFirstItems) ? 1 : 0;
   hipLaunchKernelGGL((sv::pair_pass_wave_kernel<E, kStep, kPairVec>), dim3(static_cast<unsigned>(wgs)),
-                     dim3(sv::kThreads), 0, s, a, items, split);
+                     dim3(sv::kThreads), 0, s, a, items, split, longest_first);
   // the finish inverts the CDF inside one sub-chunk (kStep tiles, one load step)
   hipLaunchKernelGGL((sv::finish_kernel<E, kStep, kStep>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0,
                      s, a);

@@ -345,11 +345,16 @@ __device__ __forceinline__ StepSums pair_step_sums(const typename E::raw* rt, co
 // load steps in float64 (in step order), then one float64 sum over the
 // wave's lanes.
 //
-// Items 0 .. B*C-1 are the sub-chunks of each batch row's residual step (its
-// first rejected step, or step K-1 of a row that accepts every draft), the
-// B*(K-1)*C items after them the rows' other steps (item (b*(K-1) + m)*C + j
-// is sub-chunk j of the m-th of row b's other steps).  A residual item costs
-// about three times an overlap item, so these come first in the launch.
+// Two item orders.  Longest first (longest_first != 0): items 0 .. B*C-1
+// are the sub-chunks of each batch row's residual step (its first rejected
+// step, or step K-1 of a row that accepts every draft), the B*(K-1)*C items
+// after them the rows' other steps (item (b*(K-1) + m)*C + j is sub-chunk j
+// of the m-th of row b's other steps): a residual item costs about three
+// times an overlap item, and taking them first keeps them from piling up at
+// the end of a launch the device holds at once.  Pair order (item
+// (b*K + i)*C + j), for launches many times what the device holds: there the
+// longest-first order would run a phase of residual items alone, bound by
+// the VALU, before a phase bound by memory, while the pair order mixes them.
 // Two launch shapes:
 //  - split == 0: one wave per item, kWaves items per workgroup;
 //  - split == 1 (small batches, where one wave per item leaves the device
@@ -359,7 +364,8 @@ __device__ __forceinline__ StepSums pair_step_sums(const typename E::raw* rt, co
 //    through LDS.
 // Without overlaps only the residual-step items are launched.
 template <class E, int ST, int S>
-__global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, int64_t nitems, int split) {
+__global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, int64_t nitems, int split,
+                                                                  int longest_first) {
   constexpr int EPV = E::EPV;
   constexpr int WV = ST * (kThreads / 64);
   constexpr int NS = WV / S;  // load steps per sub-chunk
@@ -372,25 +378,37 @@ __global__ __launch_bounds__(kThreads) void pair_pass_wave_kernel(VerifyArgs a, 
   const bool shared_item = split != 0;
   const int64_t g = shared_item ? static_cast<int64_t>(blockIdx.x) : static_cast<int64_t>(blockIdx.x) * kWaves + wave;
   if (g >= nitems) return;  // (uniform over a workgroup that shares its item)
-  int b, j, m = 0;
-  if (g < first) {
-    b = static_cast<int>(g / C);
-    j = static_cast<int>(g - static_cast<int64_t>(b) * C);
-  } else {
-    const int64_t g2 = g - first, per = static_cast<int64_t>(a.K - 1) * C;
-    b = static_cast<int>(g2 / per);
-    const int r = static_cast<int>(g2 - static_cast<int64_t>(b) * per);
-    m = r / C;
-    j = r - m * C;
+  int b, i, j;
+  bool need_z;
+  if (longest_first) {
+    int m = 0;
+    if (g < first) {
+      b = static_cast<int>(g / C);
+      j = static_cast<int>(g - static_cast<int64_t>(b) * C);
+    } else {
+      const int64_t g2 = g - first, per = static_cast<int64_t>(a.K - 1) * C;
+      b = static_cast<int>(g2 / per);
+      const int r = static_cast<int>(g2 - static_cast<int64_t>(b) * per);
+      m = r / C;
+      j = r - m * C;
+    }
+    const int n = a.decision[b];
+    if (n < 0) return;  // data error: finish ignores this row's partials
+    const bool rejects = a.want_z && n < a.K;
+    const int i0 = rejects ? n : a.K - 1;
+    i = g < first ? i0 : (m < i0 ? m : m + 1);
+    need_z = rejects && g < first;
+  } else {  // pair order: item g = (b * K + i) * C + j
+    const int u = static_cast<int>(g / C);
+    j = static_cast<int>(g - static_cast<int64_t>(u) * C);
+    b = u / a.K;
+    i = u - b * a.K;
+    const int n = a.decision[b];
+    if (n < 0) return;
+    need_z = a.want_z && i == n;
   }
-  // (uniform over a workgroup that shares its item, so the returns below
-  // leave its barrier to all of its waves or to none)
-  const int n = a.decision[b];
-  if (n < 0) return;  // data error: finish ignores this row's partials
-  const bool rejects = a.want_z && n < a.K;
-  const int i0 = rejects ? n : a.K - 1;
-  const int i = g < first ? i0 : (m < i0 ? m : m + 1);
-  const bool need_z = rejects && g < first;
+  // (all of the above is uniform over a workgroup that shares its item, so
+  // the returns leave its barrier to all of its waves or to none)
   if (!need_z && a.overlap == nullptr) return;  // no overlap requested: only the residual step is read again
   const int rt_i = target_row(a, b, i), rd_i = draft_row(a, b, i);
   int bb;
