@@ -347,12 +347,15 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, 
   // grid of what the device holds at once striding over them), or one
   // workgroup per item where that measured faster: calls without overlaps
   // (B = 32..256, K = 3, V = 151936 bf16: 42.1 against 50.8 us at B = 32,
-  // 54.0 against 63.5 at B = 64, 135.3 against 136.8 at B = 256) and calls
-  // with fewer than kSharedItems items (47.8 against 53.2 us at B = 32, 70.1
-  // against 71.5 at B = 64; 113.2 against 107.9 at B = 128)
+  // 54.0 against 63.5 at B = 64, 135.3 against 136.8 at B = 256), K = 1, where
+  // every item is a residual-step item (pair pass 41.3 against 45.5 us at
+  // B = 256), and calls with fewer than kSharedItems items (47.8 against
+  // 53.2 us at B = 32, 70.1 against 71.5 at B = 64; 113.2 against 107.9 at
+  // B = 128)
   const int64_t items = int64_t{a.B} * (a.overlap ? a.K : 1) * a.rows.C;
   const int shape = lc ? lc->residual_shape : 0;
-  const int split = shape == 2 || (shape == 0 && (items < kSharedItems || a.overlap == nullptr)) ? 1 : 0;
+  const int split =
+      shape == 2 || (shape == 0 && (items < kSharedItems || a.overlap == nullptr || a.K == 1)) ? 1 : 0;
   const int64_t wgs = split ? items : (items + sv::kWaves - 1) / sv::kWaves;
   // residual-step items first while they fit in about one round of what the
   // device holds at once, else the pair order (without overlaps every item
