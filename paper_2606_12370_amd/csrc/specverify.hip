@@ -38,9 +38,9 @@ constexpr int kStep = 4;
 // pass) or kDiagPairVec (diagnostics pair pass) vectors per lane at a time.
 constexpr int kStatVec = 8;
 constexpr int kPairVec = 4;
-// Pair-pass items below which each one gets a workgroup (the small-batch
-// launch shape).
-constexpr int64_t kSharedItems = 4096;
+// Pair-pass items below which a launch of residual-step items only gives
+// each one a workgroup (the small-batch launch shape).
+constexpr int64_t kSharedItems = 8192;
 // Residual-step items up to which the pair pass takes them first (about the
 // waves the device holds at once).
 constexpr int64_t kLongestFirstItems = 8192;
@@ -345,17 +345,19 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, 
   // pair pass: without overlaps only each batch row's residual step is read
   // again.  One wave per item, four per workgroup (measured faster than a
   // grid of what the device holds at once striding over them), or one
-  // workgroup per item where that measured faster: calls without overlaps
-  // (B = 32..256, K = 3, V = 151936 bf16: 42.1 against 50.8 us at B = 32,
-  // 54.0 against 63.5 at B = 64, 135.3 against 136.8 at B = 256), K = 1, where
-  // every item is a residual-step item (pair pass 41.3 against 45.5 us at
-  // B = 256), and calls with fewer than kSharedItems items (47.8 against
-  // 53.2 us at B = 32, 70.1 against 71.5 at B = 64; 113.2 against 107.9 at
-  // B = 128)
+  // workgroup per item for launches whose every item is a residual-step item
+  // (calls without overlaps, and K = 1) with fewer than kSharedItems items.
+  // Measured with warm clocks, the two shapes interleaved (K = 3, V = 151936
+  // bf16 unless noted; us per call): without overlaps B = 64 54.8 against
+  // 64.5, B = 256 136.4 against 137.6, B = 512 247.3 against 245.6, B = 1024
+  // 474.1 against 461.0; K = 1 B = 256 95.4 against 101.0, B = 512 163.7
+  // against 161.6, B = 1024 302.2 against 285.0; with overlaps at K = 3 the
+  // wave shape is faster at every B measured (64: 70.2 against 71.5, 128:
+  // 106.5 against 114.3, 256: 183.2 against 200.3)
   const int64_t items = int64_t{a.B} * (a.overlap ? a.K : 1) * a.rows.C;
   const int shape = lc ? lc->residual_shape : 0;
-  const int split =
-      shape == 2 || (shape == 0 && (items < kSharedItems || a.overlap == nullptr || a.K == 1)) ? 1 : 0;
+  const bool residual_only = a.overlap == nullptr || a.K == 1;
+  const int split = shape == 2 || (shape == 0 && residual_only && items < kSharedItems) ? 1 : 0;
   const int64_t wgs = split ? items : (items + sv::kWaves - 1) / sv::kWaves;
   // residual-step items first while they fit in about one round of what the
   // device holds at once, else the pair order (without overlaps every item
