@@ -249,6 +249,26 @@ def verify_sweep(torch, binding, W, stream, warmup, steps):
                     torch.cuda.empty_cache()
 
 
+# Ceilings measured on MI355X: a streaming read of this library's statistics
+# passes with non-temporal loads and a resident grid, and a device-to-device
+# copy (read + write traffic together).
+STREAM_READ_GBS = 6650.0
+COPY_GBS = 5050.0
+
+
+def tv_three_pass_floor_ms(N, K, V):
+    """The TV loss's three passes at those ceilings, for bf16 logits: both
+    logit tensors read (statistics), read again with one 64-bit indicator
+    word per thread and 16384-element chunk written (pair pass), the draft
+    and the indicator words read and the float32 gradient written (gradient
+    pass)."""
+    logits = N * K * V * 2
+    words = N * K * (-(-V // 16384)) * 256 * 8
+    reads = 2 * logits / STREAM_READ_GBS + (2 * logits + words) / STREAM_READ_GBS
+    grad = (logits + words + N * K * V * 4) / COPY_GBS
+    return (reads + grad) / 1e6
+
+
 def hbm_roofline(nbytes, ms, key):
     achieved = nbytes / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -543,6 +563,8 @@ def main():
             result["tv_loss"] = {
                 "workload": "tv_bf16_n16384_k3_v151936", "mode": "prod", "ms_per_call": tv_ms,
                 "positions_per_s": N / (tv_ms * 1e-3),
+                "algorithmic_bytes": tv_bytes,
+                "three_pass_floor_ms": tv_three_pass_floor_ms(N, KT, VT),
                 "roofline": {"bound": "hbm", "achieved": tv_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": tv_ach / HBM_PEAK_GBS,
                              "traffic": measured_traffic("tv_bf16_n16384_k3_v151936", tv_bytes)},

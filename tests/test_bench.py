@@ -99,3 +99,15 @@ def test_all_cores_baseline_on_a_tiny_batch():
     assert r["cores"] == 2 and r["kind"] == "oracle" and r["value"] > 0
     assert r["host_cpus"] == os.cpu_count()
     assert int(r["sample"].split()[0]) >= B
+
+
+def test_tv_three_pass_floor():
+    """The TV loss's three-pass floor at the measured ceilings: the two
+    tensors read twice (plus the indicator words written), then the draft
+    and the words read and the float32 gradient written."""
+    N, K, V = 16384, 3, 151936
+    logits = N * K * V * 2
+    words = N * K * 10 * 256 * 8
+    expect = (4 * logits + words) / bench.STREAM_READ_GBS / 1e6 + (logits + words + 2 * logits) / bench.COPY_GBS / 1e6
+    assert bench.tv_three_pass_floor_ms(N, K, V) == pytest.approx(expect, rel=1e-12)
+    assert 17.5 < expect < 19.0
