@@ -436,8 +436,8 @@ def main():
                     help="also run a 1 GiB device copy (scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (the verification "
-              "rows are independent and would shard over GPUs with no exchange; see DESIGN.md)",
+        print("bench.py measures one GPU only: the library has no multi-GPU path (the verification "
+              "rows are independent and would shard over GPUs with no exchange)",
               file=sys.stderr)
         sys.exit(2)
 
