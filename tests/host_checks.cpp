@@ -3,7 +3,8 @@
 // UndefinedBehaviorSanitizer on the host code only and run without a GPU.
 // Every call below either fails validation (the status is checked) or, for
 // the shapes marked "valid", passes validation and lays out its workspace,
-// then reports the failed launch (no GPU, no device code in this build).
+// then reports the failed launch (no GPU in the process: the device code is
+// compiled, and never runs).
 // Exit status 0 when every status matched; sanitizer reports abort the run.
 #include <climits>
 #include <cmath>
