@@ -132,16 +132,20 @@ size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
  *
  * Two launch paths compute the same method (spec_verify takes the chain;
  * spec_verify_ex selects either):
- *  - single read (K <= 4, 16-byte aligned rows, at most 64 sub-chunks of
- *    8192 bf16 / 4096 fp32 elements per row): each batch row is spread over a
- *    group of workgroups, one per sub-chunk, which keep their sub-chunk of all
- *    2K+1 rows in registers, exchange the sub-chunk statistics through the
+ *  - single read (K <= 4, 16-byte aligned rows, at most 64 slices of 4096
+ *    bf16 / 2048 fp32 elements per row): each batch row is spread over a
+ *    group of workgroups, one per slice, which keep their slice of all 2K+1
+ *    rows in registers and LDS, exchange the slice statistics through the
  *    workspace and take the overlaps and residual sums without reading the
  *    logits again; then one launch per batch row picks the resampled token
- *    (reading one sub-chunk of one row pair again);
- *  - chain (every other shape): statistics, decision, a second read of the
- *    draft pairs (only the rejected pair without `overlap`), then the same
- *    per-row launch.
+ *    (reading one slice of one row pair again);
+ *  - chain (every shape): statistics, decision, a second read of the draft
+ *    pairs (only each batch row's residual step without `overlap`), then the
+ *    same per-row launch.
+ * Either path forms each element's p - q for the residual from the exact
+ * logit difference, with the two rows' normalisations reconciled, so that
+ * the residual distribution matches exact arithmetic where p and q nearly
+ * coincide.
  * Tokens are bit-exact functions of the inputs, seed and offset for either
  * path and any number of groups; the two paths' float32 normaliser sums differ
  * in summation order, which can move a decision only where its uniform lies

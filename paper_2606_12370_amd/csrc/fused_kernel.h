@@ -3,21 +3,25 @@
 // logits.
 //
 // Every batch row is spread over a group of G co-resident workgroups, one per
-// sub-chunk of the vocabulary (1024 16-byte vectors: 8192 bf16 or 4096 fp32
-// elements), and a group takes its batch rows one after another.  For one
-// batch row, each workgroup of the group:
-//   1 loads its sub-chunk of all 2K+1 rows (four vectors per thread and row)
-//     into registers and keeps them there;
-//   2 reduces each row's sub-chunk to (max reference, exp2 sum) and publishes
-//     the record with agent-scope atomic stores;
-//   3 waits for the G records of each row (the other workgroups of its group,
-//     which run at the same time), combines them into the row normalisers in
-//     the fixed order every kernel of the library uses, and takes the accept
-//     decisions (every workgroup the same ones; the first writes them);
-//   4 sums, from the registers, the overlap of every draft step and the
-//     residual sums of the first rejected step over its sub-chunk.
+// slice of the vocabulary (2 tiles: 512 16-byte vectors, 4096 bf16 or 2048
+// fp32 elements), and a group takes its batch rows one after another
+// (group k: rows k, k + NG, ...).  Each workgroup runs a three-stage
+// pipeline over its group's rows, one step per row:
+//   1 issue the loads of the next row's slice of all 2K+1 rows (two vectors
+//     per thread and row) into one of two register sets;
+//   2 reduce the current row's slice of each row to (max reference, exp2
+//     sum) and publish the records with agent-scope atomic stores, then park
+//     the slice's K pair rows (and the draft-token inputs of the decisions)
+//     in LDS;
+//   3 for the row parked one step earlier: wait for the G records of each of
+//     its rows (published by the other workgroups of the group, which run at
+//     the same time), combine them into the row normalisers in the fixed
+//     order every kernel of the library uses, take the accept decisions
+//     (every workgroup the same ones; the first writes them), and sum from
+//     LDS the overlap of every draft step and the residual sums of the
+//     residual step over its slice.
 // The finish launch (verify_kernel.h) then forms the overlaps, picks the
-// sub-chunk holding the resampled token and inverts the CDF inside it.
+// slice holding the resampled token and inverts the CDF inside it.
 //
 // The record array is set to all-ones bits before the launch; a record is
 // complete once neither of its two 64-bit words is all ones (a normaliser sum
