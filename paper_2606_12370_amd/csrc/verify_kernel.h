@@ -9,17 +9,19 @@
 //                 (float64, u q(x) < p(x) with the two gathered logits and
 //                 Philox uniforms); accept length; every output except the
 //                 overlaps and the resampled token.
-//   3 pair_pass   every (target row i, draft row i) pair, one wave per
-//                 sub-chunk:
-//                 overlap sum min(p, q); for the row's first rejected step
-//                 also the residual mass sum max(0, p - q).  Bonus rows are
-//                 not read again, and without an overlap output only the
-//                 first rejected step's pair is.
-//   4 finish      one workgroup per batch row: overlaps; the chunk whose
-//                 cumulative residual (or bonus) mass crosses u' Z, found
-//                 from the per-sub-chunk masses; only that one is read again
-//                 to invert the CDF inside it (tile sums, thread scan,
-//                 element scan).
+//   3 pair_pass   every (target row i, draft row i) pair, one wave (or, for
+//                 small launches of residual steps, one workgroup) per
+//                 sub-chunk: overlap sum min(p, q); for the row's first
+//                 rejected step also the residual sums (residual mass,
+//                 sum (p - q), sum over p > q of q).  Bonus rows are not read
+//                 again, and without an overlap output only each row's
+//                 residual step is.
+//   4 finish      one workgroup per batch row: overlaps; the normalisation
+//                 correction of the residual; the sub-chunk whose cumulative
+//                 residual (or bonus) mass crosses u' Z, found from the
+//                 per-sub-chunk masses; only that one is read again to
+//                 invert the CDF inside it (tile sums, thread scan, element
+//                 scan).
 #pragma once
 
 #include "sv_device.h"
@@ -526,9 +528,9 @@ struct SampleShared {
 
 // Per-tile masses of chunk `c` (NT tiles of kThreads vectors, read S tiles at
 // a time), per thread: tsum[j] = this thread's mass in tile j.  The mass of an
-// element is the residual max(0, p - q) = p - min(p, q) (`residual`), else p;
-// element `excl` (-1: none) has mass 0.  Returns the number of tiles in the
-// chunk.
+// element is the residual max(0, p - q) with the normalisation correction
+// (`residual`, residual_mass), else p; element `excl` (-1: none) has mass 0.
+// Returns the number of tiles in the chunk.
 template <class E, int NT, int S>
 __device__ __forceinline__ int tile_masses(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
                                            bool al_d, bool residual, int excl, int c, int V, int ntiles, float s,
