@@ -16,27 +16,35 @@
 //                 Sf = sum f and the weighted log-ratio sum W (forward:
 //                 sum e (t - u); CE: sum e (-u)), all in float64 from the same
 //                 e, f, t, u, so the loss (formed in kl_coef) is normalised by
-//                 its own sums; for reverse KL the sums of f and f d over the
-//                 elements other than the draft's largest logit, and of f d
-//                 over those, with d = log2 q - log2 p.  Forward KL and CE
-//                 also write the gradient (q - p) here, since it needs no
-//                 global sum.
+//                 its own sums; for forward KL and CE also x = Z_d' - Z_t',
+//                 the sum of 2^(b) - 2^(a) over every element, a and b its
+//                 logits less each row's largest (times s), each term from
+//                 the exact log ratio; for reverse KL the sums of f and f d
+//                 over the elements other than the draft's largest logit,
+//                 and of f d over those, with d = log2 q - log2 p.
 //   4 kl_coef     per position: L_{n,k} from its chunks, the per-step output,
-//                 the position loss, the reverse-KL gradient constants.
-//   5 kl_grad     reverse KL only: q (log q - log p - L), read again.
+//                 the position loss, and the gradient constants: for forward
+//                 KL and CE lam_t - lam_d = log2(Z_t' / Z_d') =
+//                 log2(1 - x / Z_d'), for reverse KL mu and the complement
+//                 constants.
+//   5 kl_grad     every kind: the gradient, reading the pair again.
 //   6 kl_loss     position losses added in a fixed order.
 //
 // Where p and q nearly agree, q - p and log q - log p are small differences
-// of large terms.  Both are formed from d = log2 q - log2 p, taken in float64
-// as ((z_d - z_t) - (zmax_d - zmax_t)) s + (lam_t - lam_d) with
-// lam = log2 Z - zmax s: the logits enter as exact differences and lam
-// carries no float32 rounding of a sum near 1.
-// Then q - p = sign(d) max(p, q) (1 - 2^-|d|), with 1 - 2^-x from its series
-// for small x.  For reverse KL, the term log q_j - log p_j - L of the element
-// holding nearly all of q is a difference of two nearly equal numbers; with
-// L = ln2 sum_i q_i d_i and sum_i q_i = 1 it equals
-// ln2 sum_{i != j} q_i (d_j - d_i), which is formed from the sums over the
-// other elements instead.
+// of large terms.  Both are formed from d = log2 q - log2 p =
+// ((z_d - z_t) - (zmax_d - zmax_t)) s + (lam_t - lam_d), lam = log2 Z - zmax s:
+// the logits enter as exact differences (float64 for float32 logits, float32
+// for bfloat16 logits, whose differences are exact there), and for forward
+// KL and CE lam_t - lam_d comes from the pairwise sum x, not from two
+// separately rounded partition functions, whose float32 error would set q - p
+// of tokens that nearly coincide in the two rows.  Then
+// q - p = sign(d) max(p, q) (1 - 2^-|d|), with 1 - 2^-x from its series
+// below x = 1/2 and the difference of the two probabilities above.  For
+// reverse KL the gradient is invariant under a common shift of d (mu moves
+// with it); the term log q_j - log p_j - L of the element holding nearly all
+// of q is a difference of two nearly equal numbers; with L = ln2 sum_i q_i d_i
+// and sum_i q_i = 1 it equals ln2 sum_{i != j} q_i (d_j - d_i), which is
+// formed from the sums over the other elements instead.
 #pragma once
 
 #include <type_traits>
