@@ -126,11 +126,6 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
     const typename E::raw* rd = row_of<E>(d, rd_i, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
     const RowNorm nt = a.norms[rt_i], nd = a.norms[rd_i];
-    // bfloat16 logits: each row's reference and log2 normaliser folded into
-    // one float (one rounding of M + L, a few 1e-7 of it, inside the
-    // bfloat16 tolerance and the float32 decision freedom at p = q)
-    const float rft = static_cast<float>(static_cast<double>(nt.M) + static_cast<double>(nt.L));
-    const float rfd = static_cast<float>(static_cast<double>(nd.M) + static_cast<double>(nd.L));
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, d.ntiles - tile0);
     static_assert(NT * EPV <= 64, "indicator bits of a chunk fit one word per thread");
@@ -149,8 +144,11 @@ __global__ __launch_bounds__(kThreads) void tv_pair_kernel(TvArgs a, int64_t nta
         for (int kk = 0; kk < EPV; ++kk) {
           // log2 p and log2 q; min(p, q) is one exponential, and it is q
           // itself wherever q <= p, so it also carries the S term
-          const float lp = E::kFoldRef ? fmaf(xt[j][kk], s, -rft) : fmaf(xt[j][kk], s, -nt.M) - nt.L;
-          const float lq = E::kFoldRef ? fmaf(xd[j][kk], s, -rfd) : fmaf(xd[j][kk], s, -nd.M) - nd.L;
+          // (the reference and the log normaliser are not folded into one
+          // float: its rounding, a few 1e-7 of M + L, would move alpha of
+          // identical rows off 1 by about 1e-6, and the loss with it)
+          const float lp = fmaf(xt[j][kk], s, -nt.M) - nt.L;
+          const float lq = fmaf(xd[j][kk], s, -nd.M) - nd.L;
           const float mn = __builtin_amdgcn_exp2f(fminf(lp, lq));
           al += mn;
           const bool le = lq <= lp;
