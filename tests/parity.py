@@ -128,10 +128,15 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
     differ from the oracle by one common shift of S: grad_j - ref_j = -w_j dS
     with w = g q / T and |dS| <= sum_{ties} q.  dS is fitted by least squares
     over the untied elements and clipped to that slack; what remains beyond
-    each element's own q error, |ref_j| qerr_j, must be within the tolerance
-    times the row's largest gradient.  (The kernel sums S and its complement
-    1 - S separately, each from the same float32 q values, so no float32
-    rounding of S near 1 enters the gradient.)"""
+    each element's own q error, qerr_j times the size of that element's
+    gradient (the larger of |ref_j| and |ref_j - w_j dS|, the gradient under
+    the shifted S), must be within the tolerance times the row's largest
+    gradient.  The second size matters where a tied token holds nearly all of
+    q: the row's reference gradient is then of the order of the untied mass,
+    while the kernel's, with that token on the other side, is of the order of
+    q_j, and q_j's own float32 error is relative to the latter.  (The kernel
+    sums S and its complement 1 - S separately, each from the same float32 q
+    values, so no float32 rounding of S near 1 enters the gradient.)"""
     tol = TOL[dtype]
     ov = ov_g.cpu().numpy().astype(np.float64)
     if positions is not None:
@@ -168,7 +173,8 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
         with np.errstate(divide="ignore", invalid="ignore"):
             dS = np.where(den > 0, -num / den, 0.0)
         dS = np.clip(dS, -s_slack, s_slack)
-        resid = np.abs(d + w * dS[..., None]) - np.abs(gr) * qerr
+        size = np.maximum(np.abs(gr), np.abs(gr - w * dS[..., None]))
+        resid = np.abs(d + w * dS[..., None]) - size * qerr
         resid = np.where(untied, np.maximum(resid, 0.0), 0.0).max(axis=-1)
         scale = np.maximum(np.abs(gr).max(axis=-1), 1e-300)
         worst = float((resid / scale).max())

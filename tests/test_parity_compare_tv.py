@@ -94,3 +94,62 @@ def test_loss_floor_near_zero_and_relative_elsewhere():
     ref = tv_ref(zt, zd, T, MODE_E2E, scale=1.0)
     with pytest.raises(AssertionError):
         compare_tv(*as_gpu(ref, loss=ref["loss"] * (1 + 1e-3)), ref, W.F32)
+
+
+
+def dominant_tie_logits(seed, N=2, K=2, V=24, m=1e-7, delta=1e-4):
+    """Logits whose row (0, 0) has q_0 = p_0 = 1 - m (a tie) and all but
+    delta m of the other mass on tokens with p = q (1 - delta); the last
+    three tokens, holding delta m of q, take the surplus of p, so they alone
+    have q < p and S = sum 1[q <= p] q off the tie is delta m.  The other
+    rows are random."""
+    rng = np.random.default_rng(seed)
+    zd = rng.normal(0, 1.5, size=(N, K, V))
+    zt = zd + rng.normal(0, 0.7, size=(N, K, V))
+    q = np.empty(V)
+    q[0] = 1 - m
+    big = rng.uniform(0.5, 1.5, size=V - 4)
+    big *= (1 - delta) * m / big.sum()
+    q[1:V - 3] = big
+    q[V - 3:] = (m - big.sum()) / 3
+    p = q.copy()
+    p[1:V - 3] *= 1 - delta
+    p[V - 3:] += delta * big.sum() / 3
+    assert abs(p.sum() - 1) < 1e-15
+    zd[0, 0] = T * np.log(q)
+    zt[0, 0] = T * np.log(p)
+    return zt, zd, 0, 1 - m
+
+
+def test_dominant_tied_token_with_float32_q_errors():
+    """A tied token that holds all but 1e-7 of q: on the side of the tie that
+    leaves it out of S the row's gradient is of the order of the small mass
+    with q <= p, on the other of the q_j themselves.  The second side, with
+    each q_j off by a relative error inside its float32 bound, is accepted
+    against the first; one element off by 1e-3 of its own size is not."""
+    zt, zd, j0, qj = dominant_tie_logits(11)
+    # log p_j0 moves by (1 - p_j0) / T per unit of its logit and every other
+    # log p_v by -p_j0 / T: a nudge that puts log q_j0 - log p_j0 at +-1e-13
+    # moves the other ratios by 1e-6, well inside delta
+    eps = 1e-13 * T / (1 - qj)
+    above, below = zt.copy(), zt.copy()
+    above[0, 0, j0] += eps
+    below[0, 0, j0] -= eps
+    for mode in (MODE_E2E, MODE_PER_STEP):
+        ra = tv_ref(above, zd, T, mode, scale=1.0)
+        rb = tv_ref(below, zd, T, mode, scale=1.0)
+        assert ra["tie_margin"][0, 0, j0] < 1e-12 and rb["tie_margin"][0, 0, j0] < 1e-12
+        small, large = (ra, rb) if ra["S"][0, 0] < rb["S"][0, 0] else (rb, ra)
+        gs, gl = np.abs(small["grad"][0, 0]).max(), np.abs(large["grad"][0, 0]).max()
+        assert gl > 30 * gs
+        qerr = 2e-6 + 2.0 ** -22 * large["tie_condition"]
+        rng = np.random.default_rng(5 + mode)
+        noisy = large["grad"] * (1 + 0.5 * qerr * rng.uniform(-1, 1, size=qerr.shape))
+        compare_tv(*as_gpu(large, grad=noisy), small, W.F32)
+        compare_tv(*as_gpu(small, grad=small["grad"]), large, W.F32)
+        bad = large["grad"].copy()
+        v = int(np.argmax(np.where(np.arange(bad.shape[-1]) == j0, 0.0, np.abs(bad[0, 0]))))
+        bad[0, 0, v] *= 1 + 1e-3
+        with pytest.raises(AssertionError):
+            compare_tv(*as_gpu(large, grad=bad), small, W.F32)
+            pytest.fail("accepted an element off by 1e-3")
