@@ -132,8 +132,9 @@ size_t spec_verify_workspace_size(int B, int K, int V, spec_dtype dtype);
  *
  * Two launch paths compute the same method (spec_verify takes the chain;
  * spec_verify_ex selects either):
- *  - single read (K <= 4, 16-byte aligned rows, at most 64 slices of 4096
- *    bf16 / 2048 fp32 elements per row): each batch row is spread over a
+ *  - single read (K <= 4, 16-byte aligned rows, V a multiple of 8 for bf16
+ *    or of 4 for fp32, at most 64 slices of 4096 bf16 / 2048 fp32 elements
+ *    per row): each batch row is spread over a
  *    group of workgroups, one per slice, which keep their slice of all 2K+1
  *    rows in registers and LDS, exchange the slice statistics through the
  *    workspace and take the overlaps and residual sums without reading the

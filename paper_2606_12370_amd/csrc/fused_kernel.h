@@ -45,23 +45,17 @@ __device__ __forceinline__ void st_agent(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// The vector at element v0 of a row that ends inside it (v0 + EPV > V), built
-// element by element with -inf beyond V.
+// A vector of -inf elements: the slice's vectors past the end of the row (the
+// path runs only on rows whose length is a multiple of the vector, so a
+// vector lies wholly inside or wholly past it).
 template <class E>
-__device__ __forceinline__ typename E::vec tail_vector(const typename E::raw* row, int v0, int V) {
+__device__ __forceinline__ typename E::vec neg_inf_vector() {
+  const uint32_t h = E::EPV == 8 ? 0xFF80FF80u : 0xFF800000u;
   typename E::vec w;
-  if constexpr (E::EPV == 8) {  // bfloat16 bit patterns, two per 32-bit word
-    uint32_t h[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) h[k] = (v0 + k < V) ? static_cast<uint32_t>(row[v0 + k]) : 0xFF80u;
-    w.x = h[0] | (h[1] << 16); w.y = h[2] | (h[3] << 16);
-    w.z = h[4] | (h[5] << 16); w.w = h[6] | (h[7] << 16);
-  } else {
-    uint32_t h[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) h[k] = (v0 + k < V) ? __float_as_uint(row[v0 + k]) : 0xFF800000u;
-    w.x = h[0]; w.y = h[1]; w.z = h[2]; w.w = h[3];
-  }
+  w.x = h;
+  w.y = h;
+  w.z = h;
+  w.w = h;
   return w;
 }
 
@@ -80,6 +74,7 @@ struct FusedShared {
   float2 part[2 * K + 1][kThreads];
   DecideShared dec;  // the 2K+1 row normalisers of the batch row in its overlap stage
   double pr[kWaves][SPEC_MAX_K_DEV + 3];
+  float pT;  // temperature of the parked batch row
   int n, pb, gave_up;
 };
 
@@ -90,7 +85,17 @@ template <class E, int K>
 struct FusedUnit {
   typename E::vec w[2 * K + 1][kFusedNV];
   DraftGather gx;
-  int b;  // batch row, or -1 when the stage is empty
+  float T;  // the batch row's temperature
+  int id;   // lane i < K: draft token of step i (other lanes: step 0's)
+  int b;    // batch row, or -1 when the stage is empty
+};
+
+// The exchange records of a batch row's 2K+1 rows that one wave reads (rows
+// wave, wave + 4, ...; lane g < G: member g's record), as first polled.
+template <int K>
+struct FusedPoll {
+  static constexpr int RW = (2 * K + 1 + kWaves - 1) / kWaves;
+  uint64_t w0[RW], w1[RW];
 };
 
 template <class E, int K>
@@ -115,29 +120,72 @@ __device__ __forceinline__ int fused_row_index(const VerifyArgs& a, int b, int r
   return r <= K ? target_row(a, b, r) : draft_row(a, b, r - K - 1);
 }
 
-// Stage 1: issue the loads of batch row b's slice (no wait).
+// Every stage issues the same loads on every path (an empty stage or a lane
+// past the group loads from row 0 and ignores the result), so that the
+// compiler's wait counts stay exact: a wait for an older load never drains
+// the loads issued after it.
+
+// Stage 1: issue the loads of batch row b's slice (no wait): the
+// temperature and the draft tokens first, then the 2K+1 rows.
 template <class E, int K>
 __device__ __forceinline__ void fused_load(const FusedCtx<E, K>& c, int b, FusedUnit<E, K>& u) {
   using vec = typename E::vec;
   constexpr int EPV = E::EPV;
+  const VerifyArgs& a = c.a;
   u.b = b;
-  if (b < 0) return;
-  const int V = c.a.rows.V;
+  const int bl = b < 0 ? 0 : b;
+  const int V = a.rows.V;
+  const float* tp = a.rows.temp ? a.rows.temp + bl : reinterpret_cast<const float*>(a.ids);
+  u.T = *tp;
+  u.id = a.ids[static_cast<int64_t>(bl) * a.K + (c.lane < K ? c.lane : 0)];
 #pragma unroll
   for (int r = 0; r < 2 * K + 1; ++r) {
-    const typename E::raw* rp = fused_row<E, K>(c.a, b, r);
+    const typename E::raw* rp = fused_row<E, K>(a, bl, r);
 #pragma unroll
     for (int j = 0; j < kFusedNV; ++j) {
       const int v0 = c.e0 + (j * kThreads + c.tid) * EPV;
       u.w[r][j] = __builtin_nontemporal_load(reinterpret_cast<const vec*>(rp + ((v0 + EPV <= V) ? v0 : 0)));
     }
   }
-  u.gx = DraftGather{0, 0.f, 0.f, 0.0};
-  if (c.tid < K) u.gx = gather_draft<E>(c.a, b, c.tid);
 }
 
-// Stage 2: complete the row-end vectors, reduce every row of the slice to
-// (max reference, exp2 sum) and publish one record per row.
+// The draft token's two logits and the step's accept uniform (lane i < K:
+// step i), from the token loaded one stage earlier (no wait for the logits).
+template <class E, int K>
+__device__ __forceinline__ void fused_gather(const FusedCtx<E, K>& c, FusedUnit<E, K>& u) {
+  const VerifyArgs& a = c.a;
+  const int bl = u.b < 0 ? 0 : u.b;
+  const int i = c.lane < K ? c.lane : 0;
+  const int x = u.id;
+  const int xs = (x >= 0 && x < a.rows.V) ? x : 0;
+  u.gx.x = x;
+  u.gx.zt = E::one(fused_row<E, K>(a, bl, i) + xs);
+  u.gx.zd = E::one(fused_row<E, K>(a, bl, K + 1 + i) + xs);
+  u.gx.u = 0.0;
+  if (c.tid < K) {
+    const Philox4x64 ph =
+        philox4x64_10(static_cast<uint64_t>(bl), static_cast<uint64_t>(i), a.offset, 0ull, a.seed, 0ull);
+    u.gx.u = u24(ph.w[0]);
+  }
+}
+
+// The first poll of the exchange records of batch row b (no wait).
+template <class E, int K>
+__device__ __forceinline__ void fused_poll(const FusedCtx<E, K>& c, int b, FusedPoll<K>& pl) {
+  const int bl = b < 0 ? 0 : b;
+#pragma unroll
+  for (int i = 0; i < FusedPoll<K>::RW; ++i) {
+    const int r = c.wave + kWaves * i;
+    const int row = fused_row_index<E, K>(c.a, bl, r < 2 * K + 1 ? r : 0);
+    const uint64_t* rec = reinterpret_cast<const uint64_t*>(c.a.stats + static_cast<int64_t>(row) * c.G) +
+                          2 * (c.lane < c.G ? c.lane : 0);
+    pl.w0[i] = ld_agent(rec);
+    pl.w1[i] = ld_agent(rec + 1);
+  }
+}
+
+// Stage 2: reduce every row of the slice to (max reference, exp2 sum) and
+// publish one record per row.
 template <class E, int K>
 __device__ __forceinline__ void fused_stats(const FusedCtx<E, K>& c, FusedUnit<E, K>& u) {
   constexpr int EPV = E::EPV;
@@ -146,14 +194,14 @@ __device__ __forceinline__ void fused_stats(const FusedCtx<E, K>& c, FusedUnit<E
   FusedShared<E, K>& sh = *c.sh;
   const int b = u.b;
   const int V = a.rows.V;
-  const float T = temperature_of(a.rows, b);
+  const float T = u.T;
   const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
 #pragma unroll
     for (int j = 0; j < kFusedNV; ++j) {
       const int v0 = c.e0 + (j * kThreads + c.tid) * EPV;
-      if (v0 + EPV > V) u.w[r][j] = tail_vector<E>(fused_row<E, K>(a, b, r), v0, V);
+      if (v0 >= V) u.w[r][j] = neg_inf_vector<E>();
     }
     float x[kFusedNV][EPV];
 #pragma unroll
@@ -217,37 +265,48 @@ __device__ __forceinline__ void fused_park(const FusedCtx<E, K>& c, const FusedU
       sh.pbuf[K + i][j][c.tid] = u.w[K + 1 + i][j];
     }
   if (c.tid < K) sh.pgx[c.tid] = u.gx;
-  if (c.tid == 0) sh.pb = u.b;
+  if (c.tid == 0) {
+    sh.pb = u.b;
+    sh.pT = u.T;
+  }
 }
 
 // Stage 3: the group's records of every row (published one step earlier),
 // the row normalisers in combine_row's order, the decision, and the overlap
 // and residual sums of the slice from the parked rows.
 template <class E, int K>
-__device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
+__device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b, const FusedPoll<K>& pl) {
   constexpr int EPV = E::EPV;
   constexpr int R = 2 * K + 1;
   const VerifyArgs& a = c.a;
   const int G = c.G, lane = c.lane;
   FusedShared<E, K>& sh = *c.sh;
-  for (int r = c.wave; r < R; r += kWaves) {
+#pragma unroll
+  for (int i = 0; i < FusedPoll<K>::RW; ++i) {
+    const int r = c.wave + kWaves * i;
+    if (r >= R) break;
     const int row = fused_row_index<E, K>(a, b, r);
     const uint64_t* rec = reinterpret_cast<const uint64_t*>(a.stats + static_cast<int64_t>(row) * G);
-    uint64_t w0 = kRecordEmpty, w1 = kRecordEmpty;
+    // the first poll was issued at the start of the step; polls again only
+    // for records not yet complete
+    // (checked once outside the loop: inside it the wait for a poll covers
+    // every load issued before it)
+    uint64_t w0 = pl.w0[i], w1 = pl.w1[i];
     bool timed_out = false;
-    for (unsigned spin = 0;; ++spin) {
-      if (lane < G) {
-        if (w0 == kRecordEmpty) w0 = ld_agent(rec + 2 * lane);
-        if (w1 == kRecordEmpty) w1 = ld_agent(rec + 2 * lane + 1);
+    if (!__all(lane >= G || (w0 != kRecordEmpty && w1 != kRecordEmpty))) {
+      for (unsigned spin = 0;; ++spin) {
+        if (sh.gave_up || spin >= c.spin_limit) {
+          timed_out = true;
+          sh.gave_up = 1;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        if (lane < G) {
+          if (w0 == kRecordEmpty) w0 = ld_agent(rec + 2 * lane);
+          if (w1 == kRecordEmpty) w1 = ld_agent(rec + 2 * lane + 1);
+        }
+        if (__all(lane >= G || (w0 != kRecordEmpty && w1 != kRecordEmpty))) break;
       }
-      const bool ready = lane >= G || (w0 != kRecordEmpty && w1 != kRecordEmpty);
-      if (__all(ready)) break;
-      if (sh.gave_up || spin >= c.spin_limit) {
-        timed_out = true;
-        sh.gave_up = 1;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
     }
     const float mc = lane < G ? __uint_as_float(static_cast<uint32_t>(w0)) : -INFINITY;
     const double dc = lane < G ? __longlong_as_double(static_cast<long long>(w1)) : 0.0;
@@ -269,7 +328,7 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
   if (c.wave == 0) {
     DraftGather gx{0, 0.f, 0.f, 0.0};
     if (lane < K) gx = sh.pgx[lane];
-    const int n = decide_wave<E>(a, b, sh.dec, gx, c.g == 0);
+    const int n = decide_wave<E>(a, b, sh.dec, gx, sh.pT, c.g == 0);
     if (lane == 0) {
       sh.n = n;
       if (c.g == 0) a.decision[b] = n;
@@ -278,7 +337,7 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
   __syncthreads();
   const int n = sh.n;
   if (n >= 0) {
-    const float s = scale_of(temperature_of(a.rows, b));
+    const float s = scale_of(sh.pT);
     float al[K];
     float zp = 0.f, sd = 0.f, qg = 0.f;
 #pragma unroll
@@ -348,20 +407,26 @@ __device__ __forceinline__ void fused_pairs(const FusedCtx<E, K>& c, int b) {
   }
 }
 
-// One step of the pipeline: issue the loads of the group's batch row j + 1
-// into `ld`, reduce row j (`st`, loaded one step earlier), run the overlap
-// stage of row j - 1 from the parked rows, then park row j.  The exchange of
-// row j - 1 was published a step earlier and its wait overlaps row j's
-// statistics; row j + 1's loads are in flight all the while.
+// One step of the pipeline, its loads issued in the order they are waited
+// for: the first poll of the records of row j - 1 (parked one step earlier,
+// its records published then), the draft logits of row j, then the loads of
+// the group's batch row j + 1 into `ld`; then reduce row j (`st`, loaded one
+// step earlier), run the overlap stage of row j - 1 from the parked rows, and
+// park row j.  Row j + 1's loads stay in flight all the while.
 template <class E, int K>
 __device__ __forceinline__ void fused_step(const FusedCtx<E, K>& c, int j, int grp, int NG, int B,
                                            FusedUnit<E, K>& ld, FusedUnit<E, K>& st) {
   FusedShared<E, K>& sh = *c.sh;
+  const int pb = sh.pb;
+  FusedPoll<K> pl;
+  fused_poll<E, K>(c, pb, pl);
+  fused_gather<E, K>(c, st);
+  __builtin_amdgcn_sched_barrier(0);
   const int bl = grp + (j + 1) * NG;
   fused_load<E, K>(c, bl < B ? bl : -1, ld);
+  __builtin_amdgcn_sched_barrier(0);
   if (st.b >= 0) fused_stats<E, K>(c, st);
-  const int pb = sh.pb;
-  if (pb >= 0) fused_pairs<E, K>(c, pb);
+  if (pb >= 0) fused_pairs<E, K>(c, pb, pl);
   __syncthreads();  // the parked rows, part[] and the shared state are rewritten below
   fused_park<E, K>(c, st);
   __syncthreads();

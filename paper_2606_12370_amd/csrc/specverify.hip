@@ -287,12 +287,14 @@ const FusedFacts* fused_facts() {
 }
 
 // Workgroups of the single-read kernel the device holds at once, or 0 when the
-// shape does not qualify: K <= 4, 16-byte aligned rows, at most 64 sub-chunks
-// per row (the combine is one wave), cooperative launch, and room for at least
-// one group of G = sub-chunks workgroups.
+// shape does not qualify: K <= 4, 16-byte aligned rows whose length is a
+// multiple of the 16-byte vector (8 bf16 or 4 fp32 elements), at most 64
+// slices per row (the combine is one wave), cooperative launch, and room for
+// at least one group of G = slices workgroups.
 int fused_capacity(const sv::VerifyArgs& a, spec_dtype dt) {
   const int G = slices(a.rows.V, dt);
-  if (a.K < 1 || a.K > kFusedMaxK || !a.rows.vec_t || !a.rows.vec_d || G > 64) return 0;
+  const int epv = dt == SPEC_BF16 ? sv::BF16::EPV : sv::F32::EPV;
+  if (a.K < 1 || a.K > kFusedMaxK || !a.rows.vec_t || !a.rows.vec_d || G > 64 || a.rows.V % epv != 0) return 0;
   const FusedFacts* f = fused_facts();
   if (!f || !f->coop || f->cus <= 0) return 0;
   const int cap = f->bpc[dt][a.K] * f->cus;

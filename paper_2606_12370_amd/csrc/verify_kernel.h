@@ -171,13 +171,13 @@ __device__ __forceinline__ DraftGather gather_draft(const VerifyArgs& a, int b, 
 // outputs of position j (only with `write`: several workgroups may take the
 // same decision, one of them writes it).  Returns the accept length n, or -1
 // for a row with a data error (then every output of the row has been written).
+// (T: the row's temperature.)
 template <class E>
-__device__ int decide_wave(const VerifyArgs& a, int b, const DecideShared& sh, const DraftGather& gx,
+__device__ int decide_wave(const VerifyArgs& a, int b, const DecideShared& sh, const DraftGather& gx, float T,
                            bool write = true) {
   const RowsDesc& d = a.rows;
   const int K = a.K, V = d.V;
   const int lane = threadIdx.x & 63;
-  const float T = temperature_of(d, b);
   const bool t_ok = temperature_ok(T);
   const float s = t_ok ? scale_of(T) : 1.0f;
   double p = 0.0, q = 0.0;
@@ -254,7 +254,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(VerifyArgs a) {
   }
   __syncthreads();
   if (wave != 0) return;  // the decision is one wave's work
-  const int n = decide_wave<E>(a, b, sh, gx);
+  const int n = decide_wave<E>(a, b, sh, gx, temperature_of(d, b));
   if (lane == 0) a.decision[b] = n;
 }
 
