@@ -104,6 +104,7 @@ struct FusedCtx {
   int G, g, e0, tid, wave, lane;
   unsigned spin_limit;
   FusedShared<E, K>* sh;
+  float temp_scalar;  // the temperature of every row when there is no per-row array
 };
 
 template <class E, int K>
@@ -135,8 +136,11 @@ __device__ __forceinline__ void fused_load(const FusedCtx<E, K>& c, int b, Fused
   u.b = b;
   const int bl = b < 0 ? 0 : b;
   const int V = a.rows.V;
+  // (the value is selected, not the address: the per-row array is global
+  // memory, the scalar a kernel argument read once at the start)
   const float* tp = a.rows.temp ? a.rows.temp + bl : reinterpret_cast<const float*>(a.ids);
-  u.T = *tp;
+  const float tv = *tp;
+  u.T = a.rows.temp ? tv : c.temp_scalar;
   u.id = a.ids[static_cast<int64_t>(bl) * a.K + (c.lane < K ? c.lane : 0)];
 #pragma unroll
   for (int r = 0; r < 2 * K + 1; ++r) {
@@ -447,7 +451,8 @@ __global__ __launch_bounds__(kThreads) void verify_fused_kernel(VerifyArgs a, in
     sh.gave_up = 0;
   }
   __syncthreads();
-  const FusedCtx<E, K> c{a, G, g, g * (kThreads * kFusedNV * E::EPV), tid, tid >> 6, tid & 63, spin_limit, &sh};
+  const FusedCtx<E, K> c{a,         G,           g,   g * (kThreads * kFusedNV * E::EPV), tid, tid >> 6, tid & 63,
+                         spin_limit, &sh, a.rows.temp_scalar};
   const int B = a.B;
   FusedUnit<E, K> u0, u1;
   fused_load<E, K>(c, grp < B ? grp : -1, u0);

@@ -315,6 +315,26 @@ def test_residual_shapes_give_identical_bits(dtype, B, K, V, recipe):
     print(dtype, B, K, V, recipe, compare_verify(out, ref, dtype))
 
 
+@pytest.mark.parametrize("dtype,B,K,V", [(W.BF16, 11, 2, 20000), (W.F32, 6, 3, 16384)])
+def test_single_read_scalar_temperature(dtype, B, K, V):
+    """One temperature for every row (no per-row array): both paths match
+    the oracle at that temperature (a boundary draw may differ between them,
+    so their tokens are compared through the oracle)."""
+    d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 40 + B)
+    tgt, drf = device_inputs(d)
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = 0.8
+    ref = oracle.verify_ref(W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype), d["ids"],
+                            np.full(B, np.float32(T), dtype=np.float64), 7, 1)
+    outs = {}
+    for path in ("single_read", "chain"):
+        outs[path] = binding.verify(tgt, drf, ids, T, 7, 1, want_debug=True, path=path)
+        torch.cuda.synchronize()
+        compare_verify(outs[path], ref, dtype)
+    same = torch.equal(outs["single_read"]["emitted"], outs["chain"]["emitted"])
+    print(dtype, B, K, V, "chain and single read give the same tokens:", same)
+
+
 def test_single_read_unsupported_shapes_fall_back_or_refuse():
     """K = 8 (beyond the single-read path): the automatic launch takes the
     chain and matches the oracle; asking for the single-read path refuses."""
