@@ -8,7 +8,8 @@
 // (group k: rows k, k + NG, ...).  Each workgroup runs a three-stage
 // pipeline over its group's rows, one step per row:
 //   1 issue the loads of the next row's slice of all 2K+1 rows (two vectors
-//     per thread and row) into one of two register sets;
+//     per thread and row, with the row's temperature and draft tokens) into
+//     one of two register sets;
 //   2 reduce the current row's slice of each row to (max reference, exp2
 //     sum) and publish the records with agent-scope atomic stores, then park
 //     the slice's K pair rows (and the draft-token inputs of the decisions)
@@ -20,6 +21,9 @@
 //     (every workgroup the same ones; the first writes them), and sum from
 //     LDS the overlap of every draft step and the residual sums of the
 //     residual step over its slice.
+// A step issues its loads in the order they are waited for (the first poll
+// of stage 3's records, the draft logits of stage 2's row, then stage 1), so
+// that no wait for an older load also waits for the next row's slice.
 // The finish launch (verify_kernel.h) then forms the overlaps, picks the
 // slice holding the resampled token and inverts the CDF inside it.
 //
