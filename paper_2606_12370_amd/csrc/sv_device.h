@@ -553,48 +553,48 @@ __global__ __launch_bounds__(kThreads) void row_stats_wave_kernel(RowsDesc d, Ro
   // 1 us faster at the B=256 batch, same bits)
   for (int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave; g < nsub;
        g += static_cast<int64_t>(gridDim.x) * kWaves) {
-  const int C = d.C;
-  const int r = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
-  int b;
-  bool aligned;
-  const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
-  const float T = temperature_of(d, b);
-  const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-  const int e0 = j * WV * 64 * EPV;
-  float ref = -INFINITY, acc = 0.f;
+    const int C = d.C;
+    const int r = static_cast<int>(g / C), j = static_cast<int>(g - static_cast<int64_t>(g / C) * C);
+    int b;
+    bool aligned;
+    const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
+    const float T = temperature_of(d, b);
+    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
+    const int e0 = j * WV * 64 * EPV;
+    float ref = -INFINITY, acc = 0.f;
 #pragma unroll
-  for (int st = 0; st < WV / S; ++st) {
-    const int es = e0 + st * S * 64 * EPV;
-    if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
-    float x[S][EPV];
-    load_span<E, S, 64>(row, es, lane, d.V, aligned, x);
-    float mx = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < S; ++i)
-#pragma unroll
-      for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[i][k]);
-    const float nr = fmaxf(ref, mx * s);
-    if (nr != -INFINITY) {
-      float a2 = ref == -INFINITY ? 0.f : acc * __builtin_amdgcn_exp2f(ref - nr);
+    for (int st = 0; st < WV / S; ++st) {
+      const int es = e0 + st * S * 64 * EPV;
+      if (es >= d.V) break;  // wave-uniform: the row's last sub-chunk may be short
+      float x[S][EPV];
+      load_span<E, S, 64>(row, es, lane, d.V, aligned, x);
+      float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < S; ++i)
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) a2 += __builtin_amdgcn_exp2f(fmaf(x[i][k], s, -nr));
-      acc = a2;
-      ref = nr;
+        for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[i][k]);
+      const float nr = fmaxf(ref, mx * s);
+      if (nr != -INFINITY) {
+        float a2 = ref == -INFINITY ? 0.f : acc * __builtin_amdgcn_exp2f(ref - nr);
+#pragma unroll
+        for (int i = 0; i < S; ++i)
+#pragma unroll
+          for (int k = 0; k < EPV; ++k) a2 += __builtin_amdgcn_exp2f(fmaf(x[i][k], s, -nr));
+        acc = a2;
+        ref = nr;
+      }
     }
-  }
-  const float m = wave_max(ref);
-  double dd;
-  if (acc != acc) dd = acc;  // NaN propagates (data error)
-  else if (ref == -INFINITY) dd = 0.0;
-  else dd = static_cast<double>(acc) * static_cast<double>(__builtin_amdgcn_exp2f(ref - m));
-  dd = wave_sum(dd);
-  if (lane == 0) {
-    RowStat o;
-    o.m = m; o.pad = 0.f; o.D = dd;
-    stats[g] = o;
-  }
+    const float m = wave_max(ref);
+    double dd;
+    if (acc != acc) dd = acc;  // NaN propagates (data error)
+    else if (ref == -INFINITY) dd = 0.0;
+    else dd = static_cast<double>(acc) * static_cast<double>(__builtin_amdgcn_exp2f(ref - m));
+    dd = wave_sum(dd);
+    if (lane == 0) {
+      RowStat o;
+      o.m = m; o.pad = 0.f; o.D = dd;
+      stats[g] = o;
+    }
   }
 }
 
