@@ -335,6 +335,33 @@ def test_single_read_scalar_temperature(dtype, B, K, V):
     print(dtype, B, K, V, "chain and single read give the same tokens:", same)
 
 
+@pytest.mark.parametrize("dtype,V", [(W.BF16, 8201), (W.F32, 8202)])
+def test_single_read_refuses_rows_not_a_whole_number_of_vectors(dtype, V):
+    """A row length that is not a multiple of the 16-byte vector (8 bf16 or 4
+    fp32 elements), in rows padded to 16-byte aligned strides: the
+    single-read path refuses it, the automatic launch takes the chain and
+    matches the oracle."""
+    B, K = 5, 2
+    d = W.verify_inputs_numpy(B, K, V, dtype, "rollout_t", 23)
+    tgt0, drf0 = device_inputs(d)
+    epv = 8 if dtype == W.BF16 else 4
+    vpad = -(-V // epv) * epv
+    tgt = torch.zeros((B, K + 1, vpad), dtype=tgt0.dtype, device="cuda")[..., :V]
+    drf = torch.zeros((B, K, vpad), dtype=drf0.dtype, device="cuda")[..., :V]
+    tgt.copy_(tgt0)
+    drf.copy_(drf0)
+    assert tgt.stride(1) * tgt.element_size() % 16 == 0 and tgt.data_ptr() % 16 == 0
+    ids = torch.from_numpy(d["ids"]).cuda()
+    T = torch.from_numpy(d["temperature"]).cuda()
+    with pytest.raises(binding.SpecError):
+        binding.verify(tgt, drf, ids, T, 3, 1, path="single_read")
+    out = binding.verify(tgt, drf, ids, T, 3, 1, want_debug=True)
+    torch.cuda.synchronize()
+    ref = oracle.verify_ref(W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype), d["ids"],
+                            d["temperature"].astype(np.float64), 3, 1)
+    compare_verify(out, ref, dtype)
+
+
 def test_single_read_unsupported_shapes_fall_back_or_refuse():
     """K = 8 (beyond the single-read path): the automatic launch takes the
     chain and matches the oracle; asking for the single-read path refuses."""
