@@ -35,7 +35,7 @@ constexpr int kStep = 4;
 // diagnostics keep statistics per sub-chunk of kStep tiles (8192 bf16 or 4096
 // fp32 elements), which is what their per-row launches read again; one wave
 // streams one sub-chunk, kStatVec (statistics), kPairVec (verification pair
-// pass) or kDiagPairVec (diagnostics pair pass) vectors per lane at a time.
+// pass), kDiagStatVec / kDiagPairVec (diagnostics) vectors per lane at a time.
 constexpr int kStatVec = 8;
 // (2 vectors per load step in the wave-stride pair pass: B=256, K=3,
 // V=151936 bf16 177.6 against 179.0 us per call with 4, K=1 88.0 against
@@ -48,6 +48,9 @@ constexpr int64_t kSharedItems = 8192;
 // waves the device holds at once).
 constexpr int64_t kLongestFirstItems = 8192;
 constexpr int kDiagPairVec = 2;
+// (4 vectors per load step for the diagnostics statistics: 166.5-167.5
+// against 170.1-170.6 us per call with 8 at B=256, K=3, V=151936 bf16)
+constexpr int kDiagStatVec = 4;
 constexpr int kChunkElems = 16384;
 static_assert(kNtBf16 * sv::kThreads * sv::BF16::EPV == kChunkElems, "chunk geometry");
 static_assert(kNtF32 * sv::kThreads * sv::F32::EPV == kChunkElems, "chunk geometry");
@@ -509,7 +512,7 @@ spec_status launch_diag(const sv::DiagArgs& a, hipStream_t s) {
   const int C = a.rows.C;
   const int64_t units = int64_t{a.B} * a.K;
   const int64_t nsub = 2 * units * C;
-  hipLaunchKernelGGL((sv::diag_stats_wave_kernel<E, kStep, kStatVec>),
+  hipLaunchKernelGGL((sv::diag_stats_wave_kernel<E, kStep, kDiagStatVec>),
                      dim3(static_cast<unsigned>((nsub + sv::kWaves - 1) / sv::kWaves)), dim3(sv::kThreads), 0, s,
                      a.rows, const_cast<sv::DiagStat*>(a.stats), nsub);
   hipLaunchKernelGGL(sv::diag_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
