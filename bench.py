@@ -202,9 +202,12 @@ def quantile(sorted_vals, q):
     return sorted_vals[i] + (sorted_vals[j] - sorted_vals[i]) * (x - i)
 
 
-def timed(torch, stream, fn, steps):
-    """Mean milliseconds of fn(it) over `steps` calls, HIP events on `stream`."""
-    fn(0)
+def timed(torch, stream, fn, steps, warmup=1):
+    """Mean milliseconds of fn(it) over `steps` calls, HIP events on `stream`,
+    after `warmup` untimed calls (the clocks rise over tens of milliseconds of
+    sustained load)."""
+    for it in range(max(1, warmup)):
+        fn(it)
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
@@ -287,7 +290,7 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
         c = copies[it % len(copies)]
         binding.verify_target_only(c["target"], greedy[it % len(copies)], c["temperature"], seed=it, out=to_out)
 
-    ms = timed(torch, stream, to_step, steps)
+    ms = timed(torch, stream, to_step, steps, warmup=100)
     nbytes = B * (K + 1) * V * 2 + B * K * 4 + B * 4 + B * 4 + B * (K + 1) * 4
     out["target_only"] = {"ms_per_call": ms, "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
                           "mean_accept_len": float(to_out["accept_len"].float().mean()),
@@ -300,7 +303,7 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
     def sample_step(it):
         binding.sample(flats[it % len(copies)], temps[it % len(copies)], seed=it, out=s_out)
 
-    ms = timed(torch, stream, sample_step, steps)
+    ms = timed(torch, stream, sample_step, steps, warmup=100)
     nbytes = R * V * 2 + R * 4 + R * 4
     out["sample"] = {"ms_per_call": ms, "rows": R, "rows_per_s": R / (ms * 1e-3),
                      "roofline": hbm_roofline(nbytes, ms, "sample_bf16_r768_v151936")}
@@ -312,7 +315,7 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
         c = copies[it % len(copies)]
         binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=g_out, gumbel=True)
 
-    ms = timed(torch, stream, gumbel_step, steps)
+    ms = timed(torch, stream, gumbel_step, steps, warmup=100)
     nbytes = B * (2 * K + 1) * V * 2 + B * K * 4 + B * 4 + B * 4 + B * (K + 1) * 4 + B * K * 4
     out["verify_gumbel"] = {"ms_per_call": ms, "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
                             "roofline": hbm_roofline(nbytes, ms, "verify_gumbel_bf16_b256_k3_v151936")}
@@ -321,7 +324,7 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
     def sample_gumbel_step(it):
         binding.sample_gumbel(flats[it % len(copies)], temps[it % len(copies)], seed=it, out=sg_out)
 
-    ms = timed(torch, stream, sample_gumbel_step, steps)
+    ms = timed(torch, stream, sample_gumbel_step, steps, warmup=100)
     nbytes = R * V * 2 + R * 4 + R * 4
     out["sample_gumbel"] = {"ms_per_call": ms, "rows": R, "rows_per_s": R / (ms * 1e-3),
                             "roofline": hbm_roofline(nbytes, ms, "sample_gumbel_bf16_r768_v151936")}
@@ -331,7 +334,7 @@ def bench_variants(torch, binding, copies, stream, steps, B, K, V):
         c = copies[it % len(copies)]
         diag["d"] = binding.diagnostics(c["target"], c["draft"], c["temperature"])
 
-    ms = timed(torch, stream, diag_step, steps)
+    ms = timed(torch, stream, diag_step, steps, warmup=100)
     nbytes = B * 2 * K * V * 2 + B * 4 + B * K * (7 * 4 + 4 + 4)
     d = diag["d"]
     out["diagnostics"] = {"ms_per_call": ms, "roofline": hbm_roofline(nbytes, ms, "diagnostics_bf16_b256_k3_v151936"),
@@ -362,7 +365,7 @@ def bench_verify_context(torch, binding, W, copies, stream, steps):
         c = copies[it % len(copies)]
         binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, want_overlap=False, out=o)
 
-    ms = timed(torch, stream, serving, steps)
+    ms = timed(torch, stream, serving, steps, warmup=100)
     nbytes = verify_bytes(B, K, V) - B * K * 4
     out["verify_serving"] = {"workload": "verify_bf16_b256_k3_v151936 without overlaps", "ms_per_call": ms,
                              "verified_draft_tokens_per_s": B * K / (ms * 1e-3),
@@ -382,7 +385,7 @@ def bench_verify_context(torch, binding, W, copies, stream, steps):
             c = cps[it % len(cps)]
             binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=o2)
 
-        ms = timed(torch, stream, step2, steps)
+        ms = timed(torch, stream, step2, steps, warmup=100)
         out["verify_" + key] = {"ms_per_call": ms, "input_copies": ncp,
                                 "verified_draft_tokens_per_s": B2 * K2 / (ms * 1e-3),
                                 "roofline": hbm_roofline(verify_bytes(B2, K2, V2), ms, None)}
@@ -391,7 +394,7 @@ def bench_verify_context(torch, binding, W, copies, stream, steps):
                 c = cps[0]
                 binding.verify(c["target"], c["draft"], c["ids"], c["temperature"], seed=it, out=o2)
 
-            msw = timed(torch, stream, step_warm, steps)
+            msw = timed(torch, stream, step_warm, steps, warmup=100)
             out["verify_" + key]["warm"] = {"ms_per_call": msw, "input_copies": 1,
                                             "roofline": hbm_roofline(verify_bytes(B2, K2, V2), msw, None)}
         del cps
@@ -424,7 +427,7 @@ def main():
     ap.add_argument("--no-verify", action="store_true", help="skip the verify benchmark (profiling runs)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip target-only verification, the sampler and the diagnostics")
-    ap.add_argument("--variant-steps", type=int, default=20)
+    ap.add_argument("--variant-steps", type=int, default=100)
     ap.add_argument("--no-context", action="store_true",
                     help="skip spec_verify without overlaps and on the B=64 / B=1024 batches")
     ap.add_argument("--no-kl", action="store_true", help="skip the CE / KL loss legs")
