@@ -121,9 +121,11 @@ VerifyLayout verify_layout(int B, int K, int V, spec_dtype dt, bool gumbel = fal
   // multinomial verification: room for the per-slice records of the single-read path
   // (two per sub-chunk of the chain)
   const size_t C = static_cast<size_t>(gumbel ? geometry(V, dt).C : slices(V, dt));
+  // Gumbel-max verification keeps its statistics per sub-chunk, the rest per chunk
+  const size_t CS = gumbel ? std::max(C, static_cast<size_t>(sub_chunks(V, dt))) : C;
   const size_t rows = static_cast<size_t>(B) * (2 * K + 1);
   size_t off = 0;
-  L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
+  L.stats = off; off = align_up(off + rows * CS * sizeof(sv::RowStat), 256);
   L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
   L.decision = off; off = align_up(off + static_cast<size_t>(B) * sizeof(int32_t), 256);
   L.pairs = off; off = align_up(off + static_cast<size_t>(B) * K * C * sizeof(sv::PairStat), 256);
@@ -382,10 +384,13 @@ spec_status launch_verify(const sv::VerifyArgs& a, int64_t rows, hipStream_t s, 
 template <class E, int NT>
 spec_status launch_verify_gumbel(const sv::VerifyArgs& a, sv::GumbelBest* gbest, int64_t rows, hipStream_t s) {
   const int C = a.rows.C;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(rows * C)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), rows * C);
-  hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, a);
+  // the statistics per sub-chunk of kStep tiles with the chain's wave-shaped
+  // pass (6.6 against 6.3 TB/s for the one-workgroup-per-chunk one), and the
+  // decision combining them; the overlap and Gumbel passes keep their chunks
+  sv::VerifyArgs as = a;
+  as.rows.C = sub_chunks(a.rows.V, std::is_same<E, BF16>::value ? SPEC_BF16 : SPEC_F32);
+  launch_stats_wave<E>(as.rows, const_cast<sv::RowStat*>(a.stats), rows, s);
+  hipLaunchKernelGGL((sv::decide_kernel<E>), dim3(static_cast<unsigned>(a.B)), dim3(sv::kThreads), 0, s, as);
   if (a.overlap) {  // overlaps only: the Gumbel pass needs no residual mass
     void (*pp)(sv::VerifyArgs, int64_t) = sv::pair_pass_kernel<E, NT, kStep>;
     const int64_t pairs = int64_t{a.B} * a.K * C;
