@@ -101,7 +101,7 @@ bool verify_sizes_ok(int B, int K, int V, spec_dtype dt) {
 bool tv_sizes_ok(int N, int K, int V, spec_dtype dt) {
   if (N < 1 || K < 1 || K > SPEC_MAX_K || V < 1 || V > kMaxV) return false;
   const int64_t rows = static_cast<int64_t>(N) * 2 * K;
-  return rows * geometry(V, dt).C < (int64_t{1} << 31);
+  return rows * std::max(geometry(V, dt).C, sub_chunks(V, dt)) < (int64_t{1} << 31);
 }
 
 bool rows_ok(int64_t rows, int V, spec_dtype dt) {
@@ -142,9 +142,11 @@ struct TvLayout {
 TvLayout tv_layout(int N, int K, int V, spec_dtype dt) {
   TvLayout L;
   const size_t C = static_cast<size_t>(geometry(V, dt).C);
+  // statistics per sub-chunk of kStep tiles, the rest per chunk
+  const size_t CS = std::max(C, static_cast<size_t>(sub_chunks(V, dt)));
   const size_t rows = static_cast<size_t>(N) * 2 * K;
   size_t off = 0;
-  L.stats = off; off = align_up(off + rows * C * sizeof(sv::RowStat), 256);
+  L.stats = off; off = align_up(off + rows * CS * sizeof(sv::RowStat), 256);
   L.norms = off; off = align_up(off + rows * sizeof(sv::RowNorm), 256);
   L.pairs = off; off = align_up(off + static_cast<size_t>(N) * K * C * sizeof(sv::TvPair), 256);
   L.coef = off; off = align_up(off + static_cast<size_t>(N) * K * sizeof(float2), 256);
@@ -422,11 +424,14 @@ template <class E, int NT>
 spec_status launch_tv(const sv::TvArgs& a, hipStream_t s) {
   const int64_t units = int64_t{a.N} * a.K;
   const int C = a.rows.C;
-  void (*rs)(sv::RowsDesc, sv::RowStat*, int64_t) = sv::row_stats_kernel<E, NT, kStep>;
-  hipLaunchKernelGGL(rs, dim3(static_cast<unsigned>(2 * units * C)), dim3(sv::kThreads), 0, s, a.rows,
-                     const_cast<sv::RowStat*>(a.stats), 2 * units * C);
+  // the statistics per sub-chunk of kStep tiles with the wave-shaped pass,
+  // and the normalisers combining them; the pair and gradient passes keep
+  // their chunks
+  sv::RowsDesc ds = a.rows;
+  ds.C = sub_chunks(a.rows.V, std::is_same<E, BF16>::value ? SPEC_BF16 : SPEC_F32);
+  launch_stats_wave<E>(ds, const_cast<sv::RowStat*>(a.stats), 2 * units, s);
   hipLaunchKernelGGL(sv::row_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
-                     dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), C,
+                     dim3(sv::kThreads), 0, s, a.stats, static_cast<int>(2 * units), ds.C,
                      const_cast<sv::RowNorm*>(a.norms));
   void (*tp)(sv::TvArgs, int64_t) = sv::tv_pair_kernel<E, NT, kStep>;
   // one workgroup per task (measured faster than a resident grid: 5.6 against 6.0 ms at N=16384, K=3, V=151936)
