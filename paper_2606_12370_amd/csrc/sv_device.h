@@ -309,45 +309,6 @@ __host__ __device__ __forceinline__ float scale_of(float T) {
   return static_cast<float>(kLog2eD / static_cast<double>(T));
 }
 
-// Chunk statistics of one row: tiles tile0 .. tile0+nt-1, S tiles per step.
-template <class E, int NT, int S>
-__device__ __forceinline__ void chunk_stats(const typename E::raw* __restrict__ row, int tile0, int nt, int V,
-                                            bool aligned, float s, RedLds<4>& red, float* m_out, double* d_out) {
-  constexpr int EPV = E::EPV;
-  float ref = -INFINITY, dsum = 0.f;
-#pragma unroll
-  for (int j0 = 0; j0 < NT; j0 += S) {
-    if (j0 >= nt) break;
-    float x[S][EPV];
-    load_tiles<E, S>(row, tile0 + j0, V, aligned, x);
-    float mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < S; ++j)
-#pragma unroll
-      for (int k = 0; k < EPV; ++k) mx = fmaxf(mx, x[j][k]);
-    if (mx != -INFINITY) {
-      const float r = mx * s;
-      float acc = 0.f;
-#pragma unroll
-      for (int j = 0; j < S; ++j)
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) acc += __builtin_amdgcn_exp2f(fmaf(x[j][k], s, -r));
-      if (ref == -INFINITY) { ref = r; dsum = acc; }
-      else if (r > ref) { dsum = dsum * __builtin_amdgcn_exp2f(ref - r) + acc; ref = r; }
-      else dsum += acc * __builtin_amdgcn_exp2f(r - ref);
-    }
-  }
-  float m4[4] = {ref, -INFINITY, -INFINITY, -INFINITY};
-  wg_max<4>(m4, red);
-  double d4[4] = {0.0, 0.0, 0.0, 0.0};
-  if (dsum != dsum) d4[0] = dsum;  // NaN propagates (data error)
-  else if (ref != -INFINITY)
-    d4[0] = static_cast<double>(dsum) * static_cast<double>(__builtin_amdgcn_exp2f(ref - m4[0]));
-  wg_sum<4>(d4, red);
-  *m_out = m4[0];
-  *d_out = d4[0];
-}
-
 // Combine a row's C chunk statistics into (M, D).  Called by all 64 lanes of
 // one wave; every lane receives the result.  The order of the float64 sum is
 // fixed, so every kernel that combines the same row gets the same bits.
@@ -505,31 +466,6 @@ __device__ __forceinline__ float temperature_of(const RowsDesc& d, int b) {
   return d.temp ? d.temp[b] : d.temp_scalar;
 }
 __device__ __forceinline__ bool temperature_ok(float T) { return T > 0.f && T < INFINITY; }
-
-// One workgroup per (row, chunk): the chunk's statistics (pass 1).
-template <class E, int NT, int S>
-__global__ __launch_bounds__(kThreads) void row_stats_kernel(RowsDesc d, RowStat* __restrict__ stats, int64_t ntasks) {
-  __shared__ RedLds<4> red;
-  // grid-stride over the (row, chunk) tasks (launched one workgroup per task)
-  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int r = static_cast<int>(t / d.C), c = static_cast<int>(t - static_cast<int64_t>(t / d.C) * d.C);
-    int b;
-    bool aligned;
-    const typename E::raw* row = row_of<E>(d, r, &b, &aligned);
-    const float T = temperature_of(d, b);
-    const float s = temperature_ok(T) ? scale_of(T) : 1.0f;
-    const int tile0 = c * NT;
-    const int nt = min(NT, d.ntiles - tile0);
-    float m;
-    double D;
-    chunk_stats<E, NT, S>(row, tile0, nt, d.V, aligned, s, red, &m, &D);
-    if (threadIdx.x == 0) {
-      RowStat o;
-      o.m = m; o.pad = 0.f; o.D = D;
-      stats[t] = o;
-    }
-  }
-}
 
 // Statistics at sub-chunk granularity, one wave per sub-chunk: sub-chunk
 // g = blockIdx.x * kWaves + wave of the rows' C sub-chunks each (row g / C,
