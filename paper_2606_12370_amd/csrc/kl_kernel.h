@@ -16,7 +16,8 @@
 //                 Sf = sum f and the weighted log-ratio sum W (forward:
 //                 sum e (t - u); CE: sum e (-u)), all in float64 from the same
 //                 e, f, t, u, so the loss (formed in kl_coef) is normalised by
-//                 its own sums; for forward KL and CE also x = Z_d' - Z_t',
+//                 its own sums; for forward KL and CE, on the pairs whose
+//                 largest probabilities nearly agree, also x = Z_d' - Z_t',
 //                 the sum of 2^(b) - 2^(a) over every element, a and b its
 //                 logits less each row's largest (times s), each term from
 //                 the exact log ratio; for reverse KL the sums of f and f d
@@ -37,7 +38,8 @@
 // for bfloat16 logits, whose differences are exact there), and for forward
 // KL and CE lam_t - lam_d comes from the pairwise sum x, not from two
 // separately rounded partition functions, whose float32 error would set q - p
-// of tokens that nearly coincide in the two rows.  Then
+// of tokens that nearly coincide in the two rows (kl_needs_pairwise: only
+// where the rows' largest probabilities lie within the pair limit).  Then
 // q - p = sign(d) max(p, q) (1 - 2^-|d|), with 1 - 2^-x from its series
 // below x = 1/2 and the difference of the two probabilities above.  For
 // reverse KL the gradient is invariant under a common shift of d (mu moves
@@ -97,6 +99,7 @@ struct KlArgs {
   KlNorm* norms;         // [2 N K]
   KlPart* parts;         // [N K][C]
   float4* coef;          // [N K]: gradient constants (reverse KL), or lam_t - lam_d as hi + lo (forward KL, CE)
+  double pair_limit;     // forward KL, CE: |lam_t - lam_d| up to which x is summed pairwise
   double* loss_pos;      // [N]
   int vec_g;
 };
@@ -332,6 +335,90 @@ __device__ __forceinline__ void store_grad(float* gr, int v0, int V, bool vec, c
   }
 }
 
+// Whether a (position, step) pair needs the pairwise x of kl_pass.  lam_t -
+// lam_d = log2(max q / max p), so where it exceeds the limit the largest
+// |q - p| of the row is at least (1 - 2^-limit) of the larger maximum, and the
+// difference of the two separately summed normalisers (error a few 1e-7)
+// moves no gradient element by more than that error over (1 - 2^-limit) of
+// the row's largest (64 times it at the bfloat16 limit 1/64).  Both kl_pass
+// and kl_coef take the decision from the same stored values.
+__device__ __forceinline__ bool kl_needs_pairwise(const KlNorm& t, const KlNorm& d, double limit) {
+  return fabs(t.lam - d.lam) <= limit;
+}
+
+// One task's sums for kl_pass: Σe, Σf, the weighted log-ratio sum and, by
+// KIND, the reverse-KL complement sums or, with X, the pairwise x.
+template <class E, int NT, int S, int KIND, bool X>
+__device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
+                                             bool al_d, int tile0, int nt_tiles, int V, float s, const KlNorm& nt,
+                                             const KlNorm& nd, const KlDelta& dr, double (&v)[6]) {
+  constexpr int EPV = E::EPV;
+  double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0, xs = 0.0;
+  // 2^(z s - zmax s) = e 2^(M - zmax s): the scale of each row's elements against its largest
+  float kt = 0.f, kd = 0.f;
+  if (X) {
+    kt = static_cast<float>(exp2(static_cast<double>(nt.M) - static_cast<double>(nt.zmax) * dr.s));
+    kd = static_cast<float>(exp2(static_cast<double>(nd.M) - static_cast<double>(nd.zmax) * dr.s));
+  }
+#pragma unroll
+  for (int j0 = 0; j0 < NT; j0 += S) {
+    if (j0 >= nt_tiles) break;
+    float xt[S][EPV], xd[S][EPV];
+    load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
+    load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      // the EPV elements of one vector are summed in float32, vectors in float64
+      float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f, vx = 0.f;
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) {
+        const float tt = fmaf(xt[j][k], s, -nt.M);
+        const float uu = fmaf(xd[j][k], s, -nd.M);
+        const float e = __builtin_amdgcn_exp2f(tt);
+        const float f = __builtin_amdgcn_exp2f(uu);
+        float term;
+        if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
+        else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
+        else term = 0.f;
+        if (KIND == kKlReverse) {
+          const float dl = kl_ratio<E>(xt[j][k], xd[j][k], dr).dl;
+          const float fd = f > 0.f ? f * dl : 0.f;
+          const bool top = xd[j][k] == nd.zmax;
+          vfx += top ? 0.f : f;
+          vwx += top ? 0.f : fd;
+          vwm += top ? fd : 0.f;
+        }
+        ve += e;
+        vf += f;
+        vw += term;
+        if (X) {
+          // x = Z_d' - Z_t' from every element's 2^(b) - 2^(a), a and b its
+          // logits less the rows' largest (Z' = sum 2^(.)), each formed
+          // from the exact log ratio wf: kl_coef turns it into the log ratio
+          // of the two partition functions that the gradient pass uses
+          const float wf = kl_ratio<E>(xt[j][k], xd[j][k], dr).wf;
+          const float ea = e * kt, fb = f * kd;
+          const float mb = fmaxf(ea, fb);
+          const float xv = kl_absdiff<E>(mb, fminf(ea, fb), wf);
+          vx += mb > 0.f ? copysignf(xv, wf) : 0.f;
+        }
+      }
+      se += static_cast<double>(ve);
+      sf += static_cast<double>(vf);
+      w += static_cast<double>(vw);
+      if (KIND == kKlReverse) {
+        sfx += static_cast<double>(vfx);
+        wx += static_cast<double>(vwx);
+        wm += static_cast<double>(vwm);
+      }
+      if (X) xs += static_cast<double>(vx);
+    }
+  }
+  v[0] = se; v[1] = sf; v[2] = w;
+  v[3] = KIND == kKlReverse ? sfx : xs;
+  v[4] = wx; v[5] = wm;
+}
+
 template <class E, int NT, int S, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
@@ -350,66 +437,12 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
     const KlDelta dr = kl_delta_ref(nt, nd, s);
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
-    double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0, xs = 0.0;
-    // 2^(z s - zmax s) = e 2^(M - zmax s): the scale of each row's elements against its largest
-    const float kt = static_cast<float>(exp2(static_cast<double>(nt.M) - static_cast<double>(nt.zmax) * dr.s));
-    const float kd = static_cast<float>(exp2(static_cast<double>(nd.M) - static_cast<double>(nd.zmax) * dr.s));
-#pragma unroll
-    for (int j0 = 0; j0 < NT; j0 += S) {
-      if (j0 >= nt_tiles) break;
-      float xt[S][EPV], xd[S][EPV];
-      load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
-      load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
-#pragma unroll
-      for (int j = 0; j < S; ++j) {
-        // the EPV elements of one vector are summed in float32, vectors in float64
-        float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f, vx = 0.f;
-#pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          const float tt = fmaf(xt[j][k], s, -nt.M);
-          const float uu = fmaf(xd[j][k], s, -nd.M);
-          const float e = __builtin_amdgcn_exp2f(tt);
-          const float f = __builtin_amdgcn_exp2f(uu);
-          const KlRatio rk = kl_ratio<E>(xt[j][k], xd[j][k], dr);
-          const float dl = rk.dl;
-          float term;
-          if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
-          else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
-          else term = 0.f;
-          if (KIND == kKlReverse) {
-            const float fd = f > 0.f ? f * dl : 0.f;
-            const bool top = xd[j][k] == nd.zmax;
-            vfx += top ? 0.f : f;
-            vwx += top ? 0.f : fd;
-            vwm += top ? fd : 0.f;
-          }
-          ve += e;
-          vf += f;
-          vw += term;
-          if (KIND != kKlReverse) {
-            // x = Z_d' - Z_t' from every element's 2^(b) - 2^(a), a and b its
-            // logits less the rows' largest (Z' = sum 2^(.)), each formed
-            // from the exact log ratio wf: kl_coef turns it into the log ratio
-            // of the two partition functions that the gradient pass uses
-            const float ea = e * kt, fb = f * kd;
-            const float mb = fmaxf(ea, fb);
-            const float xv = kl_absdiff<E>(mb, fminf(ea, fb), rk.wf);
-            vx += mb > 0.f ? copysignf(xv, rk.wf) : 0.f;
-          }
-        }
-        se += static_cast<double>(ve);
-        sf += static_cast<double>(vf);
-        w += static_cast<double>(vw);
-        if (KIND == kKlReverse) {
-          sfx += static_cast<double>(vfx);
-          wx += static_cast<double>(vwx);
-          wm += static_cast<double>(vwm);
-        } else {
-          xs += static_cast<double>(vx);
-        }
-      }
-    }
-    double v[6] = {se, sf, w, KIND == kKlReverse ? sfx : xs, wx, wm};
+    double v[6];
+    // the same for the whole workgroup: one of two loop bodies runs
+    if (KIND != kKlReverse && kl_needs_pairwise(nt, nd, a.pair_limit))
+      kl_pass_sums<E, NT, S, KIND, true>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v);
+    else
+      kl_pass_sums<E, NT, S, KIND, false>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v);
     wg_sum<6>(v, red);
     if (threadIdx.x == 0) {
       KlPart o;
@@ -463,15 +496,18 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
       // log2(Z_t' / Z_d') = log2(1 - x / Z_d') with x = Z_d' - Z_t' summed
       // pairwise (Z' = 2^lam): not the difference of two separately rounded
       // sums, whose float32 error would set q - p of tokens that nearly
-      // coincide in the two rows
-      double xs = 0.0;
-      for (int cc = lane; cc < C; cc += 64) xs += ps[cc].x;
-      xs = wave_sum(xs);
+      // coincide in the two rows.  Where the two rows' largest probabilities
+      // lie far enough apart that error is harmless, and neither pass forms x.
       const KlNorm& nt = a.norms[static_cast<int64_t>(n) * K + kk];
       const KlNorm& nd = a.norms[static_cast<int64_t>(a.N) * K + static_cast<int64_t>(n) * K + kk];
       double dlam = nt.lam - nd.lam;
-      const double r = -xs * exp2(-nd.lam);
-      if (r > -1.0 && r < INFINITY && dlam - dlam == 0.0) dlam = log1p(r) * (1.0 / kLn2D);
+      if (kl_needs_pairwise(nt, nd, a.pair_limit)) {  // the same for the whole wave
+        double xs = 0.0;
+        for (int cc = lane; cc < C; cc += 64) xs += ps[cc].x;
+        xs = wave_sum(xs);
+        const double r = -xs * exp2(-nd.lam);
+        if (r > -1.0 && r < INFINITY && dlam - dlam == 0.0) dlam = log1p(r) * (1.0 / kLn2D);
+      }
       if (lane == 0) {
         const float hi = static_cast<float>(dlam);
         a.coef[static_cast<int64_t>(n) * K + kk] =

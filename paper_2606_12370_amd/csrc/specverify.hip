@@ -989,6 +989,11 @@ spec_status spec_kl_loss_fwd_bwd(const void* target_logits, int64_t t_stride_n, 
   a.parts = reinterpret_cast<sv::KlPart*>(ws + L.parts);
   a.coef = reinterpret_cast<float4*>(ws + L.coef);
   a.loss_pos = reinterpret_cast<double*>(ws + L.loss);
+  // lam_t - lam_d = log2(max q / max p); beyond the limit the separately
+  // summed normalisers (error a few 1e-7) move the gradient by at most
+  // 64 (bfloat16) or 3.4 (float32) times that error against the row's
+  // largest |q - p|, far inside the tolerances (2e-3, 1e-5)
+  a.pair_limit = dtype == SPEC_BF16 ? 1.0 / 64 : 0.5;
   a.vec_g = (grad_draft && aligned16(grad_draft) && (V % 4 == 0)) ? 1 : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   return dtype == SPEC_BF16 ? launch_kl_kind<BF16, kNtBf16>(a, s) : launch_kl_kind<F32, kNtF32>(a, s);

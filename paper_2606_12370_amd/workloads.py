@@ -181,14 +181,19 @@ def greedy_ids(draft, dtype):
 
 
 def tv_inputs_numpy(N, K, V, dtype, seed, noise=1.0, q_equals_p=False):
-    """Host-side TV-loss inputs: target [N, K, V], draft [N, K, V]."""
+    """Host-side TV-loss inputs: target [N, K, V], draft [N, K, V].
+
+    noise: the standard deviation of the draft's perturbation, one value or
+    one per position (a length-N sequence).
+    """
     rng = np.random.default_rng(seed)
     s = rng.uniform(1.0, 8.0, size=N).astype(np.float32)
     tgt = _store(rng.standard_normal((N, K, V), dtype=np.float32) * s[:, None, None], dtype)
     if q_equals_p:
         drf = tgt.copy()
     else:
-        nz = rng.standard_normal((N, K, V), dtype=np.float32) * np.float32(noise)
+        sd = np.float32(noise) if np.ndim(noise) == 0 else np.asarray(noise, dtype=np.float32).reshape(N, 1, 1)
+        nz = rng.standard_normal((N, K, V), dtype=np.float32) * sd
         drf = _store(to_float64(tgt, dtype).astype(np.float32) + nz, dtype)
     return dict(target=tgt, draft=drf, dtype=dtype, N=N, K=K, V=V, temperature=1.0)
 

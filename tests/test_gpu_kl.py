@@ -60,6 +60,30 @@ def test_nearly_equal_distributions(noise):
         print(kind, noise, rep, "min KL", float(ref["per_step"].min()))
 
 
+PAIR_LIMIT = {W.BF16: 1.0 / 64, W.F32: 0.5}
+
+
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+@pytest.mark.parametrize("seed", [31, 32])
+def test_pairwise_limit_both_sides(dtype, seed):
+    """Forward KL and CE sum the partition-function difference pairwise only
+    for pairs whose largest probabilities lie within a limit of each other
+    (|log2(max q / max p)| at most 1/64 for bfloat16 logits, 1/2 for float32);
+    beyond it they take the difference of the two normalisers.  Positions with
+    draft noise from 0.003 to 2 put pairs on both sides of the limit."""
+    N = 48
+    d = W.tv_inputs_numpy(N, 2, 6000, dtype, seed, noise=np.logspace(-2.5, 0.3, N))
+    zt, zd = W.to_float64(d["target"], dtype), W.to_float64(d["draft"], dtype)
+    lam = lambda z: np.log2(np.exp(z - z.max(-1, keepdims=True)).sum(-1))
+    dl = np.abs(lam(zt) - lam(zd))
+    lim = PAIR_LIMIT[dtype]
+    assert ((dl > lim / 2) & (dl <= lim)).sum() >= 2 and ((dl > lim) & (dl <= 2 * lim)).sum() >= 2
+    for kind in ("forward", "ce"):
+        loss, ps, grad, ref = run_case(d, kind)
+        rep = compare_kl(loss, ps, grad, ref, dtype)
+        print(kind, dtype, seed, rep)
+
+
 def test_forward_only_q_equals_p_and_determinism():
     d = W.tv_inputs_numpy(6, 3, 30000, W.BF16, 4)
     loss, ps, grad, ref = run_case(d, "ce", want_grad=False)
