@@ -34,10 +34,14 @@ functions:
   Z_t' = sum_v e^(zt_v / T - max zt / T),  X = Z_d' - Z_t' = sum_v e^(zt_v / T - max zt / T) (e^(w_v) - 1),
 
 with e^w - 1 and log(1 + x) evaluated by expm1 and log1p, and
-q - p = p (e^(log q - log p) - 1).  For reverse KL the draft's single
-largest element takes log q - log p - L as sum over the other elements u of
-q_u (d - d_u), d = log q - log p (the q_u sum to 1), which keeps it accurate
-where that element holds nearly all of q.  Results are returned as float64.
+q - p = p (e^(log q - log p) - 1).  For reverse KL, with d = log q - log p
+and the q_u summing to 1, d_v - L = (d_v - d_r) + sum_u q_u (d_r - d_u) for
+any element r; r is the draft's first largest element and each d_v - d_r =
+((zd_v - zt_v) - (zd_r - zt_r)) / T comes from the logits (the partition
+functions cancel), so no term is a small difference of two large log ratios
+where the draft's mass sits on tokens whose log ratios nearly agree (one
+token holding nearly all of q, or several with nearly equal d).  Results
+are returned as float64.
 """
 
 import numpy as np
@@ -83,20 +87,17 @@ def kl_ref(target_logits, draft_logits, temperature, kind, scale=1.0):
         elif kind == KIND_REVERSE:
             qdl = np.where(q > 0, q * dl, XP(0))
             L = qdl.sum(axis=-1)
-            g = np.where(q > 0, q * (dl - L[..., None]), XP(0))
-            # the draft's single largest element: dl - L = sum over the other
-            # elements u of q_u (dl - dl_u) (the q_u sum to 1), which does
-            # not cancel when that element holds nearly all of q
-            top = np.argmax(zd, axis=-1)[..., None]
-            single = (zd == np.max(zd, axis=-1, keepdims=True)).sum(axis=-1, keepdims=True) == 1
-            dl_top = np.take_along_axis(dl, top, axis=-1)
-            q_top = np.take_along_axis(q, top, axis=-1)
-            others = np.ones(zd.shape, dtype=bool)
-            np.put_along_axis(others, top, False, axis=-1)
-            comp = np.where(others & (q > 0), q * (dl_top - dl), XP(0)).sum(axis=-1, keepdims=True)
-            g_top = np.where(single & np.isfinite(dl_top), q_top * comp, np.take_along_axis(g, top, axis=-1))
-            np.put_along_axis(g, top, g_top, axis=-1)
-            g = g / T
+            # dl_v - L = (dl_v - dl_r) + sum_u q_u (dl_r - dl_u), r the
+            # draft's first largest element, dl_v - dl_r from the logits;
+            # rows where that sum is not finite (a token with p = 0 and
+            # q > 0) keep q (dl - L)
+            r = np.argmax(zd, axis=-1)[..., None]
+            x = (np.asarray(zd, dtype=XP) - np.asarray(zt, dtype=XP)) / T
+            dv = x - np.take_along_axis(x, r, axis=-1)
+            comp = np.where(q > 0, -q * dv, XP(0)).sum(axis=-1, keepdims=True)
+            g_ref = np.where(q > 0, q * (dv + comp), XP(0))
+            g_plain = np.where(q > 0, q * (dl - L[..., None]), XP(0))
+            g = np.where(np.isfinite(comp), g_ref, g_plain) / T
         else:
             raise ValueError(kind)
     loss_pos = L.mean(axis=1)

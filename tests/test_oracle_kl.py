@@ -136,14 +136,30 @@ def _case_two_tokens_shifted(rng):
     return zt, zd, 0.53
 
 
-@pytest.mark.parametrize("case", [_case_dominant_1e8, _case_dominant_1e14, _case_two_tokens_shifted])
+def _case_equal_log_ratios_far_below_target(rng):
+    # the draft holds nearly all its mass on two tokens (q about 1 and
+    # e^-12) whose log ratios log q - log p agree exactly, both rated about
+    # e^-50 below the target's largest: log q - log p - L of the second token
+    # is a difference of two numbers near 53 that agree to about 1e-19
+    V = 1024
+    zt = rng.normal(0.0, 2.0, size=(1, 1, V))
+    zd = rng.normal(0.0, 2.0, size=(1, 1, V))
+    zt[0, 0, 100], zd[0, 0, 100] = -20.0, 30.0
+    zt[0, 0, 700], zd[0, 0, 700] = -26.0, 24.0
+    return zt, zd, 0.5
+
+
+@pytest.mark.parametrize("case", [_case_dominant_1e8, _case_dominant_1e14, _case_two_tokens_shifted,
+                                  _case_equal_log_ratios_far_below_target])
 def test_near_coincident_gradients_against_50_digit_arithmetic(case):
     """Rows where the gradient is a small difference of nearly equal
     quantities: one token holding all but 4e-10 or 1e-14 of both
     distributions ((q - p) / T of that token is a difference of two numbers
     that close to 1), and two tokens sharing the mass with the draft's two
     logits shifted by one constant (log q - log p of each is the small
-    difference of the two log partition functions).  The oracle's forward-KL
+    difference of the two log partition functions), and two draft tokens
+    whose log ratios agree exactly, far below the target's mass (reverse KL's
+    log q - log p - L of the lesser one cancels to 1e-19).  The oracle's forward-KL
     and reverse-KL gradients equal an evaluation in 50-digit arithmetic
     (mpmath), element by element, to 1e-9 of the row's largest gradient."""
     mpmath = pytest.importorskip("mpmath")
