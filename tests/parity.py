@@ -362,6 +362,11 @@ def compare_sample_gumbel(tokens, ref, rows=None):
 
 
 KL_ABS = 1e-6
+# The float32 gradient cannot hold the contributions of probabilities below
+# float32's normal range (2^-126; a row's exponentials there underflow), so a
+# row whose exact gradient lies entirely below 2^-100 is measured against
+# 2^-100 rather than against its own largest element.
+KL_GRAD_FLOOR = 2.0 ** -100
 
 
 def compare_kl(loss_g, ps_g, grad_g, ref, dtype, positions=None, loss_exact=True):
@@ -369,7 +374,7 @@ def compare_kl(loss_g, ps_g, grad_g, ref, dtype, positions=None, loss_exact=True
     (the absolute term covers the float32 rounding of the log-ratios, about
     1e-7 of the log partition functions, which no longer cancels when the two
     distributions nearly coincide); the gradient norm-wise per (position,
-    step) row within tol."""
+    step) row within tol, the row's scale at least KL_GRAD_FLOOR."""
     tol = TOL[dtype]
     out = {}
     if ps_g is not None:
@@ -389,7 +394,7 @@ def compare_kl(loss_g, ps_g, grad_g, ref, dtype, positions=None, loss_exact=True
             g = g[torch.as_tensor(positions, device=g.device)]
         g = g.cpu().numpy().astype(np.float64)
         gr = ref["grad"]
-        scale = np.maximum(np.abs(gr).max(axis=-1), 1e-300)
+        scale = np.maximum(np.abs(gr).max(axis=-1), KL_GRAD_FLOOR)
         worst = float((np.abs(g - gr).max(axis=-1) / scale).max())
         assert worst <= tol, "gradient norm-wise relative error %.3e" % worst
         out["max_normwise_grad"] = worst
