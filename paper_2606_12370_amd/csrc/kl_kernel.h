@@ -11,6 +11,9 @@
 //                 the logarithm of a float32 sum near 1.
 //   2 kl_norm     each row's log2 partition function in float64 and its
 //                 per-element reference.
+//     kl_top      reverse KL, per draft row: the target's logit at the
+//                 row's first largest logit (a scan of the one sub-chunk
+//                 that holds it).
 //   3 kl_pass     per (position n, step k, chunk), with t = z_t s - M_t and
 //                 u = z_d s - M_d (log2 units), e = 2^t, f = 2^u: Se = sum e,
 //                 Sf = sum f and the weighted log-ratio sum W (forward:
@@ -20,14 +23,13 @@
 //                 largest probabilities nearly agree, also x = Z_d' - Z_t',
 //                 the sum of 2^(b) - 2^(a) over every element, a and b its
 //                 logits less each row's largest (times s), each term from
-//                 the exact log ratio; for reverse KL the sums of f and f d
-//                 over the elements other than the draft's largest logit,
-//                 and of f d over those, with d = log2 q - log2 p.
+//                 the exact log ratio; for reverse KL the sum of f (d - c),
+//                 d = log2 q - log2 p and c its value at the draft's first
+//                 largest logit, each d - c from exact logit differences.
 //   4 kl_coef     per position: L_{n,k} from its chunks, the per-step output,
 //                 the position loss, and the gradient constants: for forward
 //                 KL and CE lam_t - lam_d = log2(Z_t' / Z_d') =
-//                 log2(1 - x / Z_d'), for reverse KL mu and the complement
-//                 constants.
+//                 log2(1 - x / Z_d'), for reverse KL mu - c.
 //   5 kl_grad     every kind: the gradient, reading the pair again.
 //   6 kl_loss     position losses added in a fixed order.
 //
@@ -42,11 +44,13 @@
 // where the rows' largest probabilities lie within the pair limit).  Then
 // q - p = sign(d) max(p, q) (1 - 2^-|d|), with 1 - 2^-x from its series
 // below x = 1/2 and the difference of the two probabilities above.  For
-// reverse KL the gradient is invariant under a common shift of d (mu moves
-// with it); the term log q_j - log p_j - L of the element holding nearly all
-// of q is a difference of two nearly equal numbers; with L = ln2 sum_i q_i d_i
-// and sum_i q_i = 1 it equals ln2 sum_{i != j} q_i (d_j - d_i), which is
-// formed from the sums over the other elements instead.
+// reverse KL the gradient q (d - mu) ln2 is invariant under a common shift of
+// d (mu moves with it), so every log ratio is taken against c, its value at
+// the draft's first largest logit: d - c = ((z_d - z_t) - (zmax_d - z_t at
+// that logit)) s from exact logit differences, without the normalisers, and
+// mu - c = sum_i q_i (d_i - c).  Where the draft's mass sits on tokens whose
+// log ratios nearly agree, d - mu is then a difference of two small numbers
+// rather than of two large ones.
 #pragma once
 
 #include <type_traits>
@@ -80,12 +84,12 @@ struct KlNorm {
   int n;
   double lam;  // log2(n + R 2^-(zmax s - M)) = log2 Z - zmax s
   double D;
+  float zo;    // reverse KL, draft rows: the target's logit at the row's first largest logit (kl_top)
 };
 
 struct KlPart {  // one chunk of a (position, step) pair
   double se, sf, w;
-  double sfx, wx, wm;  // reverse KL: sum f, sum f d over the non-largest draft elements; sum f d over the largest
-  double x;            // forward KL / CE: Z_d' - Z_t', the sum of 2^(b) - 2^(a) (see kl_pass)
+  double x;  // forward KL / CE: Z_d' - Z_t', the sum of 2^(b) - 2^(a); reverse KL: sum f (d - c) (see kl_pass)
 };
 
 struct KlArgs {
@@ -98,7 +102,7 @@ struct KlArgs {
   int SC;                // sub-chunks per row of the statistics pass
   KlNorm* norms;         // [2 N K]
   KlPart* parts;         // [N K][C]
-  float4* coef;          // [N K]: gradient constants (reverse KL), or lam_t - lam_d as hi + lo (forward KL, CE)
+  float4* coef;          // [N K]: reverse KL the gradient factor and mu - c; forward KL, CE lam_t - lam_d as hi + lo
   double pair_limit;     // forward KL, CE: |lam_t - lam_d| up to which x is summed pairwise
   double* loss_pos;      // [N]
   int vec_g;
@@ -244,7 +248,58 @@ __global__ __launch_bounds__(kThreads) void kl_norm_kernel(const KlStat* __restr
     o.lam = log2(nn) + log1p(R / (nn * mt)) * kLog2eD;
     if (nan) { o.D = NAN; o.lam = NAN; }
     o.invD = static_cast<float>(1.0 / o.D);
+    o.zo = NAN;
     out[r] = o;
+  }
+}
+
+// Reverse KL, one wave per (position, step): the target's logit at the
+// draft row's first largest logit, into the draft row's norm.  The scan
+// reads the first sub-chunk (SUB elements) whose statistics hold the row's
+// largest logit.  Where no element matches (a row of NaN), the target's
+// largest logit stands in: any finite reference gives the same gradient up
+// to rounding.
+template <class E, int SUB, int S>
+__global__ __launch_bounds__(kThreads) void kl_top_kernel(RowsDesc d, const KlStat* __restrict__ stats, int SC,
+                                                          KlNorm* __restrict__ norms, int NK) {
+  constexpr int EPV = E::EPV;
+  static_assert(SUB % (S * 64 * EPV) == 0, "whole load steps per sub-chunk");
+  const int lane = threadIdx.x & 63;
+  const int u = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (u >= NK) return;
+  const float zm = norms[NK + u].zmax;
+  const KlStat* st = stats + static_cast<int64_t>(NK + u) * SC;
+  int c0 = SC;
+  for (int c = lane; c < SC; c += 64)
+    if (st[c].zmax == zm) c0 = min(c0, c);
+  c0 = wave_min_int(c0);
+  int idx = d.V;
+  if (c0 < SC) {
+    int b;
+    bool al;
+    const typename E::raw* rd = row_of<E>(d, NK + u, &b, &al);
+    const int e0 = c0 * SUB, e1 = min(d.V, e0 + SUB);
+    for (int es = e0; es < e1; es += S * 64 * EPV) {
+      float x[S][EPV];
+      load_span<E, S, 64>(rd, es, lane, d.V, al, x);
+#pragma unroll
+      for (int j = 0; j < S; ++j)
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) {
+          const int e = es + j * 64 * EPV + lane * EPV + k;
+          if (x[j][k] == zm && e < e1) idx = min(idx, e);
+        }
+    }
+    idx = wave_min_int(idx);
+  }
+  if (lane == 0) {
+    float zo = norms[u].zmax;
+    if (idx < d.V) {
+      int b;
+      bool al;
+      zo = E::one(row_of<E>(d, u, &b, &al) + idx);
+    }
+    norms[NK + u].zo = zo;
   }
 }
 
@@ -276,6 +331,20 @@ __device__ __forceinline__ KlDelta kl_delta_ref(const KlNorm& t, const KlNorm& d
   r.c1f = static_cast<float>(r.c1);
   r.lam_hi = static_cast<float>(r.lam);
   r.lam_lo = static_cast<float>(r.lam - static_cast<double>(r.lam_hi));
+  r.sf = s;
+  return r;
+}
+
+// Reverse KL: d - c = ((z_d - z_t) - (zmax_d - zo)) s, zo the target's logit
+// at the draft's first largest logit, as the wf of kl_ratio (no normalisers).
+__device__ __forceinline__ KlDelta kl_delta_top(const KlNorm& d, float s) {
+  KlDelta r;
+  r.c1 = static_cast<double>(d.zmax) - static_cast<double>(d.zo);
+  r.lam = 0.0;
+  r.s = static_cast<double>(s);
+  r.c1f = static_cast<float>(r.c1);
+  r.lam_hi = 0.f;
+  r.lam_lo = 0.f;
   r.sf = s;
   return r;
 }
@@ -347,13 +416,14 @@ __device__ __forceinline__ bool kl_needs_pairwise(const KlNorm& t, const KlNorm&
 }
 
 // One task's sums for kl_pass: Σe, Σf, the weighted log-ratio sum and, by
-// KIND, the reverse-KL complement sums or, with X, the pairwise x.
+// KIND, the reverse-KL sum of f (d - c) (dr: kl_delta_top) or, with X, the
+// pairwise x.
 template <class E, int NT, int S, int KIND, bool X>
 __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
                                              bool al_d, int tile0, int nt_tiles, int V, float s, const KlNorm& nt,
-                                             const KlNorm& nd, const KlDelta& dr, double (&v)[6]) {
+                                             const KlNorm& nd, const KlDelta& dr, double (&v)[4]) {
   constexpr int EPV = E::EPV;
-  double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0, xs = 0.0;
+  double se = 0.0, sf = 0.0, w = 0.0, xs = 0.0;
   // 2^(z s - zmax s) = e 2^(M - zmax s): the scale of each row's elements against its largest
   float kt = 0.f, kd = 0.f;
   if (X) {
@@ -369,7 +439,7 @@ __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_
 #pragma unroll
     for (int j = 0; j < S; ++j) {
       // the EPV elements of one vector are summed in float32, vectors in float64
-      float ve = 0.f, vf = 0.f, vw = 0.f, vfx = 0.f, vwx = 0.f, vwm = 0.f, vx = 0.f;
+      float ve = 0.f, vf = 0.f, vw = 0.f, vx = 0.f;
 #pragma unroll
       for (int k = 0; k < EPV; ++k) {
         const float tt = fmaf(xt[j][k], s, -nt.M);
@@ -381,12 +451,8 @@ __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_
         else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
         else term = 0.f;
         if (KIND == kKlReverse) {
-          const float dl = kl_ratio<E>(xt[j][k], xd[j][k], dr).dl;
-          const float fd = f > 0.f ? f * dl : 0.f;
-          const bool top = xd[j][k] == nd.zmax;
-          vfx += top ? 0.f : f;
-          vwx += top ? 0.f : fd;
-          vwm += top ? fd : 0.f;
+          const float dc = kl_ratio<E>(xt[j][k], xd[j][k], dr).wf;
+          vx += f > 0.f ? f * dc : 0.f;
         }
         ve += e;
         vf += f;
@@ -406,24 +472,17 @@ __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_
       se += static_cast<double>(ve);
       sf += static_cast<double>(vf);
       w += static_cast<double>(vw);
-      if (KIND == kKlReverse) {
-        sfx += static_cast<double>(vfx);
-        wx += static_cast<double>(vwx);
-        wm += static_cast<double>(vwm);
-      }
-      if (X) xs += static_cast<double>(vx);
+      if (KIND == kKlReverse || X) xs += static_cast<double>(vx);
     }
   }
-  v[0] = se; v[1] = sf; v[2] = w;
-  v[3] = KIND == kKlReverse ? sfx : xs;
-  v[4] = wx; v[5] = wm;
+  v[0] = se; v[1] = sf; v[2] = w; v[3] = xs;
 }
 
 template <class E, int NT, int S, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
-  __shared__ RedLds<6> red;
+  __shared__ RedLds<4> red;
   const RowsDesc& d = a.rows;
   const int C = d.C, V = d.V, NK = a.N * a.K;
   for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
@@ -434,22 +493,19 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
     const typename E::raw* rd = row_of<E>(d, NK + u, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
     const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
-    const KlDelta dr = kl_delta_ref(nt, nd, s);
+    const KlDelta dr = KIND == kKlReverse ? kl_delta_top(nd, s) : kl_delta_ref(nt, nd, s);
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
-    double v[6];
+    double v[4];
     // the same for the whole workgroup: one of two loop bodies runs
     if (KIND != kKlReverse && kl_needs_pairwise(nt, nd, a.pair_limit))
       kl_pass_sums<E, NT, S, KIND, true>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v);
     else
       kl_pass_sums<E, NT, S, KIND, false>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v);
-    wg_sum<6>(v, red);
+    wg_sum<4>(v, red);
     if (threadIdx.x == 0) {
       KlPart o;
-      o.se = v[0]; o.sf = v[1]; o.w = v[2];
-      o.sfx = KIND == kKlReverse ? v[3] : 0.0;
-      o.wx = v[4]; o.wm = v[5];
-      o.x = KIND == kKlReverse ? 0.0 : v[3];
+      o.se = v[0]; o.sf = v[1]; o.w = v[2]; o.x = v[3];
       a.parts[t] = o;
     }
   }
@@ -464,29 +520,34 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
   const int C = a.rows.C, K = a.K;
   double Ln = 0.0;
   for (int kk = 0; kk < K; ++kk) {
-    double se = 0.0, sf = 0.0, w = 0.0, sfx = 0.0, wx = 0.0, wm = 0.0;
+    double se = 0.0, sf = 0.0, w = 0.0;
     const KlPart* ps = a.parts + static_cast<int64_t>(n * K + kk) * C;
     for (int cc = lane; cc < C; cc += 64) {
       se += ps[cc].se; sf += ps[cc].sf; w += ps[cc].w;
-      sfx += ps[cc].sfx; wx += ps[cc].wx; wm += ps[cc].wm;
     }
     se = wave_sum(se);
     sf = wave_sum(sf);
     w = wave_sum(w);
     double L;  // nats
+    const KlNorm& nt = a.norms[static_cast<int64_t>(n) * K + kk];
+    const KlNorm& nd = a.norms[static_cast<int64_t>(a.N) * K + static_cast<int64_t>(n) * K + kk];
     if (a.kind == kKlReverse) {
-      sfx = wave_sum(sfx);
-      wx = wave_sum(wx);
-      wm = wave_sum(wm);
-      // L = ln2 sum_j q_j d_j with q_j = f_j / Sf
-      const double mu = (wx + wm) / sf;
-      L = kLn2D * mu;
+      double xc = 0.0;
+      for (int cc = lane; cc < C; cc += 64) xc += ps[cc].x;
+      xc = wave_sum(xc);
+      // L = ln2 mu, mu = sum_j q_j d_j with q_j = f_j / Sf, taken as
+      // c + (mu - c): c = d at the draft's first largest logit =
+      // (zmax_t - zo) s + lam_t - lam_d, mu - c = sum_j f_j (d_j - c) / Sf
+      const double mc = xc / sf;
+      const double c = (static_cast<double>(nt.zmax) - static_cast<double>(nd.zo)) *
+                           static_cast<double>(scale_of(a.rows.temp_scalar)) +
+                       (nt.lam - nd.lam);
+      L = kLn2D * (c + mc);
       if (lane == 0) {
-        // gradient: scale/(K T) q (ln2 (d - mu)), or, for the draft's single
-        // largest element, scale/(K T) q ln2 (d Sfx - Wx) / Sf
+        // gradient: scale/(K T) q ln2 ((d - c) - (mu - c))
         const double A = a.scale * static_cast<double>(a.inv_t) / K * kLn2D / sf;
-        a.coef[static_cast<int64_t>(n) * K + kk] = make_float4(static_cast<float>(A), static_cast<float>(mu),
-                                                               static_cast<float>(sfx / sf), static_cast<float>(wx / sf));
+        a.coef[static_cast<int64_t>(n) * K + kk] =
+            make_float4(static_cast<float>(A), static_cast<float>(mc), 0.f, 0.f);
       }
     } else {
       const double le = log2(se), lf = log2(sf);
@@ -498,8 +559,6 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
       // sums, whose float32 error would set q - p of tokens that nearly
       // coincide in the two rows.  Where the two rows' largest probabilities
       // lie far enough apart that error is harmless, and neither pass forms x.
-      const KlNorm& nt = a.norms[static_cast<int64_t>(n) * K + kk];
-      const KlNorm& nd = a.norms[static_cast<int64_t>(a.N) * K + static_cast<int64_t>(n) * K + kk];
       double dlam = nt.lam - nd.lam;
       if (kl_needs_pairwise(nt, nd, a.pair_limit)) {  // the same for the whole wave
         double xs = 0.0;
@@ -523,8 +582,7 @@ __global__ __launch_bounds__(kThreads) void kl_coef_kernel(KlArgs a) {
 // The gradient pass.  Forward KL and CE: (q - p) scale / (K T) =
 // sign(d) |q - p| scale / (K T), d = log2 q - log2 p formed with the
 // pairwise partition-function ratio of kl_coef.  Reverse KL: scale / (K T)
-// q ln2 (d - mu), or for the draft's single largest element
-// scale / (K T) q ln2 (d Sfx - Wx) / Sf.
+// q ln2 ((d - c) - (mu - c)).
 template <class E, int NT, int S, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
@@ -540,10 +598,9 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
     const typename E::raw* rd = row_of<E>(d, NK + u, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
     const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
-    KlDelta dr = kl_delta_ref(nt, nd, s);
+    KlDelta dr = KIND == kKlReverse ? kl_delta_top(nd, s) : kl_delta_ref(nt, nd, s);
     const float4 A = a.coef[u];
     if (KIND != kKlReverse) kl_delta_set_lam(dr, static_cast<double>(A.x) + static_cast<double>(A.y));
-    const bool single_top = nd.n == 1;
     float* gr = a.grad + static_cast<int64_t>(u) * V;
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
@@ -559,11 +616,12 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
 #pragma unroll
         for (int k = 0; k < EPV; ++k) {
           const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
-          const float dl = kl_ratio<E>(xt[j][k], xd[j][k], dr).dl;
+          const KlRatio rk = kl_ratio<E>(xt[j][k], xd[j][k], dr);
           if constexpr (KIND == kKlReverse) {
-            const float tm = (single_top && xd[j][k] == nd.zmax) ? fmaf(dl, A.z, -A.w) : dl - A.y;
+            const float tm = rk.wf - A.y;  // (d - c) - (mu - c)
             gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
           } else {
+            const float dl = rk.dl;
             const float e = __builtin_amdgcn_exp2f(fmaf(xt[j][k], s, -nt.M));
             const float pe = e * nt.invD, qf = f * nd.invD;
             const float mx = fmaxf(pe, qf);

@@ -463,6 +463,13 @@ spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(sv::kl_norm_kernel, dim3(static_cast<unsigned>((2 * units + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, static_cast<const sv::KlStat*>(a.stats), static_cast<int>(2 * units),
                      a.SC, sv::scale_of(a.rows.temp_scalar), a.norms);
+  if (KIND == sv::kKlReverse) {
+    // the reference logit of the reverse-KL log ratios (one sub-chunk read per draft row)
+    constexpr int kSub = kStep * sv::kThreads * E::EPV;
+    hipLaunchKernelGGL((sv::kl_top_kernel<E, kSub, 4>), dim3(static_cast<unsigned>((units + sv::kWaves - 1) / sv::kWaves)),
+                       dim3(sv::kThreads), 0, s, a.rows, static_cast<const sv::KlStat*>(a.stats), a.SC, a.norms,
+                       static_cast<int>(units));
+  }
   // the gradient pass reads bf16 as 4-element vectors, so that each lane
   // writes one float4; so does the forward-KL / CE statistics pass (with
   // 16-byte vectors it needs 124 VGPRs and measured 11.0 against 9.8 ms at

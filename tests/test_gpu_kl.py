@@ -84,6 +84,37 @@ def test_pairwise_limit_both_sides(dtype, seed):
         print(kind, dtype, seed, rep)
 
 
+def dominant_pair_inputs(dtype, seed, N=6, K=2, V=1024):
+    """Rows whose draft puts nearly all its mass on two tokens a, b that the
+    target rates about e^-27 below its largest, with log ratios
+    d = log q - log p that differ by only eps / T between a and b (d itself
+    about 27 / T): the reverse-KL gradient q (d - mu) of both is then a small
+    difference of two large log ratios.  eps is exact in the storage type;
+    row (n, 5) holds an exact tie of the two draft logits."""
+    rng = np.random.default_rng(seed)
+    zt = (rng.standard_normal((N, K, V)) * 2.0).astype(np.float32)
+    zd = (rng.standard_normal((N, K, V)) * 2.0).astype(np.float32)
+    eps = [0.01, 0.001, 0.03, 0.1, 0.0, 0.02] if dtype == W.F32 else [0.125, 0.25, 0.0, 0.5, 0.125, 0.25]
+    for n in range(N):
+        for k in range(K):
+            a, b = rng.choice(V, 2, replace=False)
+            gap = [1.0, 2.0, 3.0, 4.0, 6.0, 0.0][n]
+            e = eps[(n + k) % len(eps)]
+            zt[n, k, a], zd[n, k, a] = -20.0, 30.0
+            zt[n, k, b], zd[n, k, b] = -20.0 - gap - e, 30.0 - gap
+    store = (lambda x: W.f32_to_bf16_bits(x)) if dtype == W.BF16 else (lambda x: x)
+    return dict(target=store(zt), draft=store(zd), dtype=dtype, N=N, K=K, V=V)
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("T", [1.0, 0.5])
+def test_reverse_kl_dominant_tokens_with_close_log_ratios(dtype, T):
+    d = dominant_pair_inputs(dtype, 41 if T == 1.0 else 42)
+    for kind in ("reverse", "forward"):
+        loss, ps, grad, ref = run_case(d, kind, T)
+        print(kind, dtype, T, compare_kl(loss, ps, grad, ref, dtype))
+
+
 def test_forward_only_q_equals_p_and_determinism():
     d = W.tv_inputs_numpy(6, 3, 30000, W.BF16, 4)
     loss, ps, grad, ref = run_case(d, "ce", want_grad=False)

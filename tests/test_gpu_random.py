@@ -172,6 +172,21 @@ KL_PINNED = [
     (W.BF16, 21, 4, 1024, "ce", 0.5368787480304352, 1.0 / 21, 1952651588, 0.06469459190593548),
     # one token holding all but 1e-14 of both distributions
     (W.F32, 15, 3, 1024, "forward", 0.5975192604769664, 1.0, 831808222, 1.319960033772397),
+    # draft noise per position up to 18-92 (draft logits in the hundreds): rows whose exact
+    # gradient lies below float32's range, and reverse KL where the draft's leading tokens
+    # have nearly equal log ratios
+    (W.BF16, 4, 3, 16383, "reverse", 1.46381765942616, 0.25, 1732116239,
+     [0.08311337671380507, 0.827313912110449, 8.235116129721746, 81.97267890371153]),
+    (W.BF16, 12, 2, 1024, "reverse", 0.6184885680468026, 1.0 / 12, 763233859,
+     list(np.logspace(np.log10(0.0672955349239528), np.log10(41.74713811512776), 12))),
+    (W.F32, 16, 8, 1024, "reverse", 0.7918173928408779, 0.25, 302259778,
+     list(np.logspace(np.log10(0.09885397484826319), np.log10(91.54849261054336), 16))),
+    (W.F32, 7, 7, 1024, "reverse", 0.5040757477292378, 0.25, 165275283,
+     list(np.logspace(np.log10(0.09873318975182539), np.log10(18.93387516804222), 7))),
+    (W.F32, 8, 1, 16385, "reverse", 0.9818716294638743, 0.25, 416231049,
+     list(np.logspace(np.log10(0.053817650185256485), np.log10(48.11081547835813), 8))),
+    (W.BF16, 14, 6, 1024, "reverse", 0.5128602475661578, 1.0 / 14, 156701734,
+     list(np.logspace(np.log10(0.09527860944217414), np.log10(32.25606597973363), 14))),
 ]
 
 
