@@ -23,14 +23,16 @@
 //                 largest probabilities nearly agree, also x = Z_d' - Z_t',
 //                 the sum of 2^(b) - 2^(a) over every element, a and b its
 //                 logits less each row's largest (times s), each term from
-//                 the exact log ratio; for reverse KL the sum of f (d - c),
+//                 the exact log ratio, and on the other pairs the gradient,
+//                 written here; for reverse KL the sum of f (d - c),
 //                 d = log2 q - log2 p and c its value at the draft's first
 //                 largest logit, each d - c from exact logit differences.
 //   4 kl_coef     per position: L_{n,k} from its chunks, the per-step output,
 //                 the position loss, and the gradient constants: for forward
 //                 KL and CE lam_t - lam_d = log2(Z_t' / Z_d') =
 //                 log2(1 - x / Z_d'), for reverse KL mu - c.
-//   5 kl_grad     every kind: the gradient, reading the pair again.
+//   5 kl_grad     the gradient, reading the pair again: every reverse-KL
+//                 pair, and the forward-KL / CE pairs within the pair limit.
 //   6 kl_loss     position losses added in a fixed order.
 //
 // Where p and q nearly agree, q - p and log q - log p are small differences
@@ -388,6 +390,17 @@ __device__ __forceinline__ float kl_delta(float zt, float zd, const KlDelta& r) 
   return static_cast<float>(fma((static_cast<double>(zd) - static_cast<double>(zt)) - r.c1, r.s, r.lam));
 }
 
+// Forward KL / CE gradient of one element: sign(d) |q - p| scale / (K T)
+// from e = 2^(z_t s - M_t), f = 2^(z_d s - M_d) and d = log2 q - log2 p.
+template <class E>
+__device__ __forceinline__ float kl_fwd_grad(float e, float f, float dl, const KlNorm& nt, const KlNorm& nd,
+                                             float gcoef) {
+  const float pe = e * nt.invD, qf = f * nd.invD;
+  const float mx = fmaxf(pe, qf);
+  const float g = kl_absdiff<E>(mx, fminf(pe, qf), dl);
+  return mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
+}
+
 // Write EPV gradient values of one vector (float4 stores when aligned).
 template <int EPV>
 __device__ __forceinline__ void store_grad(float* gr, int v0, int V, bool vec, const float (&gv)[EPV]) {
@@ -417,12 +430,15 @@ __device__ __forceinline__ bool kl_needs_pairwise(const KlNorm& t, const KlNorm&
 
 // One task's sums for kl_pass: Σe, Σf, the weighted log-ratio sum and, by
 // KIND, the reverse-KL sum of f (d - c) (dr: kl_delta_top) or, with X, the
-// pairwise x.
-template <class E, int NT, int S, int KIND, bool X>
+// pairwise x.  With GW (forward KL / CE beyond the pair limit, dr carrying
+// lam_t - lam_d of the two normalisers) the task also writes its gradient.
+template <class E, int NT, int S, int KIND, bool X, bool GW>
 __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_t, const typename E::raw* rd,
                                              bool al_d, int tile0, int nt_tiles, int V, float s, const KlNorm& nt,
-                                             const KlNorm& nd, const KlDelta& dr, double (&v)[4]) {
+                                             const KlNorm& nd, const KlDelta& dr, double (&v)[4], float* gr,
+                                             float gcoef, bool vec_g) {
   constexpr int EPV = E::EPV;
+  constexpr int TILE = kThreads * EPV;
   double se = 0.0, sf = 0.0, w = 0.0, xs = 0.0;
   // 2^(z s - zmax s) = e 2^(M - zmax s): the scale of each row's elements against its largest
   float kt = 0.f, kd = 0.f;
@@ -440,12 +456,14 @@ __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_
     for (int j = 0; j < S; ++j) {
       // the EPV elements of one vector are summed in float32, vectors in float64
       float ve = 0.f, vf = 0.f, vw = 0.f, vx = 0.f;
+      float gv[EPV];
 #pragma unroll
       for (int k = 0; k < EPV; ++k) {
         const float tt = fmaf(xt[j][k], s, -nt.M);
         const float uu = fmaf(xd[j][k], s, -nd.M);
         const float e = __builtin_amdgcn_exp2f(tt);
         const float f = __builtin_amdgcn_exp2f(uu);
+        if (GW) gv[k] = kl_fwd_grad<E>(e, f, kl_ratio<E>(xt[j][k], xd[j][k], dr).dl, nt, nd, gcoef);
         float term;
         if (KIND == kKlForward) term = e > 0.f ? e * (tt - uu) : 0.f;
         else if (KIND == kKlCe) term = e > 0.f ? -(e * uu) : 0.f;
@@ -473,12 +491,14 @@ __device__ __forceinline__ void kl_pass_sums(const typename E::raw* rt, bool al_
       sf += static_cast<double>(vf);
       w += static_cast<double>(vw);
       if (KIND == kKlReverse || X) xs += static_cast<double>(vx);
+      if (GW) store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, vec_g, gv);
     }
   }
   v[0] = se; v[1] = sf; v[2] = w; v[3] = xs;
 }
 
-template <class E, int NT, int S, int KIND>
+// S tiles per load step with the pairwise x, SN without it.
+template <class E, int NT, int S, int SN, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
@@ -497,11 +517,21 @@ __global__ __launch_bounds__(kThreads) void kl_pass_kernel(KlArgs a, int64_t nta
     const int tile0 = c * NT;
     const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
     double v[4];
-    // the same for the whole workgroup: one of two loop bodies runs
+    float* gr = a.grad ? a.grad + static_cast<int64_t>(u) * V : nullptr;
+    const float gcoef = static_cast<float>(a.scale * static_cast<double>(a.inv_t) / a.K);
+    // the same for the whole workgroup: one loop body runs.  Forward KL and
+    // CE within the pair limit sum x (kl_grad writes their gradient later);
+    // beyond it the gradient needs nothing but the two normalisers and is
+    // written here, so kl_grad skips the pair.
     if (KIND != kKlReverse && kl_needs_pairwise(nt, nd, a.pair_limit))
-      kl_pass_sums<E, NT, S, KIND, true>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v);
+      kl_pass_sums<E, NT, S, KIND, true, false>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v, gr, gcoef,
+                                                a.vec_g != 0);
+    else if (KIND != kKlReverse && gr)
+      kl_pass_sums<E, NT, SN, KIND, false, true>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v, gr, gcoef,
+                                                 a.vec_g != 0);
     else
-      kl_pass_sums<E, NT, S, KIND, false>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v);
+      kl_pass_sums<E, NT, SN, KIND, false, false>(rt, al_t, rd, al_d, tile0, nt_tiles, V, s, nt, nd, dr, v, gr,
+                                                  gcoef, a.vec_g != 0);
     wg_sum<4>(v, red);
     if (threadIdx.x == 0) {
       KlPart o;
@@ -598,6 +628,7 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
     const typename E::raw* rd = row_of<E>(d, NK + u, &bb, &al_d);
     const float s = scale_of(d.temp_scalar);
     const KlNorm nt = a.norms[u], nd = a.norms[NK + u];
+    if (KIND != kKlReverse && !kl_needs_pairwise(nt, nd, a.pair_limit)) continue;  // written by kl_pass
     KlDelta dr = KIND == kKlReverse ? kl_delta_top(nd, s) : kl_delta_ref(nt, nd, s);
     const float4 A = a.coef[u];
     if (KIND != kKlReverse) kl_delta_set_lam(dr, static_cast<double>(A.x) + static_cast<double>(A.y));
@@ -621,12 +652,8 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
             const float tm = rk.wf - A.y;  // (d - c) - (mu - c)
             gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
           } else {
-            const float dl = rk.dl;
             const float e = __builtin_amdgcn_exp2f(fmaf(xt[j][k], s, -nt.M));
-            const float pe = e * nt.invD, qf = f * nd.invD;
-            const float mx = fmaxf(pe, qf);
-            const float g = kl_absdiff<E>(mx, fminf(pe, qf), dl);
-            gv[k] = mx > 0.f ? gcoef * copysignf(g, dl) : (mx == 0.f ? 0.f : mx);
+            gv[k] = kl_fwd_grad<E>(e, f, rk.dl, nt, nd, gcoef);
           }
         }
         store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
