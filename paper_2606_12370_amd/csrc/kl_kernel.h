@@ -617,11 +617,18 @@ template <class E, int NT, int S, int KIND>
 __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t ntasks) {
   constexpr int EPV = E::EPV;
   constexpr int TILE = kThreads * EPV;
+  // Forward KL / CE: one workgroup per (position, step) pair, its chunks in
+  // turn, since every pair beyond the pair limit leaves at once; reverse
+  // KL: one workgroup per chunk (ntasks of them).
+  constexpr bool kPerPair = KIND != kKlReverse;
   const RowsDesc& d = a.rows;
   const int C = d.C, V = d.V, NK = a.N * a.K;
   const float gcoef = static_cast<float>(a.scale * static_cast<double>(a.inv_t) / a.K);
-  for (int64_t t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int u = static_cast<int>(t / C), c = static_cast<int>(t - static_cast<int64_t>(t / C) * C);
+  const int64_t nitems = kPerPair ? static_cast<int64_t>(NK) : ntasks;
+  for (int64_t it = blockIdx.x; it < nitems; it += gridDim.x) {
+    const int u = kPerPair ? static_cast<int>(it) : static_cast<int>(it / C);
+    const int c0 = kPerPair ? 0 : static_cast<int>(it - static_cast<int64_t>(u) * C);
+    const int c1 = kPerPair ? C : c0 + 1;
     int bb;
     bool al_t, al_d;
     const typename E::raw* rt = row_of<E>(d, u, &bb, &al_t);
@@ -633,30 +640,32 @@ __global__ __launch_bounds__(kThreads) void kl_grad_kernel(KlArgs a, int64_t nta
     const float4 A = a.coef[u];
     if (KIND != kKlReverse) kl_delta_set_lam(dr, static_cast<double>(A.x) + static_cast<double>(A.y));
     float* gr = a.grad + static_cast<int64_t>(u) * V;
-    const int tile0 = c * NT;
-    const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
+    for (int c = c0; c < c1; ++c) {
+      const int tile0 = c * NT;
+      const int nt_tiles = min(NT, (V + TILE - 1) / TILE - tile0);
 #pragma unroll
-    for (int j0 = 0; j0 < NT; j0 += S) {
-      if (j0 >= nt_tiles) break;
-      float xt[S][EPV], xd[S][EPV];
-      load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
-      load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
+      for (int j0 = 0; j0 < NT; j0 += S) {
+        if (j0 >= nt_tiles) break;
+        float xt[S][EPV], xd[S][EPV];
+        load_tiles<E, S>(rt, tile0 + j0, V, al_t, xt);
+        load_tiles<E, S>(rd, tile0 + j0, V, al_d, xd);
 #pragma unroll
-      for (int j = 0; j < S; ++j) {
-        float gv[EPV];
+        for (int j = 0; j < S; ++j) {
+          float gv[EPV];
 #pragma unroll
-        for (int k = 0; k < EPV; ++k) {
-          const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
-          const KlRatio rk = kl_ratio<E>(xt[j][k], xd[j][k], dr);
-          if constexpr (KIND == kKlReverse) {
-            const float tm = rk.wf - A.y;  // (d - c) - (mu - c)
-            gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
-          } else {
-            const float e = __builtin_amdgcn_exp2f(fmaf(xt[j][k], s, -nt.M));
-            gv[k] = kl_fwd_grad<E>(e, f, rk.dl, nt, nd, gcoef);
+          for (int k = 0; k < EPV; ++k) {
+            const float f = __builtin_amdgcn_exp2f(fmaf(xd[j][k], s, -nd.M));
+            const KlRatio rk = kl_ratio<E>(xt[j][k], xd[j][k], dr);
+            if constexpr (KIND == kKlReverse) {
+              const float tm = rk.wf - A.y;  // (d - c) - (mu - c)
+              gv[k] = f > 0.f ? A.x * f * tm : (f == 0.f ? 0.f : f);
+            } else {
+              const float e = __builtin_amdgcn_exp2f(fmaf(xt[j][k], s, -nt.M));
+              gv[k] = kl_fwd_grad<E>(e, f, rk.dl, nt, nd, gcoef);
+            }
           }
+          store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
         }
-        store_grad<EPV>(gr, (tile0 + j0 + j) * TILE + static_cast<int>(threadIdx.x) * EPV, V, a.vec_g != 0, gv);
       }
     }
   }

@@ -492,8 +492,11 @@ spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(sv::kl_coef_kernel, dim3(static_cast<unsigned>((a.N + sv::kWaves - 1) / sv::kWaves)),
                      dim3(sv::kThreads), 0, s, a);
   if (a.grad) {
+    // reverse KL: one workgroup per chunk; forward KL / CE: one per pair (only
+    // the pairs within the pair limit are left to write)
     void (*kg)(sv::KlArgs, int64_t) = sv::kl_grad_kernel<G, NTG, kStep, KIND>;
-    hipLaunchKernelGGL(kg, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a, units * C);
+    const int64_t grid = KIND == sv::kKlReverse ? units * C : units;
+    hipLaunchKernelGGL(kg, dim3(static_cast<unsigned>(grid)), dim3(sv::kThreads), 0, s, a, units * C);
   }
   hipLaunchKernelGGL(sv::kl_loss_kernel, dim3(1), dim3(sv::kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? SPEC_OK : SPEC_EHIP;
