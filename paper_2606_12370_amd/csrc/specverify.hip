@@ -481,10 +481,10 @@ spec_status launch_kl(const sv::KlArgs& a, hipStream_t s) {
   constexpr int NTG = kChunkElems / (sv::kThreads * G::EPV);
   // tiles per load step: 2 for the forward-KL / CE pass with the pairwise x
   // (24.5-24.8 against 25.6-25.8 ms per call), 4 for its loop body without
-  // x (forward KL 21.2-21.4 against 22.4-22.7 ms; 8: 21.0-21.4), kStep for
-  // the reverse-KL one (no difference)
-  constexpr int SP = KIND == sv::kKlReverse ? kStep : 2;
-  constexpr int SPN = kStep;
+  // x (forward KL 21.2-21.4 against 22.4-22.7 ms; 8: 21.0-21.4), 2 for the
+  // reverse-KL pass (21.1-21.2 against 21.3-21.7 ms with 4, 22.5 with 8)
+  constexpr int SP = 2;
+  constexpr int SPN = KIND == sv::kKlReverse ? 2 : kStep;
   void (*kp)(sv::KlArgs, int64_t) = sv::kl_pass_kernel<P, NTP, SP, SPN, KIND>;
   // one workgroup per task (measured faster than a resident grid: reverse KL 22.8 -> 21.2 ms per call)
   hipLaunchKernelGGL(kp, dim3(static_cast<unsigned>(units * C)), dim3(sv::kThreads), 0, s, a,
