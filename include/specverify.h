@@ -35,7 +35,8 @@
  *    (spec_verify: 4, or 3 on its single-read path; spec_tv_loss_fwd_bwd:
  *    5, or 6 with a gradient; spec_verify_target_only: 2, spec_sample: 2,
  *    spec_diagnostics: 4, spec_verify_gumbel: 5, or 4 without overlaps,
- *    spec_sample_gumbel: 2, spec_kl_loss_fwd_bwd: 5, or 6 with a gradient).
+ *    spec_sample_gumbel: 2, spec_kl_loss_fwd_bwd: 5, or 6 with a gradient,
+ *    one more for reverse KL).
  *    Only the single-read path of spec_verify has
  *    workgroups that wait for other workgroups of the same launch; it is a
  *    cooperative launch (all its workgroups resident at once) and every wait
