@@ -152,3 +152,31 @@ def test_training_workload_sampled_positions():
         print(kind, "training workload", rep, "loss", lg)
         del grad
         torch.cuda.empty_cache()
+
+
+def masked_inputs(dtype, seed, N=3, K=2, V=5000):
+    """Logits with a masked vocabulary: the same 5 % of positions and the last
+    37 tokens are -inf in both the target and the draft row (p = q = 0)."""
+    d = W.tv_inputs_numpy(N, K, V, dtype, seed)
+    rng = np.random.default_rng(seed + 1)
+    mask = rng.random((N, K, V)) < 0.05
+    mask[..., V - 37:] = True
+    neg = W.f32_to_bf16_bits(np.array([-np.inf], np.float32))[0] if dtype == W.BF16 else np.float32(-np.inf)
+    for key in ("target", "draft"):
+        arr = d[key].copy()
+        arr[mask] = neg
+        d[key] = arr
+    return d
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("T", [1.0, 0.8])
+def test_masked_vocabulary(dtype, T):
+    d = masked_inputs(dtype, 61 if T == 1.0 else 62)
+    for kind in ("forward", "ce", "reverse"):
+        loss, ps, grad, ref = run_case(d, kind, T)
+        assert np.all(np.isfinite(ref["grad"])) and np.all(np.isfinite(ref["per_step"]))
+        g = grad.cpu().numpy()
+        tm = W.to_float64(d["target"], dtype)
+        assert np.all(g[np.isneginf(tm)] == 0.0)
+        print(kind, dtype, T, compare_kl(loss, ps, grad, ref, dtype))
