@@ -160,13 +160,17 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
         g = g.cpu().numpy().astype(np.float64)
         gr = ref["grad"]
         # relative error bound of q_j from its float32 log-domain evaluation,
-        # which is also the window inside which 1[q <= p] is rounding-decided
-        qerr = TIE_ABS + TIE_REL * ref["tie_condition"]
-        tie = ref["tie_margin"] <= qerr
+        # which is also the window inside which 1[q <= p] is rounding-decided;
+        # where q = 0 (a draft logit of -inf, such as a masked token) the
+        # gradient is exactly 0 and is compared exactly
+        q = ref["q"]
+        live = q > 0
+        with np.errstate(invalid="ignore"):
+            qerr = np.where(live, TIE_ABS + TIE_REL * ref["tie_condition"], 0.0)
+            tie = live & (ref["tie_margin"] <= qerr)
         untied = ~tie
         d = np.where(untied, g - gr, 0.0)
         w = ref["grad_weight"]
-        q = ref["q"]
         s_slack = np.where(tie, q, 0.0).sum(axis=-1)
         num = (d * w).sum(axis=-1)
         den = np.where(untied, w * w, 0.0).sum(axis=-1)

@@ -104,3 +104,25 @@ def test_training_workload_sampled_positions(training_inputs, mode, scale):
     lg = float(loss.cpu().numpy()[0])
     assert abs(lg - sc * L.sum()) <= TOL[W.BF16] * abs(sc * L.sum())
     print("training workload", mode, rep, "loss", lg)
+
+
+@pytest.mark.parametrize("mode", ["e2e", "prod", "per_step"])
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_masked_vocabulary(mode, dtype):
+    """The same 5 % of positions and the last 37 tokens are -inf in both the
+    target and the draft row (p = q = 0): they add nothing to the overlaps
+    and get a zero gradient."""
+    N, K, V = 3, 3, 5000
+    d = W.tv_inputs_numpy(N, K, V, dtype, 71)
+    rng = np.random.default_rng(72)
+    mask = rng.random((N, K, V)) < 0.05
+    mask[..., V - 37:] = True
+    neg = W.f32_to_bf16_bits(np.array([-np.inf], np.float32))[0] if dtype == W.BF16 else np.float32(-np.inf)
+    for key in ("target", "draft"):
+        arr = d[key].copy()
+        arr[mask] = neg
+        d[key] = arr
+    loss, ov, grad, ref = run_case(d, mode, 0.9, scale=0.5)
+    assert np.all(np.isfinite(ref["grad"]))
+    assert np.all(grad.cpu().numpy()[mask] == 0.0)
+    print(mode, dtype, compare_tv(loss, ov, grad, ref, dtype))
