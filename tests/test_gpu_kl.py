@@ -180,3 +180,22 @@ def test_masked_vocabulary(dtype, T):
         tm = W.to_float64(d["target"], dtype)
         assert np.all(g[np.isneginf(tm)] == 0.0)
         print(kind, dtype, T, compare_kl(loss, ps, grad, ref, dtype))
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_target_masked_tokens_forward_and_ce(dtype):
+    """Tokens the target masks (-inf) but the draft does not: p = 0 < q, so
+    they add nothing to forward KL or CE and their gradient is q (reverse KL
+    is infinite there).  Positions with draft noise from 0.003 to 2 put pairs
+    on both sides of the pair limit."""
+    N, K, V = 24, 2, 4000
+    d = W.tv_inputs_numpy(N, K, V, dtype, 81, noise=np.logspace(-2.5, 0.3, N))
+    mask = np.random.default_rng(82).random((N, K, V)) < 0.05
+    neg = W.f32_to_bf16_bits(np.array([-np.inf], np.float32))[0] if dtype == W.BF16 else np.float32(-np.inf)
+    arr = d["target"].copy()
+    arr[mask] = neg
+    d["target"] = arr
+    for kind in ("forward", "ce"):
+        loss, ps, grad, ref = run_case(d, kind, 0.9)
+        assert np.all(np.isfinite(ref["grad"])) and np.all(np.isfinite(ref["per_step"]))
+        print(kind, dtype, compare_kl(loss, ps, grad, ref, dtype))
