@@ -163,11 +163,17 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
         # which is also the window inside which 1[q <= p] is rounding-decided;
         # where q = 0 (a draft logit of -inf, such as a masked token) the
         # gradient is exactly 0 and is compared exactly
+        # where only the target's logit is -inf (p = 0 < q) the indicator is
+        # exact and q's error comes from the draft's terms alone: the row's
+        # largest finite condition bounds them
         q = ref["q"]
         live = q > 0
+        tc = ref["tie_condition"]
+        fin = np.isfinite(tc)
+        tc = np.where(fin, tc, np.where(fin, tc, 0.0).max(axis=-1, keepdims=True))
         with np.errstate(invalid="ignore"):
-            qerr = np.where(live, TIE_ABS + TIE_REL * ref["tie_condition"], 0.0)
-            tie = live & (ref["tie_margin"] <= qerr)
+            qerr = np.where(live, TIE_ABS + TIE_REL * tc, 0.0)
+            tie = live & fin & (ref["tie_margin"] <= qerr)
         untied = ~tie
         d = np.where(untied, g - gr, 0.0)
         w = ref["grad_weight"]

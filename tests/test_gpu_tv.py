@@ -126,3 +126,20 @@ def test_masked_vocabulary(mode, dtype):
     assert np.all(np.isfinite(ref["grad"]))
     assert np.all(grad.cpu().numpy()[mask] == 0.0)
     print(mode, dtype, compare_tv(loss, ov, grad, ref, dtype))
+
+
+@pytest.mark.parametrize("mode", ["e2e", "per_step"])
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_target_masked_tokens(mode, dtype):
+    """Tokens the target masks (-inf) but the draft does not: p = 0 < q, so
+    they add nothing to the overlap and their gradient is -g S q / T."""
+    N, K, V = 3, 3, 5000
+    d = W.tv_inputs_numpy(N, K, V, dtype, 91)
+    mask = np.random.default_rng(92).random((N, K, V)) < 0.05
+    neg = W.f32_to_bf16_bits(np.array([-np.inf], np.float32))[0] if dtype == W.BF16 else np.float32(-np.inf)
+    arr = d["target"].copy()
+    arr[mask] = neg
+    d["target"] = arr
+    loss, ov, grad, ref = run_case(d, mode, 0.9, scale=0.5)
+    assert np.all(np.isfinite(ref["grad"]))
+    print(mode, dtype, compare_tv(loss, ov, grad, ref, dtype))
