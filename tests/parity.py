@@ -186,7 +186,7 @@ def compare_tv(loss_g, ov_g, grad_g, ref, dtype, positions=None, loss_exact=True
         size = np.maximum(np.abs(gr), np.abs(gr - w * dS[..., None]))
         resid = np.abs(d + w * dS[..., None]) - size * qerr
         resid = np.where(untied, np.maximum(resid, 0.0), 0.0).max(axis=-1)
-        scale = np.maximum(np.abs(gr).max(axis=-1), 1e-300)
+        scale = np.maximum(np.abs(gr).max(axis=-1), GRAD_FLOOR)
         worst = float((resid / scale).max())
         assert worst <= tol, "gradient norm-wise relative error %.3e" % worst
         out["max_normwise_grad"] = worst
@@ -375,8 +375,9 @@ KL_ABS = 1e-6
 # The float32 gradient cannot hold the contributions of probabilities below
 # float32's normal range (2^-126; a row's exponentials there underflow), so a
 # row whose exact gradient lies entirely below 2^-100 is measured against
-# 2^-100 rather than against its own largest element.
-KL_GRAD_FLOOR = 2.0 ** -100
+# 2^-100 rather than against its own largest element (TV and CE / KL alike).
+GRAD_FLOOR = 2.0 ** -100
+KL_GRAD_FLOOR = GRAD_FLOOR
 
 
 def compare_kl(loss_g, ps_g, grad_g, ref, dtype, positions=None, loss_exact=True):
