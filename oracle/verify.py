@@ -115,7 +115,10 @@ def verify_ref(target_logits, draft_logits, draft_ids, temperature, seed, offset
       (natural-log partition functions of z/T), and diagnostics used to
       classify boundary draws: u_accept [R, K], ratio [R, K] = p(x)/q(x),
       u_resample [R], resample_margin [R] (distance of u' to the nearest
-      CDF step C/Z bracketing it), zero_mass [R], row_error [R].
+      CDF step C/Z bracketing it), zero_mass [R], row_error [R], and
+      logit_range [R, K]: the larger of the target and draft rows' spans of
+      finite logits over T (the size of the exponent differences that a
+      float32 temperature scale multiplies).
     """
     zt = np.asarray(target_logits, dtype=np.float64)
     zd = np.asarray(draft_logits, dtype=np.float64)
@@ -141,6 +144,13 @@ def verify_ref(target_logits, draft_logits, draft_ids, temperature, seed, offset
         "zero_mass": np.zeros(R, bool),
         "row_error": np.zeros(R, bool),
     }
+    with np.errstate(invalid="ignore", divide="ignore"):
+        def span(z):
+            f = np.isfinite(z)
+            hi = np.where(f, z, -np.inf).max(axis=-1)
+            lo = np.where(f, z, np.inf).min(axis=-1)
+            return np.where(f.any(axis=-1), hi - lo, 0.0)
+        out["logit_range"] = np.maximum(span(zt[:, :K]), span(zd)) / T[:, None]
     words = draw_words(seed, rows, np.arange(K + 1), offset)      # [R, K+1, 4]
     u_acc_all = u24(words[..., 0])
     u_res_all = u24(words[..., 1])

@@ -109,6 +109,11 @@ def verify_inputs_numpy(B, K, V, dtype, gen, seed, shared_target=False, q_equals
     elif gen == "near":
         s = rng.uniform(1.0, 8.0, size=Bg).astype(np.float32)
         sig = rng.uniform(0.01, 0.1, size=Bg).astype(np.float32)
+    elif gen == "wide":
+        # draft noise log-uniform over 0.001-100 per row: from nearly equal
+        # rows to drafts whose logits reach the hundreds
+        s = rng.uniform(1.0, 8.0, size=Bg).astype(np.float32)
+        sig = (10.0 ** rng.uniform(-3.0, 2.0, size=Bg)).astype(np.float32)
     else:
         raise ValueError(gen)
     tgt32 = rng.standard_normal((Bg, K + 1, V), dtype=np.float32) * s[:, None, None]
@@ -119,7 +124,7 @@ def verify_inputs_numpy(B, K, V, dtype, gen, seed, shared_target=False, q_equals
     else:
         noise = rng.standard_normal((Bg, K, V), dtype=np.float32) * sig[:, None, None]
         drf = _store(to_float64(tgt[:, :K], dtype).astype(np.float32) + noise, dtype)
-    if gen in ("rollout_t", "near"):
+    if gen in ("rollout_t", "near", "wide"):
         T = rng.uniform(0.6, 1.2, size=Bg).astype(np.float32)
     else:
         T = np.ones(Bg, np.float32)

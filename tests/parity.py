@@ -89,9 +89,16 @@ def compare_verify(gpu, ref, dtype, rows=None, report=None):
     tol = TOL[dtype]
     max_ov = 0.0
     if "overlap" in gpu:
+        # the kernels scale logits by log2(e) / T rounded to float32 (relative
+        # error up to 2^-23): each term's exponent moves by up to
+        # 2^-23 |z - zbar| / T against the exact scale, so a row whose logits
+        # span more than tol 2^23 T is allowed 2^-23 span / T
         e_ov = rel_err(ov_g[ok], ref["overlap"][ok])
+        allow = np.maximum(tol, 2.0 ** -23 * ref["logit_range"][ok]) if "logit_range" in ref else tol
         max_ov = float(e_ov.max()) if e_ov.size else 0.0
-        assert max_ov <= tol, "overlap relative error %.3e > %.1e" % (max_ov, tol)
+        excess = e_ov - allow
+        assert not np.any(excess > 0), "overlap relative error %.3e > %.1e" % (
+            float(e_ov.flat[np.argmax(excess)]), float(np.broadcast_to(allow, e_ov.shape).flat[np.argmax(excess)]))
     out = {"rows": int(len(acc_r)), "boundary_rows": len(boundary_rows), "max_rel_overlap": max_ov}
     for key in ("p_at_draft", "q_at_draft", "logz_target", "logz_draft"):
         if key in gpu:

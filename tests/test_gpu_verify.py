@@ -140,6 +140,20 @@ def test_masked_vocabularies(dtype):
 
 
 @pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("seed", [51, 52])
+def test_wide_draft_noise(dtype, seed):
+    """Draft noise log-uniform over 0.001-100 per row: from nearly equal rows
+    to drafts whose logits reach the hundreds (one-hot drafts, overlaps down
+    to 1e-30).  Tokens must match; overlaps within the tolerance, or, for rows
+    whose logits span more than tol 2^23 T, within the float32 temperature
+    scale's 2^-23 span / T."""
+    d = W.verify_inputs_numpy(40, 4, 8193, dtype, "wide", seed)
+    out, ref = run_numpy_case(d, seed=seed, offset=5)
+    assert not ref["row_error"].any()
+    print(dtype, compare_verify(out, ref, dtype), "largest span / T", float(ref["logit_range"].max()))
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
 def test_unaligned_strided_views(dtype):
     """Rows that are not 16-byte aligned and non-contiguous batch strides take
     the element-wise load path; results must not change."""
