@@ -64,7 +64,8 @@ def measured_traffic(key, launches_bytes):
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path)).get(key)
+        with open(path) as f:
+            rec = json.load(f).get(key)
     except (OSError, ValueError):
         return None
     if not rec or rec.get("source_hash") != kernel_source_hash():

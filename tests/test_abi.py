@@ -17,8 +17,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "specverify.h")
 
 
+def _header_text():
+    with open(HEADER) as f:
+        return f.read()
+
+
 def header_prototypes():
-    src = open(HEADER).read()
+    src = _header_text()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     protos = {}
     for m in re.finditer(r"\b(?:spec_status|size_t|int|const char\*)\s+(spec_\w+)\s*\(([^;]*?)\)\s*;", src, re.S):
@@ -65,7 +70,7 @@ def test_ctypes_prototypes_match_header():
 
 
 def test_diag_columns_match_header():
-    src = open(HEADER).read()
+    src = _header_text()
     cols = re.findall(r"SPEC_DIAG_(\w+) = (\d+)", src)
     named = {name.lower(): int(v) for name, v in cols}
     assert named.pop("ncols") == len(binding.DIAG_COLUMNS)
@@ -75,7 +80,7 @@ def test_diag_columns_match_header():
 
 
 def test_version_and_status_strings(lib):
-    ver = int(re.search(r"#define SPEC_VERSION (\d+)", open(HEADER).read()).group(1))
+    ver = int(re.search(r"#define SPEC_VERSION (\d+)", _header_text()).group(1))
     assert lib.spec_version() == ver
     for code in (0, 1, 2, 4, 5):
         assert lib.spec_status_string(code)
@@ -119,7 +124,7 @@ def test_workspace_sizes(lib):
 def test_vocabulary_limit(lib):
     """V up to SPEC_MAX_V = 2^31 - 2^16 is accepted (element indices, 32-bit,
     run one 16384-element chunk past V); one more is rejected everywhere."""
-    max_v = int(re.search(r"#define SPEC_MAX_V (\d+)", open(HEADER).read()).group(1))
+    max_v = int(re.search(r"#define SPEC_MAX_V (\d+)", _header_text()).group(1))
     assert max_v == (1 << 31) - (1 << 16)
     for V, ok in ((max_v, True), (max_v + 1, False)):
         for dt in (0, 1):
